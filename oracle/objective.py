@@ -1,0 +1,142 @@
+"""The RL objective on top of per-token log-probs, fp64.
+
+Follows the paper's RL section in its order:
+
+  Eq. 4   importance ratio rho_t = pi_theta / pi_rollout, formed in log space:
+          ell_t = logp_t - logp_rollout_t, rho_t = exp(ell_t)
+  Eq. 19  mirror deviation m_t = max(rho_t, 1/rho_t) = exp|ell_t|
+  Eq. 20  MirrorPop statistic: log of the length-normalised geometric mean of
+          m, i.e. S_i = (1/L_i) sum_t |ell_t|
+  Eq. 21  M_i = 1[S_i <= delta]
+  Eq. 18  the signed ("vanilla") statistic (1/L_i) sum_t ell_t, reported as a
+          diagnostic and usable as the filter instead
+  Eq. 3   (and Eq. 12 for trajectory rewards) A_i = (r_i - mean_g r) / (std_g r + eps)
+  Eq. 17  loss = -(1/sum_i M_i L_i) sum_i sum_t min(rho A_i, clip(rho, 1-eps_low,
+          1+eps_high) A_i) M_i          (KL weight beta = 0)
+
+Readings where the paper is silent or leaves a choice (each a parameter or
+a convention; the paper prints no number that pins them):
+
+  R1  natural logarithm throughout.
+  R2  L_i counts the tokens of sequence i whose loss_mask is set (the loss is
+      taken on first-turn tokens only); the same mask drives Eq. 18, 20, 21
+      and 17.
+  R3  L_i = 0: M_i = 0 and both statistics are 0; the sequence contributes
+      nothing.
+  R4  delta is a parameter (default 0.1 nats); the comparison is inclusive.
+  R5  eps_low and eps_high are separate parameters (default 0.2 each).
+  R6  std in Eq. 3 is the population standard deviation (ddof 0, a
+      parameter) over all sequences of the group, whatever their M_i;
+      eps defaults to 1e-6.  A group of one sequence has A = 0.
+  R7  several groups in one batch: one global token mean,
+      N = sum over all sequences of M_i L_i (reduces to Eq. 17 for one group).
+  R8  N = 0: loss 0 and zero gradient.
+  R9  gradient at a clip kink: the unclipped branch is taken when
+      rho A <= clip(rho) A (ties count as unclipped); the clipped branch has
+      zero gradient.  No gradient flows through M_i, S_i or A_i.
+  R10 the filter "none" keeps every sequence with L_i > 0 (plain Eq. 5).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+FILTERS = ("none", "vanilla", "mirrorpop")
+
+
+@dataclasses.dataclass
+class RLParams:
+    eps_low: float = 0.2
+    eps_high: float = 0.2
+    delta: float = 0.1
+    adv_eps: float = 1e-6
+    std_ddof: int = 0
+    filter: str = "mirrorpop"
+
+
+def _advantages(rewards, cu_groups, p: RLParams) -> np.ndarray:
+    """Eq. 3 / Eq. 12: group-normalised advantage of each sequence."""
+    A = np.zeros(len(rewards), dtype=np.float64)
+    for g in range(len(cu_groups) - 1):
+        a, b = int(cu_groups[g]), int(cu_groups[g + 1])
+        r = np.asarray(rewards[a:b], dtype=np.float64)
+        n = b - a
+        if n == 0:
+            continue
+        mean = r.sum() / n
+        dof = n - p.std_ddof
+        var = ((r - mean) ** 2).sum() / dof if dof > 0 else 0.0
+        A[a:b] = (r - mean) / (math.sqrt(var) + p.adv_eps)
+    return A
+
+
+def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
+            params: RLParams | None = None) -> dict:
+    p = params or RLParams()
+    if p.filter not in FILTERS:
+        raise ValueError(p.filter)
+    logp = np.asarray(logp, dtype=np.float64)
+    logp_rollout = np.asarray(logp_rollout, dtype=np.float64)
+    T = len(logp)
+    mask = (np.ones(T, dtype=bool) if loss_mask is None
+            else np.asarray(loss_mask).astype(bool))
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    B = len(cu) - 1
+
+    # Eq. 4 in log space (masked tokens may hold anything in logp_rollout).
+    ell = np.where(mask, logp - np.where(mask, logp_rollout, 0.0), 0.0)
+    rho = np.exp(ell)
+
+    seq_len = np.zeros(B, dtype=np.int64)
+    stat_abs = np.zeros(B, dtype=np.float64)
+    stat_signed = np.zeros(B, dtype=np.float64)
+    keep = np.zeros(B, dtype=bool)
+    for i in range(B):
+        s, e = cu[i], cu[i + 1]
+        valid = mask[s:e]
+        L = int(valid.sum())
+        seq_len[i] = L
+        if L == 0:
+            continue                                      # R3
+        stat_abs[i] = np.abs(ell[s:e][valid]).sum() / L   # Eq. 20 (log space)
+        stat_signed[i] = ell[s:e][valid].sum() / L        # Eq. 18 (log space)
+        if p.filter == "mirrorpop":
+            keep[i] = stat_abs[i] <= p.delta              # Eq. 21
+        elif p.filter == "vanilla":
+            keep[i] = abs(stat_signed[i]) <= p.delta
+        else:
+            keep[i] = True
+
+    A = _advantages(rewards, cu_groups, p)
+    N = int((seq_len * keep).sum())
+
+    lo, hi = 1.0 - p.eps_low, 1.0 + p.eps_high
+    dlogp = np.zeros(T, dtype=np.float64)
+    total = 0.0
+    n_clipped = 0
+    for i in range(B):
+        if not keep[i]:
+            continue
+        s, e = cu[i], cu[i + 1]
+        for t in range(s, e):
+            if not mask[t]:
+                continue
+            unclipped = rho[t] * A[i]
+            clipped = min(max(rho[t], lo), hi) * A[i]
+            total += min(unclipped, clipped)
+            if unclipped <= clipped:                      # R9
+                dlogp[t] = unclipped                      # d(rho A)/d ell = rho A
+            else:
+                n_clipped += 1
+    if N > 0:
+        loss = -total / N
+        dlogp *= -1.0 / N
+        clip_frac = n_clipped / N
+    else:                                                 # R8
+        loss, clip_frac = 0.0, 0.0
+        dlogp[:] = 0.0
+    return dict(loss=loss, dlogp=dlogp, seq_mask=keep.astype(np.uint8),
+                seq_len=seq_len.astype(np.int32), n_valid=N, adv=A,
+                stat_abs=stat_abs, stat_signed=stat_signed, clip_frac=clip_frac)
