@@ -1,0 +1,199 @@
+/*
+ * mc.h -- C ABI of the fused RL log-prob library (libmc.so) for AMD MI355X
+ * (gfx950).
+ *
+ * The library computes, on one GPU:
+ *   - the trainer-side per-token log-probability log pi_theta(o_t | x, o_<t)
+ *     over the full vocabulary (the numerator of the importance ratio of
+ *     Eq. 4): logits z = hidden . weight^T are reduced in the GEMM epilogue by
+ *     an online log-sum-exp and a gather of the target logit, and are never
+ *     written to memory;
+ *   - its backward (chain rule through the log-softmax);
+ *   - the RL objective on top of it: log importance ratios (Eq. 4), the
+ *     MirrorPop sequence statistic and mask (Eq. 19-21) or the signed one
+ *     (Eq. 18), group-normalised advantages (Eq. 3 / Eq. 12) and the
+ *     sequence-masked clipped surrogate (Eq. 17 with the KL weight beta = 0),
+ *     with its gradient with respect to the per-token log-probs.
+ *
+ * Conventions shared by every entry point
+ *   Memory      Every array argument is caller-owned DEVICE memory unless a
+ *               comment says "host".  The library allocates nothing and keeps
+ *               no pointer after a call returns.
+ *   Workspace   Each entry point takes a device workspace of at least the size
+ *               its *_workspace_size query returns, aligned to 256 bytes.  Its
+ *               contents on entry do not matter; on return they are undefined.
+ *   Streams     `stream` is a hipStream_t (NULL = the default stream).  Work is
+ *               enqueued on it and the call returns without waiting; buffers
+ *               must stay valid until the stream has finished the work.
+ *   Layout      Matrices are row-major and contiguous, 16-byte aligned.
+ *               d must be a multiple of 8.
+ *   Errors      Scalar and pointer arguments are checked on the host before any
+ *               launch; a bad argument returns an error code and enqueues
+ *               nothing.  A launch failure returns MC_ERR_HIP.  No exception or
+ *               abort crosses the ABI.
+ *   Threads     Re-entrant; no mutable global state apart from the opt-in
+ *               profiler at the end of this header.
+ *   Determinism Results are bit-identical from run to run for the same
+ *               inputs, shapes and device: no floating-point atomics are used.
+ */
+#ifndef MC_H_
+#define MC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MC_OK = 0,
+  MC_ERR_INVALID_ARG = 1,   /* null pointer, negative size, bad parameter */
+  MC_ERR_UNSUPPORTED = 2,   /* valid but not supported (d % 8 != 0, dtype) */
+  MC_ERR_WORKSPACE = 3,     /* workspace too small or misaligned */
+  MC_ERR_HIP = 4            /* a HIP launch or runtime call failed */
+} mc_status_t;
+
+typedef enum {
+  MC_F32 = 0,               /* fp32 hidden/weight, fp32 MFMA */
+  MC_BF16 = 1               /* bf16 hidden/weight, bf16 MFMA, fp32 accumulate */
+} mc_dtype_t;
+
+typedef enum {
+  MC_FILTER_NONE = 0,       /* keep every sequence with a valid token (Eq. 5) */
+  MC_FILTER_VANILLA = 1,    /* |(1/L_i) sum_t log rho_t| <= delta (Eq. 18) */
+  MC_FILTER_MIRRORPOP = 2   /* (1/L_i) sum_t |log rho_t| <= delta (Eq. 21) */
+} mc_filter_t;
+
+/* Parameters of the objective (host struct). */
+typedef struct {
+  float eps_low;            /* lower clip width of Eq. 5/17; ratio >= 1-eps_low, 0 <= eps_low < 1 */
+  float eps_high;           /* upper clip width; ratio <= 1+eps_high, eps_high >= 0 */
+  float delta;              /* filter threshold in log-ratio space (Eq. 21), >= 0 */
+  float adv_eps;            /* epsilon added to the group std (Eq. 3), >= 0 */
+  int32_t std_ddof;         /* 0: population std, 1: sample std */
+  int32_t filter;           /* an mc_filter_t */
+} mc_rl_params_t;
+
+/* Outputs of mc_rl_loss (host struct holding device pointers).  `loss` and
+ * `dlogp` are required; any other member may be NULL. */
+typedef struct {
+  float* loss;              /* [1]  -(1/N) sum_i M_i sum_t min(rho A_i, clip(rho) A_i) */
+  float* dlogp;             /* [T]  d loss / d logp_t */
+  uint8_t* seq_mask;        /* [B]  M_i */
+  int32_t* seq_len;         /* [B]  L_i = number of loss-mask tokens of sequence i */
+  int64_t* n_valid;         /* [1]  N = sum_i M_i L_i */
+  float* adv;               /* [B]  A_i */
+  float* stat_abs;          /* [B]  (1/L_i) sum_t |log rho_t|  (log of Eq. 20's statistic) */
+  float* stat_signed;       /* [B]  (1/L_i) sum_t log rho_t    (log of Eq. 18's statistic) */
+  float* clip_frac;         /* [1]  share of the N tokens on the clipped branch */
+  int32_t* error_flag;      /* [1]  set to 1 when cu_seqlens/cu_groups are inconsistent */
+} mc_rl_outputs_t;
+
+/* Flags of mc_logprob_bwd. */
+#define MC_BWD_ACCUMULATE_DHIDDEN 1   /* dhidden += gradient instead of = */
+#define MC_BWD_ACCUMULATE_DWEIGHT 2   /* dweight += gradient instead of = */
+
+/* Human-readable name of a status code (static string). */
+const char* mc_status_string(mc_status_t status);
+
+/* Library version string (static). */
+const char* mc_version(void);
+
+/* ------------------------------------------------------------------------
+ * Forward: per-token log-prob over the full vocabulary.
+ *   logp[t] = z[t, y_t] - lse[t],  lse[t] = log sum_v exp(z[t, v]),
+ *   z = hidden . weight^T,
+ * i.e. log pi_theta(o_t | x, o_<t) of Eq. 4, for the token y_t the rollout
+ * sampled at row t (the caller applies the next-token shift).
+ *   hidden   [T, d]  dtype         activations entering the LM head
+ *   weight   [V, d]  dtype         LM-head weight (one row per vocabulary entry)
+ *   targets  [T]     int64         y_t; a value outside [0, V) marks an ignored
+ *                                  token: logp = 0 there and it gets no gradient
+ *   logp     [T]     fp32 (out)
+ *   lse      [T]     fp32 (out)    kept for the backward
+ * T = 0 is a valid no-op.  T >= 0, d >= 8, d % 8 == 0, V >= 1.
+ * ------------------------------------------------------------------------ */
+size_t mc_logprob_fwd_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dtype);
+mc_status_t mc_logprob_fwd(const void* hidden, const void* weight, const int64_t* targets,
+                           int64_t T, int64_t d, int64_t V, mc_dtype_t dtype,
+                           float* logp, float* lse,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Backward of the forward above for an upstream gradient dlogp[t]:
+ *   G[t, v]  = dlogp_t (1[v = y_t] - exp(z[t, v] - lse_t))   (0 for ignored t)
+ *   dhidden  = G . weight      [T, d] fp32
+ *   dweight  = G^T . hidden    [V, d] fp32
+ *   lse      [T] fp32          as returned by mc_logprob_fwd for the same inputs
+ *   dlogp    [T] fp32
+ *   dhidden / dweight may be NULL to skip that gradient (not both).
+ *   flags    MC_BWD_ACCUMULATE_* bits: accumulate into the outputs.
+ * The softmax part is formed per vocabulary chunk as a transient operand
+ * (dtype) in the workspace; logits are recomputed, never stored.
+ * ------------------------------------------------------------------------ */
+size_t mc_logprob_bwd_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dtype);
+mc_status_t mc_logprob_bwd(const void* hidden, const void* weight, const int64_t* targets,
+                           const float* lse, const float* dlogp,
+                           int64_t T, int64_t d, int64_t V, mc_dtype_t dtype,
+                           float* dhidden, float* dweight, int32_t flags,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * RL objective over a packed ragged batch (Eq. 3/12, 4, 17-21; beta = 0).
+ *   logp          [T]    fp32   trainer log-probs (from mc_logprob_fwd)
+ *   logp_rollout  [T]    fp32   rollout log-probs of the same tokens
+ *                               (ignored where loss_mask is 0)
+ *   loss_mask     [T]    u8     1 = token counts (e.g. first-turn response
+ *                               tokens); NULL = all tokens count
+ *   cu_seqlens    [B+1]  int32  sequence i is rows [cu_seqlens[i], cu_seqlens[i+1]);
+ *                               cu_seqlens[0] = 0, non-decreasing, cu_seqlens[B] = T
+ *   cu_groups     [NG+1] int32  group g is sequences [cu_groups[g], cu_groups[g+1]);
+ *                               cu_groups[0] = 0, non-decreasing, cu_groups[NG] = B
+ *   rewards       [B]    fp32   r_i (or a trajectory reward, Eq. 9)
+ * The loss is one token mean over the whole batch, N = sum_i M_i L_i; N = 0
+ * gives loss 0 and dlogp 0.  A sequence with L_i = 0 has M_i = 0.  The packing
+ * arrays live on the device and are checked there: inconsistent values never
+ * cause an out-of-bounds access; they set *error_flag (when given) and the
+ * outputs are then unspecified.  mc_check_packing validates host copies.
+ * ------------------------------------------------------------------------ */
+size_t mc_rl_loss_workspace_size(int64_t T, int32_t B, int32_t NG);
+mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const uint8_t* loss_mask,
+                       const int32_t* cu_seqlens, const int32_t* cu_groups,
+                       const float* rewards, int64_t T, int32_t B, int32_t NG,
+                       const mc_rl_params_t* params, const mc_rl_outputs_t* out,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Host-side check of packing metadata (host arrays): MC_OK when cu_seqlens and
+ * cu_groups satisfy the rules stated for mc_rl_loss, MC_ERR_INVALID_ARG
+ * otherwise.  Makes no HIP call. */
+mc_status_t mc_check_packing(const int32_t* cu_seqlens_host, int32_t B,
+                             const int32_t* cu_groups_host, int32_t NG, int64_t T);
+
+/* ------------------------------------------------------------------------
+ * Per-kernel timing, a measurement aid (the one piece of global state).
+ * mc_profiler_enable(1) makes every later launch record a pair of hipEvents
+ * on its own stream, tagged with the kernel name and its algorithmic FLOPs
+ * and bytes (what the method must compute and move, not what the
+ * implementation moves).  mc_profiler_read waits for the recorded events,
+ * adds them into per-name totals and copies up to `cap` totals into `out`
+ * (host array); it returns the number of names.  mc_profiler_reset clears
+ * the totals.  Thread-safe; enabling costs one event pair per launch.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  char name[48];
+  int64_t launches;
+  double total_ms;
+  double total_flops;
+  double total_bytes;
+} mc_kernel_time_t;
+
+void mc_profiler_enable(int32_t on);
+void mc_profiler_reset(void);
+int32_t mc_profiler_read(mc_kernel_time_t* out, int32_t cap);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MC_H_ */

@@ -27,7 +27,9 @@ a convention; the paper prints no number that pins them):
   R5  eps_low and eps_high are separate parameters (default 0.2 each).
   R6  std in Eq. 3 is the population standard deviation (ddof 0, a
       parameter) over all sequences of the group, whatever their M_i;
-      eps defaults to 1e-6.  A group of one sequence has A = 0.
+      eps defaults to 1e-6.  A group whose rewards are all equal (this
+      includes a group of one sequence and the all-failed group of Eq. 13)
+      has A = 0 exactly, also when eps = 0.
   R7  several groups in one batch: one global token mean,
       N = sum over all sequences of M_i L_i (reduces to Eq. 17 for one group).
   R8  N = 0: loss 0 and zero gradient.
@@ -65,6 +67,8 @@ def _advantages(rewards, cu_groups, p: RLParams) -> np.ndarray:
         n = b - a
         if n == 0:
             continue
+        if np.all(r == r[0]):
+            continue                                       # R6: equal rewards
         mean = r.sum() / n
         dof = n - p.std_ddof
         var = ((r - mean) ** 2).sum() / dof if dof > 0 else 0.0

@@ -1,0 +1,152 @@
+// extern "C" entry points of libmc.so: argument validation on the host (no
+// HIP call on any error path), workspace checks, then the launches.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "mc_internal.hpp"
+
+namespace {
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+constexpr int64_t kMaxDim = (int64_t(1) << 31) - 1;
+
+mc_status_t check_dims(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
+  if (T < 0 || d < 1 || V < 1) return MC_ERR_INVALID_ARG;
+  if (dt != MC_F32 && dt != MC_BF16) return MC_ERR_UNSUPPORTED;
+  if (d % 8 != 0) return MC_ERR_UNSUPPORTED;
+  if (T > kMaxDim || V > kMaxDim - 256 || d > kMaxDim) return MC_ERR_UNSUPPORTED;
+  // one launch must stay below 2^31 workgroups
+  if (mc::cdiv(T, 256) * mc::cdiv(V, 256) > kMaxDim) return MC_ERR_UNSUPPORTED;
+  return MC_OK;
+}
+
+mc_status_t check_ws(void* ws, size_t bytes, size_t need) {
+  if (need == 0) return MC_OK;
+  if (ws == nullptr || bytes < need || !aligned(ws, mc::kWsAlign)) return MC_ERR_WORKSPACE;
+  return MC_OK;
+}
+
+mc_status_t from_hip(hipError_t e) { return e == hipSuccess ? MC_OK : MC_ERR_HIP; }
+
+bool finite(float x) { return std::isfinite(x); }
+
+}  // namespace
+
+extern "C" {
+
+const char* mc_status_string(mc_status_t s) {
+  switch (s) {
+    case MC_OK: return "MC_OK";
+    case MC_ERR_INVALID_ARG: return "MC_ERR_INVALID_ARG";
+    case MC_ERR_UNSUPPORTED: return "MC_ERR_UNSUPPORTED";
+    case MC_ERR_WORKSPACE: return "MC_ERR_WORKSPACE";
+    case MC_ERR_HIP: return "MC_ERR_HIP";
+  }
+  return "MC_ERR_UNKNOWN";
+}
+
+const char* mc_version(void) { return "mc 0.1.0 gfx950"; }
+
+size_t mc_logprob_fwd_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
+  if (check_dims(T, d, V, dt) != MC_OK) return 0;
+  return mc::fwd_workspace(T, d, V, dt);
+}
+
+mc_status_t mc_logprob_fwd(const void* hidden, const void* weight, const int64_t* targets,
+                           int64_t T, int64_t d, int64_t V, mc_dtype_t dt, float* logp,
+                           float* lse, void* ws, size_t ws_bytes, void* stream) {
+  mc_status_t st = check_dims(T, d, V, dt);
+  if (st != MC_OK) return st;
+  if (T == 0) return MC_OK;
+  if (!hidden || !weight || !targets || !logp || !lse) return MC_ERR_INVALID_ARG;
+  if (!aligned(hidden, 16) || !aligned(weight, 16) || !aligned(targets, 8) ||
+      !aligned(logp, 4) || !aligned(lse, 4))
+    return MC_ERR_INVALID_ARG;
+  st = check_ws(ws, ws_bytes, mc::fwd_workspace(T, d, V, dt));
+  if (st != MC_OK) return st;
+  return from_hip(mc::launch_fwd(hidden, weight, targets, T, d, V, dt, logp, lse, ws,
+                                 static_cast<hipStream_t>(stream)));
+}
+
+size_t mc_logprob_bwd_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
+  if (check_dims(T, d, V, dt) != MC_OK) return 0;
+  return mc::bwd_workspace(T, d, V, dt);
+}
+
+mc_status_t mc_logprob_bwd(const void* hidden, const void* weight, const int64_t* targets,
+                           const float* lse, const float* dlogp, int64_t T, int64_t d, int64_t V,
+                           mc_dtype_t dt, float* dhidden, float* dweight, int32_t flags,
+                           void* ws, size_t ws_bytes, void* stream) {
+  mc_status_t st = check_dims(T, d, V, dt);
+  if (st != MC_OK) return st;
+  if (flags & ~(MC_BWD_ACCUMULATE_DHIDDEN | MC_BWD_ACCUMULATE_DWEIGHT)) return MC_ERR_INVALID_ARG;
+  if (!dhidden && !dweight) return MC_ERR_INVALID_ARG;
+  if (!hidden || !weight) return MC_ERR_INVALID_ARG;
+  if (!aligned(hidden, 16) || !aligned(weight, 16) || (dhidden && !aligned(dhidden, 16)) ||
+      (dweight && !aligned(dweight, 16)))
+    return MC_ERR_INVALID_ARG;
+  if (T == 0) {
+    // no tokens: dhidden is empty; dweight receives a zero gradient
+    if (dweight && !(flags & MC_BWD_ACCUMULATE_DWEIGHT))
+      return from_hip(hipMemsetAsync(dweight, 0, size_t(V) * size_t(d) * sizeof(float),
+                                     static_cast<hipStream_t>(stream)));
+    return MC_OK;
+  }
+  if (!targets || !lse || !dlogp) return MC_ERR_INVALID_ARG;
+  if (!aligned(targets, 8) || !aligned(lse, 4) || !aligned(dlogp, 4)) return MC_ERR_INVALID_ARG;
+  st = check_ws(ws, ws_bytes, mc::bwd_workspace(T, d, V, dt));
+  if (st != MC_OK) return st;
+  return from_hip(mc::launch_bwd(hidden, weight, targets, lse, dlogp, T, d, V, dt, dhidden,
+                                 dweight, flags, ws, static_cast<hipStream_t>(stream)));
+}
+
+size_t mc_rl_loss_workspace_size(int64_t T, int32_t B, int32_t NG) {
+  if (T < 0 || B < 0 || NG < 0) return 0;
+  return mc::loss_workspace(T, B, NG);
+}
+
+mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const uint8_t* loss_mask,
+                       const int32_t* cu_seqlens, const int32_t* cu_groups, const float* rewards,
+                       int64_t T, int32_t B, int32_t NG, const mc_rl_params_t* params,
+                       const mc_rl_outputs_t* out, void* ws, size_t ws_bytes, void* stream) {
+  if (T < 0 || B < 0 || NG < 0 || T > kMaxDim) return MC_ERR_INVALID_ARG;
+  if (!params || !out || !out->loss) return MC_ERR_INVALID_ARG;
+  if (B == 0 && T > 0) return MC_ERR_INVALID_ARG;   // tokens outside every sequence
+  if (NG == 0 && B > 0) return MC_ERR_INVALID_ARG;  // sequences outside every group
+  const mc_rl_params_t& p = *params;
+  if (!finite(p.eps_low) || !finite(p.eps_high) || !finite(p.delta) || !finite(p.adv_eps))
+    return MC_ERR_INVALID_ARG;
+  if (p.eps_low < 0.0f || p.eps_low >= 1.0f || p.eps_high < 0.0f || p.delta < 0.0f ||
+      p.adv_eps < 0.0f)
+    return MC_ERR_INVALID_ARG;
+  if (p.std_ddof != 0 && p.std_ddof != 1) return MC_ERR_INVALID_ARG;
+  if (p.filter != MC_FILTER_NONE && p.filter != MC_FILTER_VANILLA &&
+      p.filter != MC_FILTER_MIRRORPOP)
+    return MC_ERR_INVALID_ARG;
+  if (!cu_seqlens || !cu_groups || (B > 0 && !rewards)) return MC_ERR_INVALID_ARG;
+  if (T > 0 && (!logp || !logp_rollout || !out->dlogp)) return MC_ERR_INVALID_ARG;
+  if (!aligned(cu_seqlens, 4) || !aligned(cu_groups, 4) || !aligned(out->loss, 4) ||
+      (out->n_valid && !aligned(out->n_valid, 8)))
+    return MC_ERR_INVALID_ARG;
+  mc_status_t st = check_ws(ws, ws_bytes, mc::loss_workspace(T, B, NG));
+  if (st != MC_OK) return st;
+  return from_hip(mc::launch_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
+                                  T, B, NG, p, *out, ws, static_cast<hipStream_t>(stream)));
+}
+
+mc_status_t mc_check_packing(const int32_t* cu, int32_t B, const int32_t* cg, int32_t NG,
+                             int64_t T) {
+  if (!cu || !cg || B < 0 || NG < 0 || T < 0) return MC_ERR_INVALID_ARG;
+  if (cu[0] != 0 || int64_t(cu[B]) != T) return MC_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < B; ++i)
+    if (cu[i + 1] < cu[i]) return MC_ERR_INVALID_ARG;
+  if (cg[0] != 0 || cg[NG] != B) return MC_ERR_INVALID_ARG;
+  for (int32_t g = 0; g < NG; ++g)
+    if (cg[g + 1] < cg[g]) return MC_ERR_INVALID_ARG;
+  return MC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,493 @@
+// Fused LM-head log-prob on gfx950: forward (GEMM + online log-sum-exp +
+// target gather in the epilogue), the partial merge, and the backward
+// (recomputed logits -> scaled softmax operand -> two contractions, plus the
+// exact one-hot terms in fp32).
+#include <hip/hip_runtime.h>
+
+#include "mc_internal.hpp"
+#include "mc_tile.hpp"
+
+namespace mc {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegInf = -__builtin_huge_valf();
+
+__device__ __forceinline__ float half_max(float x) {
+#pragma unroll
+  for (int m = 16; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m));
+  return x;
+}
+__device__ __forceinline__ float half_sum(float x) {
+#pragma unroll
+  for (int m = 16; m >= 1; m >>= 1) x += __shfl_xor(x, m);
+  return x;
+}
+
+// ---------------------------------------------------------------------------
+// Forward epilogue.  For each of the tile's 256 rows: max and sum of exp over
+// the tile's valid columns -> one (m, s) partial per (vocab tile, row); the
+// target logit z[t, y_t] is written by the one lane that holds it.
+// ---------------------------------------------------------------------------
+struct EpiFwd {
+  const int64_t* y;
+  int64_t T, V;
+  float* part_m;   // [nTn][T]
+  float* part_s;   // [nTn][T]
+  float* zy;       // [T]: receives z[t, y_t]
+  static constexpr int kLdsExtra = 256 * 4 + 4 * 256 * 4;
+
+  __device__ void prologue(int64_t m0, int64_t, char* extra) const {
+    int* ys = reinterpret_cast<int*>(extra);
+    const int64_t t = m0 + threadIdx.x;
+    int v = -1;
+    if (t < T) {
+      const int64_t yy = y[t];
+      if (yy >= 0 && yy < V) v = int(yy);
+    }
+    ys[threadIdx.x] = v;
+  }
+
+  __device__ void epilogue(f32x16 (&acc)[4][4], int, int tn, int64_t m0, int64_t n0, char*,
+                           char* extra) const {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    const int* ys = reinterpret_cast<const int*>(extra);
+    float* red = reinterpret_cast<float*>(extra + 1024);   // [m|s][wn][row]
+    const int cbase = int(n0) + wn * 128;
+    const int vlim = int(min<int64_t>(V - cbase, 128));    // valid columns of this wave
+    const int cl = lane & 31;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = acc_row(wm, i, e, lane);
+        float mx = kNegInf;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (j * 32 + cl < vlim) mx = fmaxf(mx, acc[i][j][e]);
+        mx = half_max(mx);
+        float s = 0.0f;
+        const float mb = mx * kLog2e;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (j * 32 + cl < vlim) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
+        s = half_sum(s);
+        const int yl = ys[r] - cbase;
+        if (yl >= 0 && yl < 128 && (yl & 31) == cl) {
+          const int jj = yl >> 5;
+          float z = acc[i][0][e];
+          z = jj == 1 ? acc[i][1][e] : z;
+          z = jj == 2 ? acc[i][2][e] : z;
+          z = jj == 3 ? acc[i][3][e] : z;
+          zy[m0 + r] = z;
+        }
+        if (cl == 0) {
+          red[(0 * 2 + wn) * 256 + r] = mx;
+          red[(1 * 2 + wn) * 256 + r] = s;
+        }
+      }
+    }
+    __syncthreads();
+    const int r = tid;
+    const int64_t t = m0 + r;
+    if (t < T) {
+      const float ma = red[r], mb = red[256 + r];
+      const float sa = red[512 + r], sb = red[768 + r];
+      const float M = fmaxf(ma, mb);
+      float S = sa * __builtin_amdgcn_exp2f((ma - M) * kLog2e);
+      if (mb != kNegInf) S += sb * __builtin_amdgcn_exp2f((mb - M) * kLog2e);
+      part_m[int64_t(tn) * T + t] = M;
+      part_s[int64_t(tn) * T + t] = S;
+    }
+  }
+};
+
+// Merge of the per-vocab-tile partials, in tile order: lse = m + log s and
+// logp = z_y - lse (0 for ignored targets).  64 rows per block, 8 waves
+// stride over the tiles, then wave 0 folds the 8 running pairs in order.
+__global__ __launch_bounds__(512) void k_lse_merge(const float* __restrict__ pm,
+                                                   const float* __restrict__ ps, int nT,
+                                                   int64_t T, const int64_t* __restrict__ y,
+                                                   int64_t V, float* __restrict__ logp,
+                                                   float* __restrict__ lse) {
+  __shared__ float sm[8][64], ss[8][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t t = int64_t(blockIdx.x) * 64 + lane;
+  float M = kNegInf, S = 0.0f;
+  if (t < T) {
+    for (int j = w; j < nT; j += 8) {
+      const float m = pm[int64_t(j) * T + t], s = ps[int64_t(j) * T + t];
+      if (m > M) {
+        S = S * expf(M - m) + s;
+        M = m;
+      } else {
+        S += s * expf(m - M);
+      }
+    }
+  }
+  sm[w][lane] = M;
+  ss[w][lane] = S;
+  __syncthreads();
+  if (w == 0 && t < T) {
+    M = sm[0][lane];
+    S = ss[0][lane];
+    for (int k = 1; k < 8; ++k) {
+      const float m = sm[k][lane], s = ss[k][lane];
+      if (m == kNegInf) continue;
+      if (m > M) {
+        S = S * expf(M - m) + s;
+        M = m;
+      } else {
+        S += s * expf(m - M);
+      }
+    }
+    const float l = M + logf(S);
+    lse[t] = l;
+    const int64_t yy = y[t];
+    logp[t] = (yy >= 0 && yy < V) ? logp[t] - l : 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward, step 1: recompute the logits of a vocabulary chunk and write the
+// transient operand P~[t, v] = -dlogp_t exp(z_tv - lse_t) (zero for ignored
+// rows and for the padding columns [chunk, ld)).
+// ---------------------------------------------------------------------------
+template <typename T>
+struct EpiProbs {
+  const int64_t* y;
+  const float* lse;
+  const float* dlogp;
+  int64_t Tn, V, width, ld;
+  T* P;
+  static constexpr int kLdsExtra = 2 * 256 * 4;
+
+  __device__ void prologue(int64_t m0, int64_t, char* extra) const {
+    float* l2 = reinterpret_cast<float*>(extra);
+    float* g = l2 + 256;
+    const int64_t t = m0 + threadIdx.x;
+    float a = 0.0f, b = 0.0f;
+    if (t < Tn) {
+      const int64_t yy = y[t];
+      a = lse[t] * kLog2e;
+      b = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
+    }
+    l2[threadIdx.x] = a;
+    g[threadIdx.x] = b;
+  }
+
+  __device__ void epilogue(f32x16 (&acc)[4][4], int, int, int64_t m0, int64_t n0, char*,
+                           char* extra) const {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    const float* l2 = reinterpret_cast<const float*>(extra);
+    const float* g = l2 + 256;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = acc_row(wm, i, e, lane);
+        const int64_t t = m0 + r;
+        if (t >= Tn) continue;
+        const float lb = l2[r], gs = g[r];
+        T* row = P + t * ld;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int64_t c = n0 + acc_col(wn, j, lane);
+          if (c < ld) {
+            const float p = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -lb));
+            row[c] = T(c < width ? gs * p : 0.0f);
+          }
+        }
+      }
+    }
+  }
+};
+
+// Plain fp32 store (or accumulate) of the tile into C[rows x cols], ld = ldc.
+struct EpiStore {
+  float* C;
+  int64_t ldc, rows, cols;
+  int accumulate;
+  static constexpr int kLdsExtra = 16;
+
+  __device__ void prologue(int64_t, int64_t, char*) const {}
+  __device__ void epilogue(f32x16 (&acc)[4][4], int, int, int64_t m0, int64_t n0, char*,
+                           char*) const {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t r = m0 + acc_row(wm, i, e, lane);
+        if (r >= rows) continue;
+        float* crow = C + r * ldc;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int64_t c = n0 + acc_col(wn, j, lane);
+          if (c < cols) {
+            float v = acc[i][j][e];
+            if (accumulate) v += crow[c];
+            crow[c] = v;
+          }
+        }
+      }
+    }
+  }
+};
+
+// dH[t, :] += dlogp_t W[y_t, :]  (the one-hot part of G W, exact in fp32).
+template <typename T>
+__global__ __launch_bounds__(256) void k_onehot_dh(const T* __restrict__ W,
+                                                   const int64_t* __restrict__ y,
+                                                   const float* __restrict__ dlogp,
+                                                   int64_t d, int64_t V,
+                                                   float* __restrict__ dH) {
+  const int64_t t = blockIdx.x;
+  const int64_t yy = y[t];
+  if (yy < 0 || yy >= V) return;
+  const float g = dlogp[t];
+  const T* w = W + yy * d;
+  float* o = dH + t * d;
+  for (int64_t k = threadIdx.x; k < d; k += blockDim.x) o[k] += g * float(w[k]);
+}
+
+// --- deterministic bucketing of tokens by target (for the one-hot part of dW)
+__global__ void k_fill_i32(int* __restrict__ p, int64_t n, int v) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+__global__ void k_hist(const int64_t* __restrict__ y, int64_t T, int64_t V,
+                       int* __restrict__ counts) {
+  const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  const int64_t yy = y[t];
+  if (yy >= 0 && yy < V) atomicAdd(counts + yy, 1);
+}
+
+// Exclusive scan of counts[V] into offsets[V+1] by one block of 1024 threads,
+// each owning a contiguous segment.
+__global__ __launch_bounds__(1024) void k_scan(const int* __restrict__ counts, int64_t V,
+                                               int* __restrict__ offsets) {
+  __shared__ int part[1024];
+  const int tid = threadIdx.x;
+  const int64_t seg = (V + 1023) / 1024;
+  const int64_t b = min<int64_t>(V, tid * seg), e = min<int64_t>(V, b + seg);
+  int s = 0;
+  for (int64_t i = b; i < e; ++i) s += counts[i];
+  part[tid] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int v = tid >= off ? part[tid - off] : 0;
+    __syncthreads();
+    part[tid] += v;
+    __syncthreads();
+  }
+  int run = part[tid] - s;
+  for (int64_t i = b; i < e; ++i) {
+    offsets[i] = run;
+    run += counts[i];
+  }
+  if (tid == 1023) offsets[V] = part[1023];
+}
+
+__global__ void k_bucket_fill(const int64_t* __restrict__ y, int64_t T, int64_t V,
+                              const int* __restrict__ offsets, int* __restrict__ cursor,
+                              int* __restrict__ unsorted) {
+  const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  const int64_t yy = y[t];
+  if (yy < 0 || yy >= V) return;
+  unsorted[offsets[yy] + atomicAdd(cursor + yy, 1)] = int(t);
+}
+
+// Place each token at its rank among the tokens of its bucket (ascending t).
+__global__ void k_bucket_rank(const int64_t* __restrict__ y, int64_t T, int64_t V,
+                              const int* __restrict__ offsets,
+                              const int* __restrict__ unsorted, int* __restrict__ sorted) {
+  const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  const int64_t yy = y[t];
+  if (yy < 0 || yy >= V) return;
+  const int b = offsets[yy], e = offsets[yy + 1];
+  int rank = 0;
+  for (int p = b; p < e; ++p) rank += unsorted[p] < int(t);
+  sorted[b + rank] = int(t);
+}
+
+// dW[v, :] += sum over tokens t with y_t = v (ascending t) of dlogp_t h_t.
+// One block per bucketed position; only the first position of a bucket works.
+template <typename T>
+__global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
+                                                   const int64_t* __restrict__ y,
+                                                   const float* __restrict__ dlogp,
+                                                   const int* __restrict__ offsets,
+                                                   const int* __restrict__ sorted, int64_t d,
+                                                   int64_t V, float* __restrict__ dW) {
+  const int p = blockIdx.x;
+  if (p >= offsets[V]) return;
+  const int t0 = sorted[p];
+  const int64_t v = y[t0];
+  const int b = offsets[v], e = offsets[v + 1];
+  if (p != b) return;
+  float* o = dW + v * d;
+  for (int64_t k = threadIdx.x; k < d; k += blockDim.x) {
+    float s = 0.0f;
+    for (int q = b; q < e; ++q) {
+      const int t = sorted[q];
+      s += dlogp[t] * float(H[int64_t(t) * d + k]);
+    }
+    o[k] += s;
+  }
+}
+
+template <typename T>
+hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_t d,
+                    int64_t V, float* logp, float* lse, void* ws, hipStream_t s) {
+  const int nTm = int(cdiv(Tn, kBM)), nTn = int(cdiv(V, kBN));
+  Carve cv(ws);
+  float* pm = cv.take<float>(size_t(nTn) * Tn);
+  float* ps = cv.take<float>(size_t(nTn) * Tn);
+  const double es = sizeof(T);
+  Operand A{H, d, Tn, d}, B{W, d, V, d};
+  EpiFwd epi{y, Tn, V, pm, ps, logp};
+  {
+    ProfScope ps_(s, "logprob_fwd_gemm", 2.0 * Tn * d * V,
+                  es * (double(Tn) * d + double(V) * d) + 12.0 * Tn);
+    hipLaunchKernelGGL((gemm_kernel<T, true, true, EpiFwd>), dim3(nTm * nTn), dim3(kThreads), 0,
+                       s, A, B, d, nTm, nTn, epi);
+  }
+  {
+    ProfScope ps_(s, "logprob_fwd_merge", 0.0, 8.0 * nTn * Tn + 20.0 * Tn);
+    hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(Tn, 64)), dim3(512), 0, s, pm, ps, nTn, Tn, y, V,
+                       logp, lse);
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
+                    const float* dlogp, int64_t Tn, int64_t d, int64_t V, float* dH, float* dW,
+                    int flags, void* ws, hipStream_t s) {
+  const int64_t chunk = bwd_chunk_cols(Tn, V, sizeof(T));
+  const int64_t ld = int64_t(align_up(size_t(min(chunk, V)), 64));
+  Carve cv(ws);
+  T* P = cv.take<T>(size_t(Tn) * ld);
+  int* counts = cv.take<int>(V);
+  int* cursor = cv.take<int>(V);
+  int* offsets = cv.take<int>(V + 1);
+  int* unsorted = cv.take<int>(Tn);
+  int* sorted = cv.take<int>(Tn);
+  const int nTm = int(cdiv(Tn, kBM));
+  const int nTd = int(cdiv(d, kBN));
+
+  const double es = sizeof(T);
+  if (dW) {
+    ProfScope ps_(s, "logprob_bwd_bucket", 0.0, 32.0 * Tn + 16.0 * V);
+    const int nb = int(cdiv(V, 256)), tb = int(cdiv(Tn, 256));
+    hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, counts, V, 0);
+    hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, cursor, V, 0);
+    hipLaunchKernelGGL(k_hist, dim3(tb), dim3(256), 0, s, y, Tn, V, counts);
+    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, counts, V, offsets);
+    hipLaunchKernelGGL(k_bucket_fill, dim3(tb), dim3(256), 0, s, y, Tn, V, offsets, cursor,
+                       unsorted);
+    hipLaunchKernelGGL(k_bucket_rank, dim3(tb), dim3(256), 0, s, y, Tn, V, offsets, unsorted,
+                       sorted);
+  }
+  for (int64_t v0 = 0; v0 < V; v0 += chunk) {
+    const int64_t width = min(chunk, V - v0);
+    const T* Wc = W + v0 * d;
+    {
+      Operand A{H, d, Tn, d}, B{Wc, d, width, d};
+      EpiProbs<T> epi{y, lse, dlogp, Tn, V, width, ld, P};
+      const int nTn = int(cdiv(ld, kBN));
+      ProfScope ps_(s, "logprob_bwd_probs", 2.0 * Tn * d * width,
+                    es * (double(Tn) * d + double(width) * d + double(Tn) * width) + 16.0 * Tn);
+      hipLaunchKernelGGL((gemm_kernel<T, true, true, EpiProbs<T>>), dim3(nTm * nTn),
+                         dim3(kThreads), 0, s, A, B, d, nTm, nTn, epi);
+    }
+    if (dH) {
+      // dH (+)= P~ Wc : M = T, N = d, K = chunk columns
+      Operand A{P, ld, Tn, ld}, B{Wc, d, d, width};
+      EpiStore epi{dH, d, Tn, d, (v0 > 0 || (flags & MC_BWD_ACCUMULATE_DHIDDEN)) ? 1 : 0};
+      ProfScope ps_(s, "logprob_bwd_dhidden", 2.0 * Tn * d * width,
+                    es * (double(Tn) * width + double(width) * d) +
+                        4.0 * Tn * d * (epi.accumulate ? 2 : 1));
+      hipLaunchKernelGGL((gemm_kernel<T, true, false, EpiStore>), dim3(nTm * nTd),
+                         dim3(kThreads), 0, s, A, B, ld, nTm, nTd, epi);
+    }
+    if (dW) {
+      // dW[chunk] (+)= P~^T H : M = chunk columns, N = d, K = T
+      Operand A{P, ld, ld, Tn}, B{H, d, d, Tn};
+      EpiStore epi{dW + v0 * d, d, width, d, (flags & MC_BWD_ACCUMULATE_DWEIGHT) ? 1 : 0};
+      const int nTv = int(cdiv(width, kBM));
+      ProfScope ps_(s, "logprob_bwd_dweight", 2.0 * Tn * d * width,
+                    es * (double(Tn) * width + double(Tn) * d) +
+                        4.0 * width * d * (epi.accumulate ? 2 : 1));
+      hipLaunchKernelGGL((gemm_kernel<T, false, false, EpiStore>), dim3(nTv * nTd),
+                         dim3(kThreads), 0, s, A, B, Tn, nTv, nTd, epi);
+    }
+  }
+  if (dH) {
+    ProfScope ps_(s, "logprob_bwd_onehot_dh", 2.0 * Tn * d, (es + 8.0) * Tn * d);
+    hipLaunchKernelGGL(k_onehot_dh<T>, dim3(Tn), dim3(256), 0, s, W, y, dlogp, d, V, dH);
+  }
+  if (dW) {
+    ProfScope ps_(s, "logprob_bwd_onehot_dw", 2.0 * Tn * d, (es + 8.0) * Tn * d);
+    hipLaunchKernelGGL(k_onehot_dw<T>, dim3(Tn), dim3(256), 0, s, H, y, dlogp, offsets, sorted,
+                       d, V, dW);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int64_t bwd_chunk_cols(int64_t T, int64_t V, size_t esize) {
+  const int64_t per_col = std::max<int64_t>(1, T) * int64_t(esize);
+  int64_t c = int64_t(kBwdChunkBytes) / per_col;
+  c = c / kBN * kBN;
+  if (c < kBN) c = kBN;
+  return c >= V ? V : c;
+}
+
+size_t fwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t) {
+  const size_t n = size_t(cdiv(V, kBN)) * size_t(T);
+  return 2 * align_up(n * sizeof(float), kWsAlign);
+}
+
+size_t bwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t dt) {
+  const size_t es = dt == MC_BF16 ? 2 : 4;
+  const int64_t chunk = bwd_chunk_cols(T, V, es);
+  const size_t ld = align_up(size_t(std::min(chunk, V)), 64);
+  size_t n = align_up(size_t(T) * ld * es, kWsAlign);
+  n += 2 * align_up(size_t(V) * 4, kWsAlign);
+  n += align_up(size_t(V + 1) * 4, kWsAlign);
+  n += 2 * align_up(size_t(T) * 4, kWsAlign);
+  return n;
+}
+
+hipError_t launch_fwd(const void* H, const void* W, const int64_t* y, int64_t T, int64_t d,
+                      int64_t V, mc_dtype_t dt, float* logp, float* lse, void* ws,
+                      hipStream_t s) {
+  if (dt == MC_BF16)
+    return fwd_impl(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W), y, T, d, V,
+                    logp, lse, ws, s);
+  return fwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, T, d, V, logp,
+                  lse, ws, s);
+}
+
+hipError_t launch_bwd(const void* H, const void* W, const int64_t* y, const float* lse,
+                      const float* dlogp, int64_t T, int64_t d, int64_t V, mc_dtype_t dt,
+                      float* dH, float* dW, int flags, void* ws, hipStream_t s) {
+  if (dt == MC_BF16)
+    return bwd_impl(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W), y, lse, dlogp,
+                    T, d, V, dH, dW, flags, ws, s);
+  return bwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, lse, dlogp, T,
+                  d, V, dH, dW, flags, ws, s);
+}
+
+}  // namespace mc

@@ -1,0 +1,144 @@
+"""The C ABI: libmc.so loads without a GPU, exports every function that
+include/mc.h declares, and rejects bad arguments on the host before any
+launch (these calls make no HIP call, so they run here without a GPU)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_04847_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mc.h")
+
+OK, INVALID, UNSUP, WS = 0, 1, 2, 3
+F32, BF16 = 0, 1
+FAKE = 1 << 20          # an aligned, never-dereferenced address
+FAKE_WS = 1 << 24       # 256-byte aligned
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        pytest.skip("libmc.so not built")
+    return binding.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]*?\b(mc_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert {"mc_logprob_fwd", "mc_logprob_bwd", "mc_rl_loss", "mc_check_packing",
+            "mc_status_string", "mc_version"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version(lib):
+    assert binding.status_string(0) == "MC_OK"
+    assert binding.status_string(3) == "MC_ERR_WORKSPACE"
+    assert "gfx950" in binding.version()
+
+
+def fwd(lib, T=16, d=64, V=100, dt=BF16, H=FAKE, W=FAKE, y=FAKE, lp=FAKE, ls=FAKE,
+        ws=FAKE_WS, nbytes=None):
+    need = lib.mc_logprob_fwd_workspace_size(max(T, 0), d, V, dt)
+    return lib.mc_logprob_fwd(H, W, y, T, d, V, dt, lp, ls, ws,
+                              need if nbytes is None else nbytes, None)
+
+
+def test_fwd_argument_checks(lib):
+    assert fwd(lib, T=-1) == INVALID
+    assert fwd(lib, d=0) == INVALID
+    assert fwd(lib, V=0) == INVALID
+    assert fwd(lib, d=60) == UNSUP
+    assert fwd(lib, dt=7) == UNSUP
+    assert fwd(lib, H=None) == INVALID
+    assert fwd(lib, y=None) == INVALID
+    assert fwd(lib, ls=None) == INVALID
+    assert fwd(lib, H=FAKE + 8) == INVALID          # hidden not 16-byte aligned
+    assert fwd(lib, nbytes=10) == WS
+    assert fwd(lib, ws=None) == WS
+    assert fwd(lib, ws=FAKE_WS + 128) == WS        # workspace not 256-byte aligned
+    assert fwd(lib, T=0, H=None, W=None, y=None, lp=None, ls=None, ws=None) == OK  # no-op
+    assert fwd(lib, V=1 << 31) == UNSUP
+
+
+def test_workspace_sizes(lib):
+    a = lib.mc_logprob_fwd_workspace_size(1000, 128, 1000, BF16)
+    b = lib.mc_logprob_fwd_workspace_size(2000, 128, 1000, BF16)
+    assert 0 < a < b
+    assert lib.mc_logprob_fwd_workspace_size(10, 60, 10, BF16) == 0      # invalid -> 0
+    bw = lib.mc_logprob_bwd_workspace_size(16384, 4096, 151936, BF16)
+    # the transient softmax operand is capped at 4 GiB plus small index arrays
+    assert (4 << 30) - 151936 * 16384 * 2 < bw < (4 << 30) + (16 << 20)
+    assert lib.mc_rl_loss_workspace_size(100, 8, 2) > 0
+    assert lib.mc_rl_loss_workspace_size(-1, 8, 2) == 0
+
+
+def bwd(lib, T=16, d=64, V=100, dt=BF16, dh=FAKE, dw=FAKE, flags=0, lse=FAKE, dl=FAKE,
+        nbytes=None):
+    need = lib.mc_logprob_bwd_workspace_size(T, d, V, dt)
+    return lib.mc_logprob_bwd(FAKE, FAKE, FAKE, lse, dl, T, d, V, dt, dh, dw, flags, FAKE_WS,
+                              need if nbytes is None else nbytes, None)
+
+
+def test_bwd_argument_checks(lib):
+    assert bwd(lib, dh=None, dw=None) == INVALID
+    assert bwd(lib, flags=4) == INVALID
+    assert bwd(lib, d=12) == UNSUP
+    assert bwd(lib, lse=None) == INVALID
+    assert bwd(lib, dl=None) == INVALID
+    assert bwd(lib, dh=FAKE + 4) == INVALID
+    assert bwd(lib, nbytes=0) == WS
+
+
+def loss(lib, T=10, B=2, NG=1, params=None, out=None, ws=FAKE_WS, nbytes=None, **ptrs):
+    p = params or binding.RLParams().to_c()
+    o = out or binding.RLOutputsC(FAKE, FAKE, *([None] * 8))
+    need = lib.mc_rl_loss_workspace_size(T, B, NG)
+    args = dict(logp=FAKE, lr=FAKE, mask=None, cu=FAKE, cg=FAKE, rw=FAKE)
+    args.update(ptrs)
+    return lib.mc_rl_loss(args["logp"], args["lr"], args["mask"], args["cu"], args["cg"],
+                          args["rw"], T, B, NG, ctypes.byref(p), ctypes.byref(o), ws,
+                          need if nbytes is None else nbytes, None)
+
+
+@pytest.mark.parametrize("field,value", [
+    ("eps_low", 1.0), ("eps_low", -0.1), ("eps_high", -0.5), ("delta", -1.0),
+    ("delta", float("nan")), ("adv_eps", float("inf")), ("std_ddof", 2), ("filter", 3),
+])
+def test_loss_parameter_checks(lib, field, value):
+    p = binding.RLParams().to_c()
+    setattr(p, field, value)
+    assert loss(lib, params=p) == INVALID
+
+
+def test_loss_argument_checks(lib):
+    assert loss(lib, T=-1) == INVALID
+    assert loss(lib, B=0, NG=0) == INVALID            # tokens but no sequence
+    assert loss(lib, NG=0) == INVALID                 # sequences but no group
+    assert loss(lib, logp=None) == INVALID
+    assert loss(lib, cu=None) == INVALID
+    assert loss(lib, rw=None) == INVALID
+    o = binding.RLOutputsC(None, FAKE, *([None] * 8))
+    assert loss(lib, out=o) == INVALID                # loss output is required
+    o = binding.RLOutputsC(FAKE, None, *([None] * 8))
+    assert loss(lib, out=o) == INVALID                # dlogp output is required
+    assert loss(lib, nbytes=1) == WS
+
+
+def test_host_packing_check(lib):
+    good_cu, good_cg = np.array([0, 3, 3, 7]), np.array([0, 1, 3])
+    assert binding.check_packing(good_cu, good_cg, 7)
+    assert not binding.check_packing(good_cu, good_cg, 8)                # end != T
+    assert not binding.check_packing(np.array([1, 3, 3, 7]), good_cg, 7)  # start != 0
+    assert not binding.check_packing(np.array([0, 4, 3, 7]), good_cg, 7)  # decreasing
+    assert not binding.check_packing(good_cu, np.array([0, 1, 2]), 7)    # groups end != B
+    assert not binding.check_packing(good_cu, np.array([0, 2, 1, 3]), 7)
+    assert binding.check_packing(np.array([0]), np.array([0]), 0)         # empty batch

@@ -335,14 +335,15 @@ def make_structure(cfg, seed=None, eps_low=DEFAULT_EPS_LOW,
 # Dense tensors H [T,d], W [V,d] and targets y [T]
 # ---------------------------------------------------------------------------
 def make_tensors_numpy(cfg, T: int, seed=None):
-    """H ~ N(0,1), W ~ 0.02 N(0,1), drawn in fp32 and rounded to bf16 for bf16
+    """H ~ N(0,1), W ~ w_std N(0,1) (w_std = 0.02 unless the workload says
+    otherwise), drawn in fp32 and rounded to bf16 for bf16
     workloads.  Returns (H, W) as float32 arrays holding the exact values the
     GPU consumes, plus their bf16 bit patterns (None for fp32 workloads)."""
     cfg = _cfg(cfg)
     rng = _rngs(cfg["seed"] if seed is None else seed)
     d, V = cfg["d"], cfg["V"]
     H = rng["H"].standard_normal((T, d), dtype=np.float32)
-    W = (np.float32(0.02) * rng["W"].standard_normal((V, d), dtype=np.float32))
+    W = (np.float32(cfg.get("w_std", 0.02)) * rng["W"].standard_normal((V, d), dtype=np.float32))
     if cfg["dtype"] == "bf16":
         hb, wb = f32_to_bf16_bits(H), f32_to_bf16_bits(W)
         return bf16_bits_to_f32(hb), bf16_bits_to_f32(wb), hb, wb
@@ -381,7 +382,7 @@ def make_tensors_torch(cfg, T: int, device, seed=None):
     step = 16384
     for v0 in range(0, V, step):
         n = min(step, V - v0)
-        W[v0:v0 + n] = (0.02 * torch.randn(n, d, generator=g, device=device,
+        W[v0:v0 + n] = (cfg.get("w_std", 0.02) * torch.randn(n, d, generator=g, device=device,
                                            dtype=torch.float32)).to(dt)
     return H, W
 
