@@ -19,6 +19,7 @@ namespace mc {
 
 typedef __bf16 bf16_t;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -189,18 +190,25 @@ template <> struct Mfma<bf16_t> {
   }
 };
 
+// fp32: each 16-byte chunk holds 4 K values, consumed by 4 MFMAs of K = 2.
+// (The chunks are bit-cast to float vectors as a whole: bit-casting a single
+// element of an integer vector compiles to element 0 with this toolchain.)
 template <> struct Mfma<float> {
   __device__ __forceinline__ static void step(f32x16 (&acc)[4][4], const u32x4 (&a)[4],
                                               const u32x4 (&b)[4]) {
+    f32x4 af[4], bf[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      af[i] = __builtin_bit_cast(f32x4, a[i]);
+      bf[i] = __builtin_bit_cast(f32x4, b[i]);
+    }
 #pragma unroll
     for (int e = 0; e < 4; ++e)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-              __builtin_bit_cast(float, a[i][e]), __builtin_bit_cast(float, b[j][e]), acc[i][j],
-              0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][e], bf[j][e], acc[i][j], 0, 0, 0);
   }
 };
 

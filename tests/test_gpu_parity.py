@@ -41,12 +41,17 @@ def test_config1_end_to_end_fp32():
     assert o["seq_mask"].sum() == case["s"].B - 1           # the drifted sequence is dropped
 
 
+def _drift(B):
+    return dict(kind="frac_normal", count=max(1, B // 10), mean=0.3, std=0.1)
+
+
 @pytest.mark.parametrize("T,d,V,groups,G", [
     (1500, 256, 3000, 4, 8),        # several tiles in every dimension, ragged tails
     (700, 136, 1000, 2, 8),         # d not a multiple of the 64-wide K step
 ])
 def test_midsize_bf16_end_to_end(T, d, V, groups, G):
-    cfg = scaled_config(4, T=T, n_groups=groups, group_size=G, d=d, V=V, hi=400, seed=11)
+    cfg = scaled_config(4, T=T, n_groups=groups, group_size=G, d=d, V=V, hi=400, seed=11,
+                        drift=_drift(groups * G))
     case = small_case(cfg)
     p = oracle.RLParams()
     o = oracle_step(case, p)
@@ -56,7 +61,8 @@ def test_midsize_bf16_end_to_end(T, d, V, groups, G):
 
 @pytest.mark.parametrize("filt", ["none", "vanilla"])
 def test_filter_modes_end_to_end(filt):
-    cfg = scaled_config(4, T=900, n_groups=4, group_size=8, d=128, V=700, hi=300, seed=12)
+    cfg = scaled_config(4, T=900, n_groups=4, group_size=8, d=128, V=700, hi=300, seed=12,
+                        drift=_drift(32))
     case = small_case(cfg)
     p = oracle.RLParams(filter=filt)
     o = oracle_step(case, p)
@@ -68,7 +74,7 @@ def test_peaked_softmax_pterm():
     # W std 0.1 at d=512: logits std ~2.3, so the softmax part of the gradient
     # is a visible share; compare it separately from the one-hot part.
     cfg = scaled_config(4, T=600, n_groups=2, group_size=8, d=512, V=2000, hi=200, seed=13,
-                        w_std=0.1)
+                        w_std=0.1, drift=_drift(16))
     case = small_case(cfg)
     p = oracle.RLParams(filter="none")
     o = oracle_step(case, p)
@@ -134,7 +140,8 @@ def test_zero_weight_closed_form():
 
 
 def test_accumulate_flags_and_partial_outputs():
-    cfg = scaled_config(4, T=400, n_groups=2, group_size=8, d=128, V=600, hi=100, seed=14)
+    cfg = scaled_config(4, T=400, n_groups=2, group_size=8, d=128, V=600, hi=100, seed=14,
+                        drift=_drift(16))
     case = small_case(cfg)
     mc = _mc()
     H, W, y = device_tensors(case)
@@ -155,7 +162,8 @@ def test_accumulate_flags_and_partial_outputs():
 
 
 def test_determinism_bit_identical():
-    cfg = scaled_config(4, T=1200, n_groups=4, group_size=8, d=256, V=1500, hi=300, seed=15)
+    cfg = scaled_config(4, T=1200, n_groups=4, group_size=8, d=256, V=1500, hi=300, seed=15,
+                        drift=_drift(32))
     case = small_case(cfg)
     p = oracle.RLParams()
     lr = (oracle.logprob_fwd(case["H"], case["W"], case["y"])[0]
