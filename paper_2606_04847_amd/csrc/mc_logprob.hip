@@ -160,8 +160,9 @@ struct EpiProbs {
   const int64_t* y;
   const float* lse;
   const float* dlogp;
-  int64_t Tn, V, width, ld;
-  T* P;
+  int64_t Tn, V, width, ld, pld;   // ld: padded chunk width; pld: padded token count
+  T* P;                            // panel layout (see Lay::TileTK)
+  static constexpr int64_t kPanel = 128 / sizeof(T);
   static constexpr int kLdsExtra = 2 * 256 * 4;
 
   __device__ void prologue(int64_t m0, int64_t, char* extra) const {
@@ -192,13 +193,13 @@ struct EpiProbs {
         const int64_t t = m0 + r;
         if (t >= Tn) continue;
         const float lb = l2[r], gs = g[r];
-        T* row = P + t * ld;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int64_t c = n0 + acc_col(wn, j, lane);
           if (c < ld) {
             const float p = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -lb));
-            row[c] = T(c < width ? gs * p : 0.0f);
+            P[(c / kPanel) * pld * kPanel + t * kPanel + c % kPanel] =
+                T(c < width ? gs * p : 0.0f);
           }
         }
       }
@@ -354,11 +355,15 @@ hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_
   float* ps = cv.take<float>(size_t(nTn) * Tn);
   const double es = sizeof(T);
   Operand A{H, d, Tn, d}, B{W, d, V, d};
+  if (!operand_in_bounds<T, Lay::KMajor>(A, size_t(Tn) * d * sizeof(T)) ||
+      !operand_in_bounds<T, Lay::KMajor>(B, size_t(V) * d * sizeof(T)))
+    return hipErrorInvalidValue;
   EpiFwd epi{y, Tn, V, pm, ps, logp};
   {
     ProfScope ps_(s, "logprob_fwd_gemm", 2.0 * Tn * d * V,
                   es * (double(Tn) * d + double(V) * d) + 12.0 * Tn);
-    hipLaunchKernelGGL((gemm_kernel<T, true, true, EpiFwd>), dim3(nTm * nTn), dim3(kThreads), 0,
+    hipLaunchKernelGGL((gemm_kernel<T, Lay::KMajor, Lay::KMajor, EpiFwd>), dim3(nTm * nTn),
+                       dim3(kThreads), 0,
                        s, A, B, d, nTm, nTn, epi);
   }
   {
@@ -375,8 +380,9 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                     int flags, void* ws, hipStream_t s) {
   const int64_t chunk = bwd_chunk_cols(Tn, V, sizeof(T));
   const int64_t ld = int64_t(align_up(size_t(min(chunk, V)), 64));
+  const int64_t pld = cdiv(Tn, 64) * 64;
   Carve cv(ws);
-  T* P = cv.take<T>(size_t(Tn) * ld);
+  T* P = cv.take<T>(size_t(pld) * ld);
   int* counts = cv.take<int>(V);
   int* cursor = cv.take<int>(V);
   int* offsets = cv.take<int>(V + 1);
@@ -400,35 +406,47 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   }
   for (int64_t v0 = 0; v0 < V; v0 += chunk) {
     const int64_t width = min(chunk, V - v0);
+    const int64_t ldc = int64_t(align_up(size_t(width), 64));   // padded width of this chunk
     const T* Wc = W + v0 * d;
+    const size_t wc_bytes = size_t(V - v0) * d * sizeof(T);
+    const size_t p_bytes = size_t(pld) * ld * sizeof(T);
     {
       Operand A{H, d, Tn, d}, B{Wc, d, width, d};
-      EpiProbs<T> epi{y, lse, dlogp, Tn, V, width, ld, P};
-      const int nTn = int(cdiv(ld, kBN));
+      if (!operand_in_bounds<T, Lay::KMajor>(A, size_t(Tn) * d * sizeof(T)) ||
+          !operand_in_bounds<T, Lay::KMajor>(B, wc_bytes) || ldc > ld)
+        return hipErrorInvalidValue;
+      EpiProbs<T> epi{y, lse, dlogp, Tn, V, width, ldc, pld, P};
+      const int nTn = int(cdiv(ldc, kBN));
       ProfScope ps_(s, "logprob_bwd_probs", 2.0 * Tn * d * width,
                     es * (double(Tn) * d + double(width) * d + double(Tn) * width) + 16.0 * Tn);
-      hipLaunchKernelGGL((gemm_kernel<T, true, true, EpiProbs<T>>), dim3(nTm * nTn),
+      hipLaunchKernelGGL((gemm_kernel<T, Lay::KMajor, Lay::KMajor, EpiProbs<T>>), dim3(nTm * nTn),
                          dim3(kThreads), 0, s, A, B, d, nTm, nTn, epi);
     }
     if (dH) {
       // dH (+)= P~ Wc : M = T, N = d, K = chunk columns
-      Operand A{P, ld, Tn, ld}, B{Wc, d, d, width};
+      Operand A{P, pld, Tn, ldc}, B{Wc, d, d, width};
+      if (!operand_in_bounds<T, Lay::TileTK>(A, p_bytes) ||
+          !operand_in_bounds<T, Lay::MNMajor>(B, wc_bytes))
+        return hipErrorInvalidValue;
       EpiStore epi{dH, d, Tn, d, (v0 > 0 || (flags & MC_BWD_ACCUMULATE_DHIDDEN)) ? 1 : 0};
       ProfScope ps_(s, "logprob_bwd_dhidden", 2.0 * Tn * d * width,
                     es * (double(Tn) * width + double(width) * d) +
                         4.0 * Tn * d * (epi.accumulate ? 2 : 1));
-      hipLaunchKernelGGL((gemm_kernel<T, true, false, EpiStore>), dim3(nTm * nTd),
-                         dim3(kThreads), 0, s, A, B, ld, nTm, nTd, epi);
+      hipLaunchKernelGGL((gemm_kernel<T, Lay::TileTK, Lay::MNMajor, EpiStore>), dim3(nTm * nTd),
+                         dim3(kThreads), 0, s, A, B, ldc, nTm, nTd, epi);
     }
     if (dW) {
       // dW[chunk] (+)= P~^T H : M = chunk columns, N = d, K = T
-      Operand A{P, ld, ld, Tn}, B{H, d, d, Tn};
+      Operand A{P, pld, ldc, Tn}, B{H, d, d, Tn};
+      if (!operand_in_bounds<T, Lay::TileVT>(A, p_bytes) ||
+          !operand_in_bounds<T, Lay::MNMajor>(B, size_t(Tn) * d * sizeof(T)))
+        return hipErrorInvalidValue;
       EpiStore epi{dW + v0 * d, d, width, d, (flags & MC_BWD_ACCUMULATE_DWEIGHT) ? 1 : 0};
       const int nTv = int(cdiv(width, kBM));
       ProfScope ps_(s, "logprob_bwd_dweight", 2.0 * Tn * d * width,
                     es * (double(Tn) * width + double(Tn) * d) +
                         4.0 * width * d * (epi.accumulate ? 2 : 1));
-      hipLaunchKernelGGL((gemm_kernel<T, false, false, EpiStore>), dim3(nTv * nTd),
+      hipLaunchKernelGGL((gemm_kernel<T, Lay::TileVT, Lay::MNMajor, EpiStore>), dim3(nTv * nTd),
                          dim3(kThreads), 0, s, A, B, Tn, nTv, nTd, epi);
     }
   }
@@ -463,7 +481,7 @@ size_t bwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t dt) {
   const size_t es = dt == MC_BF16 ? 2 : 4;
   const int64_t chunk = bwd_chunk_cols(T, V, es);
   const size_t ld = align_up(size_t(std::min(chunk, V)), 64);
-  size_t n = align_up(size_t(T) * ld * es, kWsAlign);
+  size_t n = align_up(size_t(cdiv(T, 64)) * 64 * ld * es, kWsAlign);
   n += 2 * align_up(size_t(V) * 4, kWsAlign);
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);

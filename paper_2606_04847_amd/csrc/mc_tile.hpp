@@ -37,15 +37,75 @@ template <> struct Elem<bf16_t> { static constexpr int kChunk = 8; };
 template <> struct Elem<float> { static constexpr int kChunk = 4; };
 
 // Operand of a contraction C[m][n] = sum_k A[m][k] B[n][k].  For A the "rows"
-// are M, for B they are N.  K-major: element (r, k) at ptr[r * ld + k];
-// MN-major: element (r, k) at ptr[k * ld + r].  Rows >= rows and k >= K read
-// as zero.  K-major needs K % chunk == 0; MN-major needs rows % chunk == 0.
+// are M, for B they are N.  Rows >= rows and k >= K read as zero.  The layout
+// is a template policy of the copy (see below); `ld` is its stride parameter.
 struct Operand {
   const void* ptr;
   int64_t ld;
   int64_t rows;
   int64_t K;
 };
+
+// Layout policies.  A 16-byte chunk runs along k for the K-contiguous kinds
+// and along r for the M/N-contiguous ones.
+//   KMajor   (r, k) at r * ld + k
+//   MNMajor  (r, k) at k * ld + r
+//   TileTK   panel buffer read with r = token, k = vocab
+//   TileVT   the same buffer read with r = vocab, k = token
+// The panel buffer (the backward's transient operand) holds the vocabulary
+// in panels of BV = 128 bytes of elements; panel j is a row-major
+// [ld x BV] matrix (ld = padded token count), panels stored one after the
+// other: element (t, v) at (v / BV) * ld * BV + t * BV + v % BV.  Every
+// 128-byte run either contraction reads is contiguous.
+enum class Lay { KMajor, MNMajor, TileTK, TileVT };
+
+template <Lay L> struct KContig {
+  static constexpr bool value = (L == Lay::KMajor || L == Lay::TileTK);
+};
+
+// Byte offsets: base of the tile starting at row r0 (stage 0), the advance of
+// one K stage, and the offset of (r0 + dr, k0 + dk) relative to the stage base.
+template <typename T, Lay L> struct LayMath {
+  static constexpr int64_t es = sizeof(T);
+  static constexpr int64_t BV = 128 / sizeof(T);
+  static constexpr int64_t KT = 128 / sizeof(T);
+  __host__ __device__ static int64_t tile_base(const Operand& op, int64_t r0) {
+    if constexpr (L == Lay::KMajor) return r0 * op.ld * es;
+    else if constexpr (L == Lay::MNMajor) return r0 * es;
+    else if constexpr (L == Lay::TileTK) return r0 * BV * es;
+    else return (r0 / BV) * op.ld * BV * es;
+  }
+  __host__ __device__ static int64_t stage_step(const Operand& op) {
+    if constexpr (L == Lay::KMajor) return KT * es;
+    else if constexpr (L == Lay::MNMajor) return KT * op.ld * es;
+    else if constexpr (L == Lay::TileTK) return op.ld * BV * es;
+    else return KT * BV * es;
+  }
+  __host__ __device__ static uint32_t rel(const Operand& op, int dr, int dk) {
+    if constexpr (L == Lay::KMajor) return uint32_t((int64_t(dr) * op.ld + dk) * es);
+    else if constexpr (L == Lay::MNMajor) return uint32_t((int64_t(dk) * op.ld + dr) * es);
+    else if constexpr (L == Lay::TileTK) return uint32_t((int64_t(dr) * BV + dk) * es);
+    else return uint32_t(((dr / BV) * op.ld * BV + int64_t(dk) * BV + dr % BV) * es);
+  }
+};
+
+// Host-side check used before every launch: the last in-range chunk of the
+// operand (offsets grow with r and k in every layout) lies inside `bytes`,
+// and the per-thread 32-bit offsets of one tile cannot overflow.
+template <typename T, Lay L>
+inline bool operand_in_bounds(const Operand& op, size_t bytes) {
+  using M = LayMath<T, L>;
+  constexpr int64_t E = Elem<T>::kChunk;
+  if (op.rows < 1 || op.K < 1) return false;
+  int64_t r = op.rows - 1, k = op.K - 1;
+  if (KContig<L>::value) k = k / E * E; else r = r / E * E;
+  const int64_t last = M::tile_base(op, r / 256 * 256) + (k / M::KT) * M::stage_step(op) +
+                       int64_t(M::rel(op, int(r % 256), int(k % M::KT)));
+  const int64_t span = (L == Lay::KMajor) ? 256 * op.ld * M::es
+                       : (L == Lay::MNMajor) ? M::KT * op.ld * M::es
+                       : (L == Lay::TileVT) ? 256 * op.ld * M::es : 256 * M::BV * M::es;
+  return last >= 0 && size_t(last) + 16 <= bytes && span < (int64_t(1) << 32);
+}
 
 __device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
 __device__ __forceinline__ int lds_off(int r, int c) {
@@ -72,24 +132,46 @@ __device__ __forceinline__ void tile_of(int bid, int nTm, int nTn, int& tm, int&
 
 // ---------------------------------------------------------------------------
 // Global -> register -> LDS copy of one 256-row x 128-byte operand stage.
+// Every copy keeps a uniform 64-bit tile base and per-thread 32-bit offsets
+// computed once per tile; an out-of-range chunk is loaded from the operand's
+// first element (always in bounds, even when the whole tile lies past the
+// operand's rows) and replaced by zeros.
 // ---------------------------------------------------------------------------
-template <typename T, bool KMajor> struct StageCopy;
+template <typename T, Lay L, bool KC = KContig<L>::value> struct StageCopy;
 
 // K-contiguous: thread owns chunk (tid & 7) of rows (tid >> 3) + 32 i.
-template <typename T> struct StageCopy<T, true> {
+template <typename T, Lay L> struct StageCopy<T, L, true> {
+  using M = LayMath<T, L>;
   static constexpr int E = Elem<T>::kChunk;
   u32x4 r[8];
-  __device__ __forceinline__ void load(const Operand& op, int64_t r0, int64_t k0, int tid) {
-    const int c = tid & 7;
-    const int64_t kk = k0 + c * E;
-    const T* base = static_cast<const T*>(op.ptr);
+  const char* tb;
+  const char* safe;
+  int64_t step, K;
+  uint32_t off[8];
+  uint32_t rowok;
+  int kc;
+  __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
+    safe = static_cast<const char*>(op.ptr);
+    tb = safe + M::tile_base(op, r0);
+    step = M::stage_step(op);
+    K = op.K;
+    kc = (tid & 7) * E;
+    rowok = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int64_t row = r0 + (tid >> 3) + 32 * i;
-      if (row < op.rows && kk < op.K)
-        r[i] = *reinterpret_cast<const u32x4*>(base + row * op.ld + kk);
-      else
-        r[i] = u32x4{0u, 0u, 0u, 0u};
+      const int dr = (tid >> 3) + 32 * i;
+      off[i] = M::rel(op, dr, kc);
+      if (r0 + dr < op.rows) rowok |= 1u << i;
+    }
+  }
+  __device__ __forceinline__ void load(int64_t kt) {
+    const char* sb = tb + kt * step;
+    const bool kok = kt * M::KT + kc < K;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const bool ok = kok && ((rowok >> i) & 1u);
+      const u32x4 v = *reinterpret_cast<const u32x4*>(ok ? sb + off[i] : safe);
+      r[i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
     }
   }
   __device__ __forceinline__ void store(char* lds, int tid) const {
@@ -102,19 +184,33 @@ template <typename T> struct StageCopy<T, true> {
 
 // M/N-contiguous bf16: thread owns one 8(k) x 8(mn) block, mn-block tid & 31,
 // k-block tid >> 5; transposed with byte permutes before the LDS write.
-template <> struct StageCopy<bf16_t, false> {
+template <Lay L> struct StageCopy<bf16_t, L, false> {
+  using M = LayMath<bf16_t, L>;
   u32x4 r[8];
-  __device__ __forceinline__ void load(const Operand& op, int64_t r0, int64_t k0, int tid) {
-    const int64_t mn = r0 + (tid & 31) * 8;
-    const int64_t kb = k0 + (tid >> 5) * 8;
-    const bf16_t* base = static_cast<const bf16_t*>(op.ptr);
+  const char* tb;
+  const char* safe;
+  int64_t step, K;
+  uint32_t off0, dk_bytes;
+  int kb;
+  bool mnok;
+  __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
+    safe = static_cast<const char*>(op.ptr);
+    tb = safe + M::tile_base(op, r0);
+    step = M::stage_step(op);
+    K = op.K;
+    kb = (tid >> 5) * 8;
+    off0 = M::rel(op, (tid & 31) * 8, kb);
+    dk_bytes = M::rel(op, (tid & 31) * 8, kb + 1) - off0;
+    mnok = r0 + (tid & 31) * 8 < op.rows;
+  }
+  __device__ __forceinline__ void load(int64_t kt) {
+    const char* sb = tb + kt * step;
+    const int64_t k0 = kt * M::KT + kb;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int64_t k = kb + i;
-      if (mn < op.rows && k < op.K)
-        r[i] = *reinterpret_cast<const u32x4*>(base + k * op.ld + mn);
-      else
-        r[i] = u32x4{0u, 0u, 0u, 0u};
+      const bool ok = mnok && (k0 + i < K);
+      const u32x4 v = *reinterpret_cast<const u32x4*>(ok ? sb + off0 + i * dk_bytes : safe);
+      r[i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
     }
   }
   __device__ __forceinline__ void store(char* lds, int tid) const {
@@ -135,24 +231,41 @@ template <> struct StageCopy<bf16_t, false> {
   }
 };
 
-// M/N-contiguous fp32: two 4(k) x 4(mn) blocks per thread, transposed by
-// register moves.
-template <> struct StageCopy<float, false> {
+// M/N-contiguous fp32: two 4(k) x 4(mn) blocks per thread (mn-block b & 63,
+// k-block b >> 6 for b = tid, tid + 256), transposed by register moves.
+template <Lay L> struct StageCopy<float, L, false> {
+  using M = LayMath<float, L>;
   u32x4 r[8];
-  __device__ __forceinline__ void load(const Operand& op, int64_t r0, int64_t k0, int tid) {
-    const float* base = static_cast<const float*>(op.ptr);
+  const char* tb;
+  const char* safe;
+  int64_t step, K;
+  uint32_t off0[2], dk_bytes;
+  int kb[2];
+  bool mnok[2];
+  __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
+    safe = static_cast<const char*>(op.ptr);
+    tb = safe + M::tile_base(op, r0);
+    step = M::stage_step(op);
+    K = op.K;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int b = tid + 256 * h;
-      const int64_t mn = r0 + (b & 63) * 4;
-      const int64_t kb = k0 + (b >> 6) * 4;
+      kb[h] = (b >> 6) * 4;
+      off0[h] = M::rel(op, (b & 63) * 4, kb[h]);
+      mnok[h] = r0 + (b & 63) * 4 < op.rows;
+    }
+    dk_bytes = M::rel(op, (tid & 63) * 4, kb[0] + 1) - off0[0];
+  }
+  __device__ __forceinline__ void load(int64_t kt) {
+    const char* sb = tb + kt * step;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t k0 = kt * M::KT + kb[h];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int64_t k = kb + i;
-        if (mn < op.rows && k < op.K)
-          r[4 * h + i] = *reinterpret_cast<const u32x4*>(base + k * op.ld + mn);
-        else
-          r[4 * h + i] = u32x4{0u, 0u, 0u, 0u};
+        const bool ok = mnok[h] && (k0 + i < K);
+        const u32x4 v = *reinterpret_cast<const u32x4*>(ok ? sb + off0[h] + i * dk_bytes : safe);
+        r[4 * h + i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
       }
     }
   }
@@ -213,24 +326,34 @@ template <> struct Mfma<float> {
 };
 
 template <typename T>
+__device__ __forceinline__ void read_frags(u32x4 (&a)[4], u32x4 (&b)[4], const char* ldsA,
+                                           const char* ldsB, int wm, int wn, int lane, int kk) {
+  const int c = 2 * kk + (lane >> 5);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    a[i] = *reinterpret_cast<const u32x4*>(ldsA + lds_off(wm * 128 + i * 32 + (lane & 31), c));
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    b[j] = *reinterpret_cast<const u32x4*>(ldsB + lds_off(wn * 128 + j * 32 + (lane & 31), c));
+}
+
+// The fragments of slice kk+1 are read while the MFMAs of slice kk run.
+template <typename T>
 __device__ __forceinline__ void mfma_stage(f32x16 (&acc)[4][4], const char* ldsA,
                                            const char* ldsB, int wm, int wn, int lane) {
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-    u32x4 a[4], b[4];
-    const int c = 2 * kk + (lane >> 5);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      a[i] = *reinterpret_cast<const u32x4*>(ldsA + lds_off(wm * 128 + i * 32 + (lane & 31), c));
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      b[j] = *reinterpret_cast<const u32x4*>(ldsB + lds_off(wn * 128 + j * 32 + (lane & 31), c));
-    Mfma<T>::step(acc, a, b);
-  }
+  u32x4 a0[4], b0[4], a1[4], b1[4];
+  read_frags<T>(a0, b0, ldsA, ldsB, wm, wn, lane, 0);
+  read_frags<T>(a1, b1, ldsA, ldsB, wm, wn, lane, 1);
+  Mfma<T>::step(acc, a0, b0);
+  read_frags<T>(a0, b0, ldsA, ldsB, wm, wn, lane, 2);
+  Mfma<T>::step(acc, a1, b1);
+  read_frags<T>(a1, b1, ldsA, ldsB, wm, wn, lane, 3);
+  Mfma<T>::step(acc, a0, b0);
+  Mfma<T>::step(acc, a1, b1);
 }
 
 // Full K loop for the tile at (m0, n0).  `lds` holds kLdsGemm bytes.
-template <typename T, bool AK, bool BK>
+template <typename T, Lay LA, Lay LB>
 __device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B, int64_t m0,
                                               int64_t n0, int64_t K, char* lds,
                                               f32x16 (&acc)[4][4]) {
@@ -248,15 +371,17 @@ __device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-  StageCopy<T, AK> ca;
-  StageCopy<T, BK> cb;
-  ca.load(A, m0, 0, tid);
-  cb.load(B, n0, 0, tid);
+  StageCopy<T, LA> ca;
+  StageCopy<T, LB> cb;
+  ca.init(A, m0, tid);
+  cb.init(B, n0, tid);
+  ca.load(0);
+  cb.load(0);
   ca.store(lds, tid);
   cb.store(lds + kStageBytes, tid);
   if (nk > 1) {
-    ca.load(A, m0, KT, tid);
-    cb.load(B, n0, KT, tid);
+    ca.load(1);
+    cb.load(1);
   }
   __syncthreads();
   for (int64_t kt = 0; kt < nk; ++kt) {
@@ -268,8 +393,8 @@ __device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B
       cb.store(nxt + kStageBytes, tid);
     }
     if (kt + 2 < nk) {
-      ca.load(A, m0, (kt + 2) * KT, tid);
-      cb.load(B, n0, (kt + 2) * KT, tid);
+      ca.load(kt + 2);
+      cb.load(kt + 2);
     }
     __syncthreads();
   }
@@ -286,7 +411,7 @@ __device__ __forceinline__ int acc_col(int wn, int j, int lane) {
 // Generic tiled contraction kernel: Epi provides prologue(m0, n0, extra) to
 // stage per-row data into `extra` LDS before the loop and
 // epilogue(acc, tm, tn, m0, n0, lds, extra) after it.
-template <typename T, bool AK, bool BK, class Epi>
+template <typename T, Lay LA, Lay LB, class Epi>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(Operand A, Operand B, int64_t K,
                                                            int nTm, int nTn, Epi epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + Epi::kLdsExtra];
@@ -296,7 +421,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(Operand A, Operand B,
   char* extra = lds + kLdsGemm;
   epi.prologue(m0, n0, extra);
   f32x16 acc[4][4];
-  gemm_mainloop<T, AK, BK>(A, B, m0, n0, K, lds, acc);
+  gemm_mainloop<T, LA, LB>(A, B, m0, n0, K, lds, acc);
   epi.epilogue(acc, tm, tn, m0, n0, lds, extra);
 }
 
