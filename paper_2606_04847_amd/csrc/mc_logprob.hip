@@ -36,68 +36,74 @@ struct EpiFwd {
   float* part_m;   // [nTn][T]
   float* part_s;   // [nTn][T]
   float* zy;       // [T]: receives z[t, y_t]
-  static constexpr int kLdsExtra = 256 * 4 + 4 * 256 * 4;
+  static constexpr int kLdsExtra = 256 * 4 + 2 * kWavesN * 256 * 4;
 
   __device__ void prologue(int64_t m0, int64_t, char* extra) const {
     int* ys = reinterpret_cast<int*>(extra);
-    const int64_t t = m0 + threadIdx.x;
-    int v = -1;
-    if (t < T) {
-      const int64_t yy = y[t];
-      if (yy >= 0 && yy < V) v = int(yy);
+    for (int i = threadIdx.x; i < kBM; i += kThreads) {
+      const int64_t t = m0 + i;
+      int v = -1;
+      if (t < T) {
+        const int64_t yy = y[t];
+        if (yy >= 0 && yy < V) v = int(yy);
+      }
+      ys[i] = v;
     }
-    ys[threadIdx.x] = v;
   }
 
-  __device__ void epilogue(f32x16 (&acc)[4][4], int, int tn, int64_t m0, int64_t n0, char*,
+  __device__ void epilogue(Acc& acc, int, int tn, int64_t m0, int64_t n0, char*,
                            char* extra) const {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wm = wave_m(), wn = wave_n();
     const int* ys = reinterpret_cast<const int*>(extra);
     float* red = reinterpret_cast<float*>(extra + 1024);   // [m|s][wn][row]
-    const int cbase = int(n0) + wn * 128;
-    const int vlim = int(min<int64_t>(V - cbase, 128));    // valid columns of this wave
+    const int cbase = int(n0) + wn * kWaveCols;
+    const int vlim = int(min<int64_t>(V - cbase, kWaveCols));   // valid columns of this wave
     const int cl = lane & 31;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kTM; ++i) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int r = acc_row(wm, i, e, lane);
         float mx = kNegInf;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < kTN; ++j)
           if (j * 32 + cl < vlim) mx = fmaxf(mx, acc[i][j][e]);
         mx = half_max(mx);
         float s = 0.0f;
         const float mb = mx * kLog2e;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < kTN; ++j)
           if (j * 32 + cl < vlim) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
         s = half_sum(s);
         const int yl = ys[r] - cbase;
-        if (yl >= 0 && yl < 128 && (yl & 31) == cl) {
+        if (yl >= 0 && yl < kWaveCols && (yl & 31) == cl) {
           const int jj = yl >> 5;
           float z = acc[i][0][e];
-          z = jj == 1 ? acc[i][1][e] : z;
-          z = jj == 2 ? acc[i][2][e] : z;
-          z = jj == 3 ? acc[i][3][e] : z;
+#pragma unroll
+          for (int j = 1; j < kTN; ++j) z = jj == j ? acc[i][j][e] : z;
           zy[m0 + r] = z;
         }
         if (cl == 0) {
-          red[(0 * 2 + wn) * 256 + r] = mx;
-          red[(1 * 2 + wn) * 256 + r] = s;
+          red[(0 * kWavesN + wn) * 256 + r] = mx;
+          red[(1 * kWavesN + wn) * 256 + r] = s;
         }
       }
     }
     __syncthreads();
-    const int r = tid;
-    const int64_t t = m0 + r;
-    if (t < T) {
-      const float ma = red[r], mb = red[256 + r];
-      const float sa = red[512 + r], sb = red[768 + r];
-      const float M = fmaxf(ma, mb);
-      float S = sa * __builtin_amdgcn_exp2f((ma - M) * kLog2e);
-      if (mb != kNegInf) S += sb * __builtin_amdgcn_exp2f((mb - M) * kLog2e);
+    for (int r = tid; r < kBM; r += kThreads) {
+      const int64_t t = m0 + r;
+      if (t >= T) continue;
+      float M = red[r];
+#pragma unroll
+      for (int w = 1; w < kWavesN; ++w) M = fmaxf(M, red[w * 256 + r]);
+      float S = 0.0f;
+#pragma unroll
+      for (int w = 0; w < kWavesN; ++w) {
+        const float mw = red[w * 256 + r];
+        if (mw != kNegInf)
+          S += red[(kWavesN + w) * 256 + r] * __builtin_amdgcn_exp2f((mw - M) * kLog2e);
+      }
       part_m[int64_t(tn) * T + t] = M;
       part_s[int64_t(tn) * T + t] = S;
     }
@@ -168,25 +174,27 @@ struct EpiProbs {
   __device__ void prologue(int64_t m0, int64_t, char* extra) const {
     float* l2 = reinterpret_cast<float*>(extra);
     float* g = l2 + 256;
-    const int64_t t = m0 + threadIdx.x;
-    float a = 0.0f, b = 0.0f;
-    if (t < Tn) {
-      const int64_t yy = y[t];
-      a = lse[t] * kLog2e;
-      b = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
+    for (int i = threadIdx.x; i < kBM; i += kThreads) {
+      const int64_t t = m0 + i;
+      float a = 0.0f, b = 0.0f;
+      if (t < Tn) {
+        const int64_t yy = y[t];
+        a = lse[t] * kLog2e;
+        b = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
+      }
+      l2[i] = a;
+      g[i] = b;
     }
-    l2[threadIdx.x] = a;
-    g[threadIdx.x] = b;
   }
 
-  __device__ void epilogue(f32x16 (&acc)[4][4], int, int, int64_t m0, int64_t n0, char*,
+  __device__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char*,
                            char* extra) const {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int lane = threadIdx.x & 63;
+    const int wm = wave_m(), wn = wave_n();
     const float* l2 = reinterpret_cast<const float*>(extra);
     const float* g = l2 + 256;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kTM; ++i) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int r = acc_row(wm, i, e, lane);
@@ -194,7 +202,7 @@ struct EpiProbs {
         if (t >= Tn) continue;
         const float lb = l2[r], gs = g[r];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < kTN; ++j) {
           const int64_t c = n0 + acc_col(wn, j, lane);
           if (c < ld) {
             const float p = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -lb));
@@ -215,19 +223,18 @@ struct EpiStore {
   static constexpr int kLdsExtra = 16;
 
   __device__ void prologue(int64_t, int64_t, char*) const {}
-  __device__ void epilogue(f32x16 (&acc)[4][4], int, int, int64_t m0, int64_t n0, char*,
-                           char*) const {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave & 1, wn = wave >> 1;
+  __device__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char*, char*) const {
+    const int lane = threadIdx.x & 63;
+    const int wm = wave_m(), wn = wave_n();
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kTM; ++i) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int64_t r = m0 + acc_row(wm, i, e, lane);
         if (r >= rows) continue;
         float* crow = C + r * ldc;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < kTN; ++j) {
           const int64_t c = n0 + acc_col(wn, j, lane);
           if (c < cols) {
             float v = acc[i][j][e];

@@ -1,15 +1,17 @@
-// MFMA tile core for gfx950 (CDNA4): a 256 x 256 output tile per workgroup,
-// four wave64s in a 2 x 2 arrangement, each owning 128 x 128 outputs held as
-// 4 x 4 blocks of 32 x 32 fp32 accumulators.
+// MFMA tile core for gfx950 (CDNA4): a 256 x 256 output tile per workgroup of
+// kWavesM x kWavesN wave64s (two waves per SIMD), each owning a
+// kWaveRows x kWaveCols sub-tile held as 32 x 32 fp32 accumulator blocks.
+// With two waves per SIMD, one wave's MFMAs run while the other waits on
+// memory or a barrier.
 //
 // Operands are staged through LDS in a K-contiguous layout: each tile row
 // holds 128 bytes of K (64 bf16 or 32 fp32) as eight 16-byte chunks, and the
-// chunk index is XOR-swizzled with the row so that both the 16-byte writes of
-// the global->LDS copy and the 16-byte fragment reads of the MFMA loop are free
-// of bank conflicts.  An operand that is contiguous along M/N in memory is
-// transposed in registers (8 x 8 bf16 or 4 x 4 fp32 blocks) on its way to LDS,
-// so every contraction runs the same inner loop.  Two LDS stages: the global
-// loads of step k+2 are in flight while step k is multiplied.
+// chunk index is XOR-swizzled with the row so that the 16-byte writes of the
+// global->LDS copy and the 16-byte fragment reads of the MFMA loop avoid bank
+// conflicts.  An operand that is contiguous along M/N in memory is transposed
+// in registers on its way to LDS, so every contraction runs the same inner
+// loop.  Two LDS stages: the global loads of step k+2 are in flight while
+// step k is multiplied.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -21,16 +23,25 @@ typedef __bf16 bf16_t;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 256;                       // tile rows (M)
 constexpr int kBN = 256;                       // tile columns (N)
 constexpr int kRowBytes = 128;                 // K bytes per tile row per stage
-constexpr int kThreads = 256;                  // 4 waves
+constexpr int kWavesM = 4;                     // waves along M
+constexpr int kWavesN = 2;                     // waves along N
+constexpr int kThreads = 64 * kWavesM * kWavesN;
+constexpr int kWaveRows = kBM / kWavesM;       // 64
+constexpr int kWaveCols = kBN / kWavesN;       // 128
+constexpr int kTM = kWaveRows / 32;            // 32-row accumulator blocks per wave
+constexpr int kTN = kWaveCols / 32;            // 32-column accumulator blocks per wave
 constexpr int kStageBytes = kBM * kRowBytes;   // 32 KiB per operand per stage
 constexpr int kLdsGemm = 4 * kStageBytes;      // 2 operands x 2 stages
 constexpr int kGroupM = 8;                     // tile rows per scheduling group
 constexpr int kXcds = 8;                       // MI355X: 8 XCDs, workgroup i -> XCD i % 8
+
+typedef f32x16 Acc[kTM][kTN];
 
 template <typename T> struct Elem;
 template <> struct Elem<bf16_t> { static constexpr int kChunk = 8; };
@@ -133,33 +144,41 @@ __device__ __forceinline__ void tile_of(int bid, int nTm, int nTn, int& tm, int&
 // ---------------------------------------------------------------------------
 // Global -> register -> LDS copy of one 256-row x 128-byte operand stage.
 // Every copy keeps a uniform 64-bit tile base and per-thread 32-bit offsets
-// computed once per tile; an out-of-range chunk is loaded from the operand's
-// first element (always in bounds, even when the whole tile lies past the
-// operand's rows) and replaced by zeros.
+// computed once per tile.  An out-of-range chunk is read from a 16-byte
+// constant of zeros instead: the address is selected, never the loaded value,
+// so nothing waits on a load before its data is needed in LDS.
 // ---------------------------------------------------------------------------
+// (global address space, like the operands, so the selected pointer stays a
+// global one and the copies use global loads; nothing ever writes it)
+static __device__ __attribute__((aligned(16))) uint32_t kZeroChunk[4] = {0u, 0u, 0u, 0u};
+
+__device__ __forceinline__ const char* zero_chunk() {
+  return reinterpret_cast<const char*>(kZeroChunk);
+}
+
 template <typename T, Lay L, bool KC = KContig<L>::value> struct StageCopy;
 
-// K-contiguous: thread owns chunk (tid & 7) of rows (tid >> 3) + 32 i.
+// K-contiguous: thread owns chunk (tid & 7) of rows (tid >> 3) + kPass * i.
 template <typename T, Lay L> struct StageCopy<T, L, true> {
   using M = LayMath<T, L>;
   static constexpr int E = Elem<T>::kChunk;
-  u32x4 r[8];
+  static constexpr int kPass = kThreads / 8;   // rows per pass
+  static constexpr int NL = kBM / kPass;       // loads per thread
+  u32x4 r[NL];
   const char* tb;
-  const char* safe;
   int64_t step, K;
-  uint32_t off[8];
+  uint32_t off[NL];
   uint32_t rowok;
   int kc;
   __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
-    safe = static_cast<const char*>(op.ptr);
-    tb = safe + M::tile_base(op, r0);
+    tb = static_cast<const char*>(op.ptr) + M::tile_base(op, r0);
     step = M::stage_step(op);
     K = op.K;
     kc = (tid & 7) * E;
     rowok = 0;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int dr = (tid >> 3) + 32 * i;
+    for (int i = 0; i < NL; ++i) {
+      const int dr = (tid >> 3) + kPass * i;
       off[i] = M::rel(op, dr, kc);
       if (r0 + dr < op.rows) rowok |= 1u << i;
     }
@@ -168,37 +187,36 @@ template <typename T, Lay L> struct StageCopy<T, L, true> {
     const char* sb = tb + kt * step;
     const bool kok = kt * M::KT + kc < K;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < NL; ++i) {
       const bool ok = kok && ((rowok >> i) & 1u);
-      const u32x4 v = *reinterpret_cast<const u32x4*>(ok ? sb + off[i] : safe);
-      r[i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
+      r[i] = *reinterpret_cast<const u32x4*>(ok ? sb + off[i] : zero_chunk());
     }
   }
   __device__ __forceinline__ void store(char* lds, int tid) const {
     const int c = tid & 7;
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      *reinterpret_cast<u32x4*>(lds + lds_off((tid >> 3) + 32 * i, c)) = r[i];
+    for (int i = 0; i < NL; ++i)
+      *reinterpret_cast<u32x4*>(lds + lds_off((tid >> 3) + kPass * i, c)) = r[i];
   }
 };
 
-// M/N-contiguous bf16: thread owns one 8(k) x 8(mn) block, mn-block tid & 31,
-// k-block tid >> 5; transposed with byte permutes before the LDS write.
+// M/N-contiguous bf16: thread owns an 8(mn) x KB(k) block, mn-block tid & 31,
+// k-block tid >> 5 (KB = 8 with 256 threads, 4 with 512); transposed with
+// byte permutes, written as KB*2-byte pieces of the K-contiguous rows.
 template <Lay L> struct StageCopy<bf16_t, L, false> {
   using M = LayMath<bf16_t, L>;
-  u32x4 r[8];
+  static constexpr int KB = 8 * 256 / kThreads;
+  u32x4 r[KB];
   const char* tb;
-  const char* safe;
   int64_t step, K;
   uint32_t off0, dk_bytes;
   int kb;
   bool mnok;
   __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
-    safe = static_cast<const char*>(op.ptr);
-    tb = safe + M::tile_base(op, r0);
+    tb = static_cast<const char*>(op.ptr) + M::tile_base(op, r0);
     step = M::stage_step(op);
     K = op.K;
-    kb = (tid >> 5) * 8;
+    kb = (tid >> 5) * KB;
     off0 = M::rel(op, (tid & 31) * 8, kb);
     dk_bytes = M::rel(op, (tid & 31) * 8, kb + 1) - off0;
     mnok = r0 + (tid & 31) * 8 < op.rows;
@@ -207,49 +225,55 @@ template <Lay L> struct StageCopy<bf16_t, L, false> {
     const char* sb = tb + kt * step;
     const int64_t k0 = kt * M::KT + kb;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < KB; ++i) {
       const bool ok = mnok && (k0 + i < K);
-      const u32x4 v = *reinterpret_cast<const u32x4*>(ok ? sb + off0 + i * dk_bytes : safe);
-      r[i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
+      r[i] = *reinterpret_cast<const u32x4*>(ok ? sb + off0 + i * dk_bytes : zero_chunk());
     }
   }
   __device__ __forceinline__ void store(char* lds, int tid) const {
     const int row0 = (tid & 31) * 8;
-    const int c = tid >> 5;
+    const int kq = tid >> 5;   // k-block index; KB k values = KB*2 bytes
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      // out[q] packs (k = 2q, k = 2q+1) of column j: low halves for even j,
+      // word q packs (k = 2q, k = 2q+1) of column j: low halves for even j,
       // high halves for odd j.
       const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-      u32x4 out;
-      out[0] = __builtin_amdgcn_perm(r[1][j >> 1], r[0][j >> 1], sel);
-      out[1] = __builtin_amdgcn_perm(r[3][j >> 1], r[2][j >> 1], sel);
-      out[2] = __builtin_amdgcn_perm(r[5][j >> 1], r[4][j >> 1], sel);
-      out[3] = __builtin_amdgcn_perm(r[7][j >> 1], r[6][j >> 1], sel);
-      *reinterpret_cast<u32x4*>(lds + lds_off(row0 + j, c)) = out;
+      const int row = row0 + j;
+      if constexpr (KB == 8) {
+        u32x4 out;
+        out[0] = __builtin_amdgcn_perm(r[1][j >> 1], r[0][j >> 1], sel);
+        out[1] = __builtin_amdgcn_perm(r[3][j >> 1], r[2][j >> 1], sel);
+        out[2] = __builtin_amdgcn_perm(r[5][j >> 1], r[4][j >> 1], sel);
+        out[3] = __builtin_amdgcn_perm(r[7][j >> 1], r[6][j >> 1], sel);
+        *reinterpret_cast<u32x4*>(lds + lds_off(row, kq)) = out;
+      } else {
+        u32x2 out;
+        out[0] = __builtin_amdgcn_perm(r[1][j >> 1], r[0][j >> 1], sel);
+        out[1] = __builtin_amdgcn_perm(r[3][j >> 1], r[2][j >> 1], sel);
+        *reinterpret_cast<u32x2*>(lds + lds_off(row, kq >> 1) + (kq & 1) * 8) = out;
+      }
     }
   }
 };
 
-// M/N-contiguous fp32: two 4(k) x 4(mn) blocks per thread (mn-block b & 63,
-// k-block b >> 6 for b = tid, tid + 256), transposed by register moves.
+// M/N-contiguous fp32: 4(k) x 4(mn) blocks (mn-block b & 63, k-block b >> 6),
+// kThreads/... per thread, transposed by register moves.
 template <Lay L> struct StageCopy<float, L, false> {
   using M = LayMath<float, L>;
-  u32x4 r[8];
+  static constexpr int NB = 512 / kThreads;   // blocks per thread
+  u32x4 r[4 * NB];
   const char* tb;
-  const char* safe;
   int64_t step, K;
-  uint32_t off0[2], dk_bytes;
-  int kb[2];
-  bool mnok[2];
+  uint32_t off0[NB], dk_bytes;
+  int kb[NB];
+  bool mnok[NB];
   __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
-    safe = static_cast<const char*>(op.ptr);
-    tb = safe + M::tile_base(op, r0);
+    tb = static_cast<const char*>(op.ptr) + M::tile_base(op, r0);
     step = M::stage_step(op);
     K = op.K;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int b = tid + 256 * h;
+    for (int h = 0; h < NB; ++h) {
+      const int b = tid + kThreads * h;
       kb[h] = (b >> 6) * 4;
       off0[h] = M::rel(op, (b & 63) * 4, kb[h]);
       mnok[h] = r0 + (b & 63) * 4 < op.rows;
@@ -259,20 +283,20 @@ template <Lay L> struct StageCopy<float, L, false> {
   __device__ __forceinline__ void load(int64_t kt) {
     const char* sb = tb + kt * step;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < NB; ++h) {
       const int64_t k0 = kt * M::KT + kb[h];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const bool ok = mnok[h] && (k0 + i < K);
-        const u32x4 v = *reinterpret_cast<const u32x4*>(ok ? sb + off0[h] + i * dk_bytes : safe);
-        r[4 * h + i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
+        r[4 * h + i] =
+            *reinterpret_cast<const u32x4*>(ok ? sb + off0[h] + i * dk_bytes : zero_chunk());
       }
     }
   }
   __device__ __forceinline__ void store(char* lds, int tid) const {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int b = tid + 256 * h;
+    for (int h = 0; h < NB; ++h) {
+      const int b = tid + kThreads * h;
       const int row0 = (b & 63) * 4;
       const int c = b >> 6;
 #pragma unroll
@@ -285,19 +309,19 @@ template <Lay L> struct StageCopy<float, L, false> {
 };
 
 // ---------------------------------------------------------------------------
-// One 128-byte K stage of MFMA work for this wave's 128 x 128 sub-tile.
-// Lane l supplies row (l & 31) of each 32-row block and K-chunk (l >> 5) of
-// each 32-byte K slice; A and B use the same lane -> k assignment.
+// One 128-byte K stage of MFMA work for this wave's sub-tile.  Lane l
+// supplies row (l & 31) of each 32-row block and K-chunk (l >> 5) of each
+// 32-byte K slice; A and B use the same lane -> k assignment.
 // ---------------------------------------------------------------------------
 template <typename T> struct Mfma;
 
 template <> struct Mfma<bf16_t> {
-  __device__ __forceinline__ static void step(f32x16 (&acc)[4][4], const u32x4 (&a)[4],
-                                              const u32x4 (&b)[4]) {
+  __device__ __forceinline__ static void step(Acc& acc, const u32x4 (&a)[kTM],
+                                              const u32x4 (&b)[kTN]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < kTM; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < kTN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             __builtin_bit_cast(bf16x8, a[i]), __builtin_bit_cast(bf16x8, b[j]), acc[i][j], 0, 0, 0);
   }
@@ -307,41 +331,42 @@ template <> struct Mfma<bf16_t> {
 // (The chunks are bit-cast to float vectors as a whole: bit-casting a single
 // element of an integer vector compiles to element 0 with this toolchain.)
 template <> struct Mfma<float> {
-  __device__ __forceinline__ static void step(f32x16 (&acc)[4][4], const u32x4 (&a)[4],
-                                              const u32x4 (&b)[4]) {
-    f32x4 af[4], bf[4];
+  __device__ __forceinline__ static void step(Acc& acc, const u32x4 (&a)[kTM],
+                                              const u32x4 (&b)[kTN]) {
+    f32x4 af[kTM], bf[kTN];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      af[i] = __builtin_bit_cast(f32x4, a[i]);
-      bf[i] = __builtin_bit_cast(f32x4, b[i]);
-    }
+    for (int i = 0; i < kTM; ++i) af[i] = __builtin_bit_cast(f32x4, a[i]);
+#pragma unroll
+    for (int j = 0; j < kTN; ++j) bf[j] = __builtin_bit_cast(f32x4, b[j]);
 #pragma unroll
     for (int e = 0; e < 4; ++e)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kTM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < kTN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][e], bf[j][e], acc[i][j], 0, 0, 0);
   }
 };
 
 template <typename T>
-__device__ __forceinline__ void read_frags(u32x4 (&a)[4], u32x4 (&b)[4], const char* ldsA,
+__device__ __forceinline__ void read_frags(u32x4 (&a)[kTM], u32x4 (&b)[kTN], const char* ldsA,
                                            const char* ldsB, int wm, int wn, int lane, int kk) {
   const int c = 2 * kk + (lane >> 5);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    a[i] = *reinterpret_cast<const u32x4*>(ldsA + lds_off(wm * 128 + i * 32 + (lane & 31), c));
+  for (int i = 0; i < kTM; ++i)
+    a[i] = *reinterpret_cast<const u32x4*>(
+        ldsA + lds_off(wm * kWaveRows + i * 32 + (lane & 31), c));
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-    b[j] = *reinterpret_cast<const u32x4*>(ldsB + lds_off(wn * 128 + j * 32 + (lane & 31), c));
+  for (int j = 0; j < kTN; ++j)
+    b[j] = *reinterpret_cast<const u32x4*>(
+        ldsB + lds_off(wn * kWaveCols + j * 32 + (lane & 31), c));
 }
 
 // The fragments of slice kk+1 are read while the MFMAs of slice kk run.
 template <typename T>
-__device__ __forceinline__ void mfma_stage(f32x16 (&acc)[4][4], const char* ldsA,
-                                           const char* ldsB, int wm, int wn, int lane) {
-  u32x4 a0[4], b0[4], a1[4], b1[4];
+__device__ __forceinline__ void mfma_stage(Acc& acc, const char* ldsA, const char* ldsB, int wm,
+                                           int wn, int lane) {
+  u32x4 a0[kTM], b0[kTN], a1[kTM], b1[kTN];
   read_frags<T>(a0, b0, ldsA, ldsB, wm, wn, lane, 0);
   read_frags<T>(a1, b1, ldsA, ldsB, wm, wn, lane, 1);
   Mfma<T>::step(acc, a0, b0);
@@ -355,19 +380,18 @@ __device__ __forceinline__ void mfma_stage(f32x16 (&acc)[4][4], const char* ldsA
 // Full K loop for the tile at (m0, n0).  `lds` holds kLdsGemm bytes.
 template <typename T, Lay LA, Lay LB>
 __device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B, int64_t m0,
-                                              int64_t n0, int64_t K, char* lds,
-                                              f32x16 (&acc)[4][4]) {
+                                              int64_t n0, int64_t K, char* lds, Acc& acc) {
   constexpr int KT = kRowBytes / sizeof(T);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave % kWavesM, wn = wave / kWavesM;
   const int64_t nk = (K + KT - 1) / KT;
 
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < kTM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < kTN; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
@@ -400,12 +424,15 @@ __device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B
   }
 }
 
-// Row / column of accumulator element e of block (i, j) held by this lane.
+// This lane's wave coordinates, and the row / column (within the tile) of
+// accumulator element e of block (i, j).
+__device__ __forceinline__ int wave_m() { return (threadIdx.x >> 6) % kWavesM; }
+__device__ __forceinline__ int wave_n() { return (threadIdx.x >> 6) / kWavesM; }
 __device__ __forceinline__ int acc_row(int wm, int i, int e, int lane) {
-  return wm * 128 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+  return wm * kWaveRows + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
 }
 __device__ __forceinline__ int acc_col(int wn, int j, int lane) {
-  return wn * 128 + j * 32 + (lane & 31);
+  return wn * kWaveCols + j * 32 + (lane & 31);
 }
 
 // Generic tiled contraction kernel: Epi provides prologue(m0, n0, extra) to
@@ -420,7 +447,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(Operand A, Operand B,
   const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
   char* extra = lds + kLdsGemm;
   epi.prologue(m0, n0, extra);
-  f32x16 acc[4][4];
+  Acc acc;
   gemm_mainloop<T, LA, LB>(A, B, m0, n0, K, lds, acc);
   epi.epilogue(acc, tm, tn, m0, n0, lds, extra);
 }
