@@ -27,8 +27,10 @@ struct Carve {
 };
 
 // Vocabulary chunk width of the backward: the transient [T x chunk] softmax
-// operand stays within kBwdChunkBytes.
-constexpr size_t kBwdChunkBytes = size_t(4) << 30;
+// operand stays within kBwdChunkBytes (sized for 288 GB of HBM: the
+// 16384 x 151936 bf16 operand of the headline shape is one 5 GB chunk);
+// larger problems are split into equal chunks, multiples of 256 columns.
+constexpr size_t kBwdChunkBytes = size_t(8) << 30;
 int64_t bwd_chunk_cols(int64_t T, int64_t V, size_t esize);
 
 // RAII timing scope around one or more launches on `s` (see mc_profiler_*).

@@ -473,10 +473,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
 
 int64_t bwd_chunk_cols(int64_t T, int64_t V, size_t esize) {
   const int64_t per_col = std::max<int64_t>(1, T) * int64_t(esize);
-  int64_t c = int64_t(kBwdChunkBytes) / per_col;
-  c = c / kBN * kBN;
-  if (c < kBN) c = kBN;
-  return c >= V ? V : c;
+  int64_t cap = int64_t(kBwdChunkBytes) / per_col;
+  cap = std::max<int64_t>(kBN, cap / kBN * kBN);
+  if (cap >= V) return V;
+  const int64_t n = cdiv(V, cap);
+  return std::min(cap, cdiv(cdiv(V, n), kBN) * kBN);
 }
 
 size_t fwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t) {

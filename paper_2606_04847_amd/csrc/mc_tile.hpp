@@ -29,8 +29,14 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kBM = 256;                       // tile rows (M)
 constexpr int kBN = 256;                       // tile columns (N)
 constexpr int kRowBytes = 128;                 // K bytes per tile row per stage
-constexpr int kWavesM = 4;                     // waves along M
-constexpr int kWavesN = 2;                     // waves along N
+#ifndef MC_WAVES_M
+#define MC_WAVES_M 4
+#endif
+#ifndef MC_WAVES_N
+#define MC_WAVES_N 2
+#endif
+constexpr int kWavesM = MC_WAVES_M;            // waves along M
+constexpr int kWavesN = MC_WAVES_N;            // waves along N
 constexpr int kThreads = 64 * kWavesM * kWavesN;
 constexpr int kWaveRows = kBM / kWavesM;       // 64
 constexpr int kWaveCols = kBN / kWavesN;       // 128
@@ -362,7 +368,7 @@ __device__ __forceinline__ void read_frags(u32x4 (&a)[kTM], u32x4 (&b)[kTN], con
         ldsB + lds_off(wn * kWaveCols + j * 32 + (lane & 31), c));
 }
 
-// The fragments of slice kk+1 are read while the MFMAs of slice kk run.
+// The fragments of slice kk+1 are requested before the MFMAs of slice kk.
 template <typename T>
 __device__ __forceinline__ void mfma_stage(Acc& acc, const char* ldsA, const char* ldsB, int wm,
                                            int wn, int lane) {
