@@ -353,6 +353,32 @@ __global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
   }
 }
 
+// Named kernels, one per role of the shared tile core.
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void k_fwd_logits_lse(Operand A, Operand B, int64_t K,
+                                                                int nTm, int nTn, EpiFwd epi) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiFwd::kLdsExtra];
+  gemm_body<T, Lay::KMajor, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
+}
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B, int64_t K,
+                                                           int nTm, int nTn, EpiProbs<T> epi) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiProbs<T>::kLdsExtra];
+  gemm_body<T, Lay::KMajor, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
+}
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand B, int64_t K,
+                                                             int nTm, int nTn, EpiStore epi) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiStore::kLdsExtra];
+  gemm_body<T, Lay::TileTK, Lay::MNMajor>(A, B, K, nTm, nTn, epi, lds);
+}
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand B, int64_t K,
+                                                             int nTm, int nTn, EpiStore epi) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiStore::kLdsExtra];
+  gemm_body<T, Lay::TileVT, Lay::MNMajor>(A, B, K, nTm, nTn, epi, lds);
+}
+
 template <typename T>
 hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_t d,
                     int64_t V, float* logp, float* lse, void* ws, hipStream_t s) {
@@ -369,8 +395,7 @@ hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_
   {
     ProfScope ps_(s, "logprob_fwd_gemm", 2.0 * Tn * d * V,
                   es * (double(Tn) * d + double(V) * d) + 12.0 * Tn);
-    hipLaunchKernelGGL((gemm_kernel<T, Lay::KMajor, Lay::KMajor, EpiFwd>), dim3(nTm * nTn),
-                       dim3(kThreads), 0,
+    hipLaunchKernelGGL(k_fwd_logits_lse<T>, dim3(nTm * nTn), dim3(kThreads), 0,
                        s, A, B, d, nTm, nTn, epi);
   }
   {
@@ -426,7 +451,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       const int nTn = int(cdiv(ldc, kBN));
       ProfScope ps_(s, "logprob_bwd_probs", 2.0 * Tn * d * width,
                     es * (double(Tn) * d + double(width) * d + double(Tn) * width) + 16.0 * Tn);
-      hipLaunchKernelGGL((gemm_kernel<T, Lay::KMajor, Lay::KMajor, EpiProbs<T>>), dim3(nTm * nTn),
+      hipLaunchKernelGGL(k_bwd_probs<T>, dim3(nTm * nTn),
                          dim3(kThreads), 0, s, A, B, d, nTm, nTn, epi);
     }
     if (dH) {
@@ -439,7 +464,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       ProfScope ps_(s, "logprob_bwd_dhidden", 2.0 * Tn * d * width,
                     es * (double(Tn) * width + double(width) * d) +
                         4.0 * Tn * d * (epi.accumulate ? 2 : 1));
-      hipLaunchKernelGGL((gemm_kernel<T, Lay::TileTK, Lay::MNMajor, EpiStore>), dim3(nTm * nTd),
+      hipLaunchKernelGGL(k_bwd_dhidden<T>, dim3(nTm * nTd),
                          dim3(kThreads), 0, s, A, B, ldc, nTm, nTd, epi);
     }
     if (dW) {
@@ -453,7 +478,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       ProfScope ps_(s, "logprob_bwd_dweight", 2.0 * Tn * d * width,
                     es * (double(Tn) * width + double(Tn) * d) +
                         4.0 * width * d * (epi.accumulate ? 2 : 1));
-      hipLaunchKernelGGL((gemm_kernel<T, Lay::TileVT, Lay::MNMajor, EpiStore>), dim3(nTv * nTd),
+      hipLaunchKernelGGL(k_bwd_dweight<T>, dim3(nTv * nTd),
                          dim3(kThreads), 0, s, A, B, Tn, nTv, nTd, epi);
     }
   }

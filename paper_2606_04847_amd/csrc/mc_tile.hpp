@@ -441,13 +441,13 @@ __device__ __forceinline__ int acc_col(int wn, int j, int lane) {
   return wn * kWaveCols + j * 32 + (lane & 31);
 }
 
-// Generic tiled contraction kernel: Epi provides prologue(m0, n0, extra) to
-// stage per-row data into `extra` LDS before the loop and
-// epilogue(acc, tm, tn, m0, n0, lds, extra) after it.
+// Body of every tiled contraction kernel: Epi provides prologue(m0, n0,
+// extra) to stage per-row data into `extra` LDS before the loop and
+// epilogue(acc, tm, tn, m0, n0, lds, extra) after it.  Each use is wrapped in
+// a __global__ function of its own name (so profiles name the role).
 template <typename T, Lay LA, Lay LB, class Epi>
-__global__ __launch_bounds__(kThreads, 1) void gemm_kernel(Operand A, Operand B, int64_t K,
-                                                           int nTm, int nTn, Epi epi) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + Epi::kLdsExtra];
+__device__ __forceinline__ void gemm_body(const Operand& A, const Operand& B, int64_t K, int nTm,
+                                          int nTn, const Epi& epi, char* lds) {
   int tm, tn;
   tile_of(blockIdx.x, nTm, nTn, tm, tn);
   const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
