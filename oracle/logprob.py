@@ -57,6 +57,18 @@ def logprob_fwd(H, W, y):
     return logp, lse
 
 
+def token_entropy(H, W):
+    """Entropy of the model's next-token distribution at each row,
+    -sum_v p_tv log p_tv (the entropy diagnostic of the MirrorPop ablation,
+    Sec. 5.4), from the same two-pass log-sum-exp."""
+    H64 = np.asarray(H, dtype=np.float64)
+    z = _logits(H64, W)
+    m = z.max(axis=1)
+    lse = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+    logq = z - lse[:, None]
+    return -(np.exp(logq) * logq).sum(axis=1)
+
+
 def _grad_logits(z, y, lse, dlogp, V, cols=None):
     """G restricted to the given vocabulary columns (all when None)."""
     T = z.shape[0]

@@ -37,6 +37,14 @@ a convention; the paper prints no number that pins them):
       rho A <= clip(rho) A (ties count as unclipped); the clipped branch has
       zero gradient.  No gradient flows through M_i, S_i or A_i.
   R10 the filter "none" keeps every sequence with L_i > 0 (plain Eq. 5).
+  R11 the KL term beta * D_KL(pi_theta || pi_ref) of Eq. 5 / Eq. 17: the paper
+      names neither beta nor the estimator.  Reading: the per-token
+      estimator k3 = exp(r) - r - 1 with r = logp_ref - logp (non-negative,
+      zero iff the policies agree on the token), averaged with the same
+      token mean as the surrogate, (1/N) sum_i M_i sum_t mask_t k3_t.  Its
+      gradient is d k3 / d logp = 1 - exp(r).  Parity of this estimator with
+      the paper is unpinned (the paper prints none); its arithmetic is pinned
+      by closed forms and finite differences.
 """
 from __future__ import annotations
 
@@ -56,6 +64,7 @@ class RLParams:
     adv_eps: float = 1e-6
     std_ddof: int = 0
     filter: str = "mirrorpop"
+    kl_beta: float = 0.0
 
 
 def _advantages(rewards, cu_groups, p: RLParams) -> np.ndarray:
@@ -77,7 +86,7 @@ def _advantages(rewards, cu_groups, p: RLParams) -> np.ndarray:
 
 
 def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
-            params: RLParams | None = None) -> dict:
+            params: RLParams | None = None, logp_ref=None) -> dict:
     p = params or RLParams()
     if p.filter not in FILTERS:
         raise ValueError(p.filter)
@@ -119,7 +128,11 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
     lo, hi = 1.0 - p.eps_low, 1.0 + p.eps_high
     dlogp = np.zeros(T, dtype=np.float64)
     total = 0.0
+    kl_total = 0.0
     n_clipped = 0
+    use_kl = logp_ref is not None and p.kl_beta != 0.0
+    if use_kl:
+        logp_ref = np.asarray(logp_ref, dtype=np.float64)
     for i in range(B):
         if not keep[i]:
             continue
@@ -134,13 +147,20 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
                 dlogp[t] = unclipped                      # d(rho A)/d ell = rho A
             else:
                 n_clipped += 1
+            if use_kl:                                    # R11
+                r = logp_ref[t] - logp[t]
+                kl_total += math.exp(r) - r - 1.0
+                # loss carries +beta k3 against the -(...) surrogate: undo the
+                # common -1/N below with a minus sign here
+                dlogp[t] -= p.kl_beta * (1.0 - math.exp(r))
     if N > 0:
-        loss = -total / N
+        loss = -total / N + (p.kl_beta * kl_total / N if use_kl else 0.0)
         dlogp *= -1.0 / N
         clip_frac = n_clipped / N
+        kl = kl_total / N
     else:                                                 # R8
-        loss, clip_frac = 0.0, 0.0
+        loss, clip_frac, kl = 0.0, 0.0, 0.0
         dlogp[:] = 0.0
     return dict(loss=loss, dlogp=dlogp, seq_mask=keep.astype(np.uint8),
                 seq_len=seq_len.astype(np.int32), n_valid=N, adv=A,
-                stat_abs=stat_abs, stat_signed=stat_signed, clip_frac=clip_frac)
+                stat_abs=stat_abs, stat_signed=stat_signed, clip_frac=clip_frac, kl=kl)
