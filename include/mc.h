@@ -73,6 +73,8 @@ typedef struct {
   float adv_eps;            /* epsilon added to the group std (Eq. 3), >= 0 */
   int32_t std_ddof;         /* 0: population std, 1: sample std */
   int32_t filter;           /* an mc_filter_t */
+  float kl_beta;            /* weight beta of the KL term of Eq. 5/17 (>= 0); used only
+                               when a reference log-prob array is passed */
 } mc_rl_params_t;
 
 /* Outputs of mc_rl_loss (host struct holding device pointers).  `loss` and
@@ -88,6 +90,7 @@ typedef struct {
   float* stat_signed;       /* [B]  (1/L_i) sum_t log rho_t    (log of Eq. 18's statistic) */
   float* clip_frac;         /* [1]  share of the N tokens on the clipped branch */
   int32_t* error_flag;      /* [1]  set to 1 when cu_seqlens/cu_groups are inconsistent */
+  float* kl;                /* [1]  (1/N) sum_i M_i sum_t k3_t (0 without a reference) */
 } mc_rl_outputs_t;
 
 /* Flags of mc_logprob_bwd. */
@@ -112,13 +115,38 @@ const char* mc_version(void);
  *                                  token: logp = 0 there and it gets no gradient
  *   logp     [T]     fp32 (out)
  *   lse      [T]     fp32 (out)    kept for the backward
+ *   entropy  [T]     fp32 (out)    optional (NULL to skip): -sum_v p log p of the
+ *                                  row's softmax, the entropy diagnostic of the
+ *                                  MirrorPop ablation (Sec. 5.4), from one extra
+ *                                  running sum in the same epilogue
  * T = 0 is a valid no-op.  T >= 0, d >= 8, d % 8 == 0, V >= 1.
  * ------------------------------------------------------------------------ */
 size_t mc_logprob_fwd_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dtype);
 mc_status_t mc_logprob_fwd(const void* hidden, const void* weight, const int64_t* targets,
                            int64_t T, int64_t d, int64_t V, mc_dtype_t dtype,
-                           float* logp, float* lse,
+                           float* logp, float* lse, float* entropy,
                            void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Vocabulary-sharded forward (the one-GPU part of a tensor-parallel LM head,
+ * Sec. 5.1): this call sees the shard weight[V_shard, d] holding vocabulary
+ * entries [v_offset, v_offset + V_shard) and writes, per row, the shard's
+ * partial[4][T] = (max_v z, sum_v exp(z - max), sum_v exp(z - max) z,
+ * z[t, y_t] if y_t is in the shard else -inf), fp32.  Targets are global
+ * indices.  Workspace: mc_logprob_fwd_workspace_size(T, d, V_shard, dtype).
+ * mc_logprob_merge_shards folds S such partials (partials[S][4][T], shard
+ * order; gathered from the shards by the caller) into logp, lse and
+ * (optionally) entropy, exactly as the unsharded forward defines them;
+ * V_total is the full vocabulary size (targets outside it are ignored).
+ * ------------------------------------------------------------------------ */
+mc_status_t mc_logprob_fwd_shard(const void* hidden, const void* weight_shard,
+                                 const int64_t* targets, int64_t T, int64_t d, int64_t V_shard,
+                                 int64_t v_offset, int64_t V_total, mc_dtype_t dtype,
+                                 float* partial, void* workspace, size_t workspace_bytes,
+                                 void* stream);
+mc_status_t mc_logprob_merge_shards(const float* partials, int32_t S, const int64_t* targets,
+                                    int64_t T, int64_t V_total, float* logp, float* lse,
+                                    float* entropy, void* stream);
 
 /* ------------------------------------------------------------------------
  * Backward of the forward above for an upstream gradient dlogp[t]:
@@ -139,11 +167,28 @@ mc_status_t mc_logprob_bwd(const void* hidden, const void* weight, const int64_t
                            float* dhidden, float* dweight, int32_t flags,
                            void* workspace, size_t workspace_bytes, void* stream);
 
+/* Backward on a vocabulary shard (see mc_logprob_fwd_shard): with the global
+ * lse of the merged forward, dhidden receives this shard's part of G . W
+ * (the shards' parts sum to the full dhidden) and dweight_shard[V_shard, d]
+ * the shard's rows of dW.  Workspace:
+ * mc_logprob_bwd_workspace_size(T, d, V_shard, dtype). */
+mc_status_t mc_logprob_bwd_shard(const void* hidden, const void* weight_shard,
+                                 const int64_t* targets, const float* lse, const float* dlogp,
+                                 int64_t T, int64_t d, int64_t V_shard, int64_t v_offset,
+                                 int64_t V_total, mc_dtype_t dtype, float* dhidden,
+                                 float* dweight_shard, int32_t flags, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------
- * RL objective over a packed ragged batch (Eq. 3/12, 4, 17-21; beta = 0).
+ * RL objective over a packed ragged batch (Eq. 3/12, 4, 17-21).
  *   logp          [T]    fp32   trainer log-probs (from mc_logprob_fwd)
  *   logp_rollout  [T]    fp32   rollout log-probs of the same tokens
  *                               (ignored where loss_mask is 0)
+ *   logp_ref      [T]    fp32   reference-policy log-probs for the KL term of
+ *                               Eq. 5/17, or NULL for beta = 0.  The paper
+ *                               names no estimator; the term is
+ *                               kl_beta * (1/N) sum_i M_i sum_t k3_t with
+ *                               k3 = exp(r) - r - 1, r = logp_ref - logp
  *   loss_mask     [T]    u8     1 = token counts (e.g. first-turn response
  *                               tokens); NULL = all tokens count
  *   cu_seqlens    [B+1]  int32  sequence i is rows [cu_seqlens[i], cu_seqlens[i+1]);
@@ -158,11 +203,24 @@ mc_status_t mc_logprob_bwd(const void* hidden, const void* weight, const int64_t
  * outputs are then unspecified.  mc_check_packing validates host copies.
  * ------------------------------------------------------------------------ */
 size_t mc_rl_loss_workspace_size(int64_t T, int32_t B, int32_t NG);
-mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const uint8_t* loss_mask,
+mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const float* logp_ref,
+                       const uint8_t* loss_mask,
                        const int32_t* cu_seqlens, const int32_t* cu_groups,
                        const float* rewards, int64_t T, int32_t B, int32_t NG,
                        const mc_rl_params_t* params, const mc_rl_outputs_t* out,
                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* PrimeEcho trajectory rewards (Sec. 4.4.3, Eq. 9-10), one per trajectory:
+ *   R_i = alpha s_i1 + (1 - alpha) max_{k <= K_i} s_ik
+ *         + beta1 [success_i1] + beta2 [not success_i1 and success_i2]
+ *   scores   [B][Kmax] fp32   turn scores s_ik
+ *   success  [B][Kmax] u8     turn verified (NULL: no early-success bonus)
+ *   n_turns  [B]       int32  K_i, clamped into [1, Kmax] (NULL: all Kmax)
+ *   rewards  [B]       fp32 (out), to pass to mc_rl_loss (Eq. 12)
+ * 0 <= alpha <= 1 (the paper's default is 0.75), beta1, beta2 finite. */
+mc_status_t mc_primeecho_rewards(const float* scores, const uint8_t* success,
+                                 const int32_t* n_turns, int32_t B, int32_t Kmax, float alpha,
+                                 float beta1, float beta2, float* rewards, void* stream);
 
 /* Host-side check of packing metadata (host arrays): MC_OK when cu_seqlens and
  * cu_groups satisfy the rules stated for mc_rl_loss, MC_ERR_INVALID_ARG

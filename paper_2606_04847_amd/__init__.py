@@ -10,7 +10,11 @@ from .binding import (  # noqa: F401
     check_packing,
     load_library,
     logprob_bwd,
+    logprob_bwd_shard,
     logprob_fwd,
+    logprob_fwd_shard,
+    logprob_merge_shards,
+    primeecho_rewards,
     profiler_enable,
     profiler_read,
     profiler_reset,

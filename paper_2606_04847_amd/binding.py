@@ -26,12 +26,16 @@ _c_i64, _c_i32, _c_sz, _vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t, ct
 class RLParamsC(ctypes.Structure):
     _fields_ = [("eps_low", ctypes.c_float), ("eps_high", ctypes.c_float),
                 ("delta", ctypes.c_float), ("adv_eps", ctypes.c_float),
-                ("std_ddof", ctypes.c_int32), ("filter", ctypes.c_int32)]
+                ("std_ddof", ctypes.c_int32), ("filter", ctypes.c_int32),
+                ("kl_beta", ctypes.c_float)]
+
+
+_OUT_FIELDS = ("loss", "dlogp", "seq_mask", "seq_len", "n_valid", "adv", "stat_abs",
+               "stat_signed", "clip_frac", "error_flag", "kl")
 
 
 class RLOutputsC(ctypes.Structure):
-    _fields_ = [(n, _vp) for n in ("loss", "dlogp", "seq_mask", "seq_len", "n_valid", "adv",
-                                   "stat_abs", "stat_signed", "clip_frac", "error_flag")]
+    _fields_ = [(n, _vp) for n in _OUT_FIELDS]
 
 
 class KernelTimeC(ctypes.Structure):
@@ -48,10 +52,11 @@ class RLParams:
     adv_eps: float = 1e-6
     std_ddof: int = 0
     filter: str = "mirrorpop"
+    kl_beta: float = 0.0
 
     def to_c(self) -> RLParamsC:
         return RLParamsC(self.eps_low, self.eps_high, self.delta, self.adv_eps,
-                         int(self.std_ddof), MC_FILTER[self.filter])
+                         int(self.std_ddof), MC_FILTER[self.filter], self.kl_beta)
 
 
 class MCError(RuntimeError):
@@ -84,14 +89,26 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mc_rl_loss_workspace_size.argtypes = [_c_i64, _c_i32, _c_i32]
     lib.mc_logprob_fwd.restype = ctypes.c_int
     lib.mc_logprob_fwd.argtypes = [_vp, _vp, _vp, _c_i64, _c_i64, _c_i64, ctypes.c_int,
-                                   _vp, _vp, _vp, _c_sz, _vp]
+                                   _vp, _vp, _vp, _vp, _c_sz, _vp]
+    lib.mc_logprob_fwd_shard.restype = ctypes.c_int
+    lib.mc_logprob_fwd_shard.argtypes = [_vp, _vp, _vp, _c_i64, _c_i64, _c_i64, _c_i64, _c_i64,
+                                         ctypes.c_int, _vp, _vp, _c_sz, _vp]
+    lib.mc_logprob_merge_shards.restype = ctypes.c_int
+    lib.mc_logprob_merge_shards.argtypes = [_vp, _c_i32, _vp, _c_i64, _c_i64, _vp, _vp, _vp, _vp]
     lib.mc_logprob_bwd.restype = ctypes.c_int
     lib.mc_logprob_bwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _c_i64,
                                    ctypes.c_int, _vp, _vp, _c_i32, _vp, _c_sz, _vp]
+    lib.mc_logprob_bwd_shard.restype = ctypes.c_int
+    lib.mc_logprob_bwd_shard.argtypes = [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _c_i64,
+                                         _c_i64, _c_i64, ctypes.c_int, _vp, _vp, _c_i32, _vp,
+                                         _c_sz, _vp]
     lib.mc_rl_loss.restype = ctypes.c_int
-    lib.mc_rl_loss.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i32, _c_i32,
+    lib.mc_rl_loss.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i32, _c_i32,
                                ctypes.POINTER(RLParamsC), ctypes.POINTER(RLOutputsC),
                                _vp, _c_sz, _vp]
+    lib.mc_primeecho_rewards.restype = ctypes.c_int
+    lib.mc_primeecho_rewards.argtypes = [_vp, _vp, _vp, _c_i32, _c_i32, ctypes.c_float,
+                                         ctypes.c_float, ctypes.c_float, _vp, _vp]
     lib.mc_check_packing.restype = ctypes.c_int
     lib.mc_check_packing.argtypes = [_vp, _c_i32, _vp, _c_i32, _c_i64]
     lib.mc_profiler_enable.restype = None
@@ -160,11 +177,13 @@ def _need(cond, msg):
         raise ValueError(msg)
 
 
-def logprob_fwd(hidden, weight, targets, *, logp=None, lse=None, workspace=None, stream=None):
+def logprob_fwd(hidden, weight, targets, *, logp=None, lse=None, entropy=None,
+                with_entropy=False, workspace=None, stream=None):
     """Per-token log-prob over the full vocabulary (see mc_logprob_fwd).
 
     hidden [T,d] and weight [V,d] bf16 or fp32 (same dtype), targets [T] int64,
-    all on one GPU.  Returns (logp, lse), fp32 [T]."""
+    all on one GPU.  Returns (logp, lse), fp32 [T], or (logp, lse, entropy)
+    when with_entropy is set."""
     torch = _torch()
     lib = load_library()
     _need(hidden.is_cuda and weight.is_cuda and targets.is_cuda, "tensors must be on the GPU")
@@ -179,12 +198,98 @@ def logprob_fwd(hidden, weight, targets, *, logp=None, lse=None, workspace=None,
     dev = hidden.device
     logp = torch.empty(T, dtype=torch.float32, device=dev) if logp is None else logp
     lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
+    if with_entropy and entropy is None:
+        entropy = torch.empty(T, dtype=torch.float32, device=dev)
     need = lib.mc_logprob_fwd_workspace_size(T, d, V, dt)
     ws, nbytes = _workspace(need, dev, workspace)
     _check(lib.mc_logprob_fwd(_ptr(hidden), _ptr(weight), _ptr(targets), T, d, V, dt,
-                              _ptr(logp), _ptr(lse), _ptr(ws), nbytes, _stream(stream)),
-           "mc_logprob_fwd")
-    return logp, lse
+                              _ptr(logp), _ptr(lse), _ptr(entropy), _ptr(ws), nbytes,
+                              _stream(stream)), "mc_logprob_fwd")
+    return (logp, lse, entropy) if entropy is not None else (logp, lse)
+
+
+def logprob_fwd_shard(hidden, weight_shard, targets, v_offset, V_total, *, partial=None,
+                      workspace=None, stream=None):
+    """Partial forward on a vocabulary shard (see mc_logprob_fwd_shard).
+    Returns partial [4, T] fp32: (max, sum exp, sum exp*z, target logit or -inf)."""
+    torch = _torch()
+    lib = load_library()
+    T, d = hidden.shape
+    Vs = weight_shard.shape[0]
+    _need(hidden.dtype == weight_shard.dtype and targets.dtype == torch.int64, "dtypes")
+    for t in (hidden, weight_shard, targets):
+        _need(t.is_cuda and t.is_contiguous(), "contiguous GPU tensors")
+    dt = _dtype_code(hidden)
+    dev = hidden.device
+    partial = torch.empty(4, T, dtype=torch.float32, device=dev) if partial is None else partial
+    need = lib.mc_logprob_fwd_workspace_size(T, d, Vs, dt)
+    ws, nbytes = _workspace(need, dev, workspace)
+    _check(lib.mc_logprob_fwd_shard(_ptr(hidden), _ptr(weight_shard), _ptr(targets), T, d, Vs,
+                                    int(v_offset), int(V_total), dt, _ptr(partial), _ptr(ws),
+                                    nbytes, _stream(stream)), "mc_logprob_fwd_shard")
+    return partial
+
+
+def logprob_merge_shards(partials, targets, V_total, *, with_entropy=True, stream=None):
+    """Fold partials [S, 4, T] (shard order) into (logp, lse, entropy)."""
+    torch = _torch()
+    lib = load_library()
+    S, four, T = partials.shape
+    _need(four == 4 and partials.dtype == torch.float32 and partials.is_contiguous(),
+          "partials [S, 4, T] fp32")
+    dev = partials.device
+    logp = torch.empty(T, dtype=torch.float32, device=dev)
+    lse = torch.empty(T, dtype=torch.float32, device=dev)
+    ent = torch.empty(T, dtype=torch.float32, device=dev) if with_entropy else None
+    _check(lib.mc_logprob_merge_shards(_ptr(partials), S, _ptr(targets), T, int(V_total),
+                                       _ptr(logp), _ptr(lse), _ptr(ent), _stream(stream)),
+           "mc_logprob_merge_shards")
+    return logp, lse, ent
+
+
+def logprob_bwd_shard(hidden, weight_shard, targets, lse, dlogp, v_offset, V_total, *,
+                      dhidden=None, dweight=None, need_dhidden=True, need_dweight=True,
+                      workspace=None, stream=None):
+    """Backward on a vocabulary shard (see mc_logprob_bwd_shard).  Returns
+    (this shard's part of dhidden, the shard's rows of dW)."""
+    torch = _torch()
+    lib = load_library()
+    T, d = hidden.shape
+    Vs = weight_shard.shape[0]
+    dt = _dtype_code(hidden)
+    dev = hidden.device
+    if need_dhidden and dhidden is None:
+        dhidden = torch.empty(T, d, dtype=torch.float32, device=dev)
+    if need_dweight and dweight is None:
+        dweight = torch.empty(Vs, d, dtype=torch.float32, device=dev)
+    need = lib.mc_logprob_bwd_workspace_size(T, d, Vs, dt)
+    ws, nbytes = _workspace(need, dev, workspace)
+    _check(lib.mc_logprob_bwd_shard(_ptr(hidden), _ptr(weight_shard), _ptr(targets), _ptr(lse),
+                                    _ptr(dlogp), T, d, Vs, int(v_offset), int(V_total), dt,
+                                    _ptr(dhidden if need_dhidden else None),
+                                    _ptr(dweight if need_dweight else None), 0, _ptr(ws),
+                                    nbytes, _stream(stream)), "mc_logprob_bwd_shard")
+    return (dhidden if need_dhidden else None), (dweight if need_dweight else None)
+
+
+def primeecho_rewards(scores, success=None, n_turns=None, *, alpha=0.75, beta1=0.0, beta2=0.0,
+                      stream=None):
+    """PrimeEcho trajectory rewards (see mc_primeecho_rewards): scores [B, Kmax]
+    fp32, success [B, Kmax] uint8, n_turns [B] int32.  Returns rewards [B]."""
+    torch = _torch()
+    lib = load_library()
+    B, K = scores.shape
+    _need(scores.dtype == torch.float32 and scores.is_cuda and scores.is_contiguous(),
+          "scores fp32 [B, Kmax] on the GPU")
+    _need(success is None or (success.dtype == torch.uint8 and success.shape == (B, K)),
+          "success uint8 [B, Kmax]")
+    _need(n_turns is None or (n_turns.dtype == torch.int32 and n_turns.shape == (B,)),
+          "n_turns int32 [B]")
+    out = torch.empty(B, dtype=torch.float32, device=scores.device)
+    _check(lib.mc_primeecho_rewards(_ptr(scores), _ptr(success), _ptr(n_turns), B, K,
+                                    float(alpha), float(beta1), float(beta2), _ptr(out),
+                                    _stream(stream)), "mc_primeecho_rewards")
+    return out
 
 
 def logprob_bwd(hidden, weight, targets, lse, dlogp, *, dhidden=None, dweight=None,
@@ -223,10 +328,10 @@ def logprob_bwd(hidden, weight, targets, lse, dlogp, *, dhidden=None, dweight=No
 
 
 def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
-            params: RLParams | None = None, *, workspace=None, stream=None):
+            params: RLParams | None = None, *, logp_ref=None, workspace=None, stream=None):
     """RL objective over a packed batch (see mc_rl_loss).  Returns a dict of
     device tensors: loss, dlogp, seq_mask, seq_len, n_valid, adv, stat_abs,
-    stat_signed, clip_frac, error_flag."""
+    stat_signed, clip_frac, error_flag, kl."""
     torch = _torch()
     lib = load_library()
     p = params or RLParams()
@@ -238,7 +343,9 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
     _need(rewards.dtype == torch.float32 and rewards.shape == (B,), "rewards fp32 [B]")
     _need(loss_mask is None or (loss_mask.dtype == torch.uint8 and loss_mask.shape == (T,)),
           "loss_mask uint8 [T]")
-    for t in (logp, logp_rollout, cu_seqlens, cu_groups, rewards, loss_mask):
+    _need(logp_ref is None or (logp_ref.dtype == torch.float32 and logp_ref.shape == (T,)),
+          "logp_ref fp32 [T]")
+    for t in (logp, logp_rollout, logp_ref, cu_seqlens, cu_groups, rewards, loss_mask):
         _need(t is None or (t.is_cuda and t.is_contiguous()), "contiguous GPU tensors")
     dev = logp.device
     out = dict(
@@ -252,14 +359,14 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
         stat_signed=torch.empty(B, dtype=torch.float32, device=dev),
         clip_frac=torch.empty(1, dtype=torch.float32, device=dev),
         error_flag=torch.empty(1, dtype=torch.int32, device=dev),
+        kl=torch.empty(1, dtype=torch.float32, device=dev),
     )
-    oc = RLOutputsC(*[out[k].data_ptr() if out[k].numel() else None
-                      for k in ("loss", "dlogp", "seq_mask", "seq_len", "n_valid", "adv",
-                                "stat_abs", "stat_signed", "clip_frac", "error_flag")])
+    oc = RLOutputsC(*[out[k].data_ptr() if out[k].numel() else None for k in _OUT_FIELDS])
     pc = p.to_c()
     need = lib.mc_rl_loss_workspace_size(T, B, NG)
     ws, nbytes = _workspace(need, dev, workspace)
-    _check(lib.mc_rl_loss(_ptr(logp), _ptr(logp_rollout), _ptr(loss_mask), _ptr(cu_seqlens),
+    _check(lib.mc_rl_loss(_ptr(logp), _ptr(logp_rollout), _ptr(logp_ref), _ptr(loss_mask),
+                          _ptr(cu_seqlens),
                           _ptr(cu_groups), _ptr(rewards), T, B, NG, ctypes.byref(pc),
                           ctypes.byref(oc), _ptr(ws), nbytes, _stream(stream)), "mc_rl_loss")
     return out

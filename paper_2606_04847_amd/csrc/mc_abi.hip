@@ -57,18 +57,50 @@ size_t mc_logprob_fwd_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t
 
 mc_status_t mc_logprob_fwd(const void* hidden, const void* weight, const int64_t* targets,
                            int64_t T, int64_t d, int64_t V, mc_dtype_t dt, float* logp,
-                           float* lse, void* ws, size_t ws_bytes, void* stream) {
+                           float* lse, float* entropy, void* ws, size_t ws_bytes, void* stream) {
   mc_status_t st = check_dims(T, d, V, dt);
   if (st != MC_OK) return st;
   if (T == 0) return MC_OK;
   if (!hidden || !weight || !targets || !logp || !lse) return MC_ERR_INVALID_ARG;
   if (!aligned(hidden, 16) || !aligned(weight, 16) || !aligned(targets, 8) ||
-      !aligned(logp, 4) || !aligned(lse, 4))
+      !aligned(logp, 4) || !aligned(lse, 4) || (entropy && !aligned(entropy, 4)))
     return MC_ERR_INVALID_ARG;
   st = check_ws(ws, ws_bytes, mc::fwd_workspace(T, d, V, dt));
   if (st != MC_OK) return st;
-  return from_hip(mc::launch_fwd(hidden, weight, targets, T, d, V, dt, logp, lse, ws,
+  return from_hip(mc::launch_fwd(hidden, weight, targets, T, d, V, 0, V, dt, logp, lse, entropy,
+                                 nullptr, entropy != nullptr, ws,
                                  static_cast<hipStream_t>(stream)));
+}
+
+mc_status_t mc_logprob_fwd_shard(const void* hidden, const void* weight_shard,
+                                 const int64_t* targets, int64_t T, int64_t d, int64_t V_shard,
+                                 int64_t v_offset, int64_t V_total, mc_dtype_t dt,
+                                 float* partial, void* ws, size_t ws_bytes, void* stream) {
+  mc_status_t st = check_dims(T, d, V_shard, dt);
+  if (st != MC_OK) return st;
+  if (v_offset < 0 || V_total < V_shard || v_offset > V_total - V_shard || V_total > kMaxDim)
+    return MC_ERR_INVALID_ARG;
+  if (T == 0) return MC_OK;
+  if (!hidden || !weight_shard || !targets || !partial) return MC_ERR_INVALID_ARG;
+  if (!aligned(hidden, 16) || !aligned(weight_shard, 16) || !aligned(targets, 8) ||
+      !aligned(partial, 4))
+    return MC_ERR_INVALID_ARG;
+  st = check_ws(ws, ws_bytes, mc::fwd_workspace(T, d, V_shard, dt));
+  if (st != MC_OK) return st;
+  return from_hip(mc::launch_fwd(hidden, weight_shard, targets, T, d, V_shard, v_offset, V_total,
+                                 dt, nullptr, nullptr, nullptr, partial, true, ws,
+                                 static_cast<hipStream_t>(stream)));
+}
+
+mc_status_t mc_logprob_merge_shards(const float* partials, int32_t S, const int64_t* targets,
+                                    int64_t T, int64_t V_total, float* logp, float* lse,
+                                    float* entropy, void* stream) {
+  if (S < 1 || T < 0 || T > kMaxDim || V_total < 1) return MC_ERR_INVALID_ARG;
+  if (T == 0) return MC_OK;
+  if (!partials || !targets || !logp || !lse) return MC_ERR_INVALID_ARG;
+  if (!aligned(partials, 4) || !aligned(targets, 8)) return MC_ERR_INVALID_ARG;
+  return from_hip(mc::launch_merge(partials, S, targets, T, V_total, logp, lse, entropy,
+                                   static_cast<hipStream_t>(stream)));
 }
 
 size_t mc_logprob_bwd_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
@@ -76,10 +108,37 @@ size_t mc_logprob_bwd_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t
   return mc::bwd_workspace(T, d, V, dt);
 }
 
+static mc_status_t bwd_common(const void* hidden, const void* weight, const int64_t* targets,
+                              const float* lse, const float* dlogp, int64_t T, int64_t d,
+                              int64_t V, int64_t v_offset, int64_t V_total, mc_dtype_t dt,
+                              float* dhidden, float* dweight, int32_t flags, void* ws,
+                              size_t ws_bytes, void* stream);
+
 mc_status_t mc_logprob_bwd(const void* hidden, const void* weight, const int64_t* targets,
                            const float* lse, const float* dlogp, int64_t T, int64_t d, int64_t V,
                            mc_dtype_t dt, float* dhidden, float* dweight, int32_t flags,
                            void* ws, size_t ws_bytes, void* stream) {
+  return bwd_common(hidden, weight, targets, lse, dlogp, T, d, V, 0, V, dt, dhidden, dweight,
+                    flags, ws, ws_bytes, stream);
+}
+
+mc_status_t mc_logprob_bwd_shard(const void* hidden, const void* weight_shard,
+                                 const int64_t* targets, const float* lse, const float* dlogp,
+                                 int64_t T, int64_t d, int64_t V_shard, int64_t v_offset,
+                                 int64_t V_total, mc_dtype_t dt, float* dhidden,
+                                 float* dweight_shard, int32_t flags, void* ws, size_t ws_bytes,
+                                 void* stream) {
+  if (v_offset < 0 || V_total < V_shard || v_offset > V_total - V_shard || V_total > kMaxDim)
+    return MC_ERR_INVALID_ARG;
+  return bwd_common(hidden, weight_shard, targets, lse, dlogp, T, d, V_shard, v_offset, V_total,
+                    dt, dhidden, dweight_shard, flags, ws, ws_bytes, stream);
+}
+
+static mc_status_t bwd_common(const void* hidden, const void* weight, const int64_t* targets,
+                              const float* lse, const float* dlogp, int64_t T, int64_t d,
+                              int64_t V, int64_t v_offset, int64_t V_total, mc_dtype_t dt,
+                              float* dhidden, float* dweight, int32_t flags, void* ws,
+                              size_t ws_bytes, void* stream) {
   mc_status_t st = check_dims(T, d, V, dt);
   if (st != MC_OK) return st;
   if (flags & ~(MC_BWD_ACCUMULATE_DHIDDEN | MC_BWD_ACCUMULATE_DWEIGHT)) return MC_ERR_INVALID_ARG;
@@ -99,8 +158,9 @@ mc_status_t mc_logprob_bwd(const void* hidden, const void* weight, const int64_t
   if (!aligned(targets, 8) || !aligned(lse, 4) || !aligned(dlogp, 4)) return MC_ERR_INVALID_ARG;
   st = check_ws(ws, ws_bytes, mc::bwd_workspace(T, d, V, dt));
   if (st != MC_OK) return st;
-  return from_hip(mc::launch_bwd(hidden, weight, targets, lse, dlogp, T, d, V, dt, dhidden,
-                                 dweight, flags, ws, static_cast<hipStream_t>(stream)));
+  return from_hip(mc::launch_bwd(hidden, weight, targets, lse, dlogp, T, d, V, v_offset, V_total,
+                                 dt, dhidden, dweight, flags, ws,
+                                 static_cast<hipStream_t>(stream)));
 }
 
 size_t mc_rl_loss_workspace_size(int64_t T, int32_t B, int32_t NG) {
@@ -108,16 +168,18 @@ size_t mc_rl_loss_workspace_size(int64_t T, int32_t B, int32_t NG) {
   return mc::loss_workspace(T, B, NG);
 }
 
-mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const uint8_t* loss_mask,
-                       const int32_t* cu_seqlens, const int32_t* cu_groups, const float* rewards,
-                       int64_t T, int32_t B, int32_t NG, const mc_rl_params_t* params,
-                       const mc_rl_outputs_t* out, void* ws, size_t ws_bytes, void* stream) {
+mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const float* logp_ref,
+                       const uint8_t* loss_mask, const int32_t* cu_seqlens,
+                       const int32_t* cu_groups, const float* rewards, int64_t T, int32_t B,
+                       int32_t NG, const mc_rl_params_t* params, const mc_rl_outputs_t* out,
+                       void* ws, size_t ws_bytes, void* stream) {
   if (T < 0 || B < 0 || NG < 0 || T > kMaxDim) return MC_ERR_INVALID_ARG;
   if (!params || !out || !out->loss) return MC_ERR_INVALID_ARG;
   if (B == 0 && T > 0) return MC_ERR_INVALID_ARG;   // tokens outside every sequence
   if (NG == 0 && B > 0) return MC_ERR_INVALID_ARG;  // sequences outside every group
   const mc_rl_params_t& p = *params;
-  if (!finite(p.eps_low) || !finite(p.eps_high) || !finite(p.delta) || !finite(p.adv_eps))
+  if (!finite(p.eps_low) || !finite(p.eps_high) || !finite(p.delta) || !finite(p.adv_eps) ||
+      !finite(p.kl_beta) || p.kl_beta < 0.0f)
     return MC_ERR_INVALID_ARG;
   if (p.eps_low < 0.0f || p.eps_low >= 1.0f || p.eps_high < 0.0f || p.delta < 0.0f ||
       p.adv_eps < 0.0f)
@@ -133,8 +195,21 @@ mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const uint8
     return MC_ERR_INVALID_ARG;
   mc_status_t st = check_ws(ws, ws_bytes, mc::loss_workspace(T, B, NG));
   if (st != MC_OK) return st;
-  return from_hip(mc::launch_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
-                                  T, B, NG, p, *out, ws, static_cast<hipStream_t>(stream)));
+  return from_hip(mc::launch_loss(logp, logp_rollout, logp_ref, loss_mask, cu_seqlens, cu_groups,
+                                  rewards, T, B, NG, p, *out, ws,
+                                  static_cast<hipStream_t>(stream)));
+}
+
+mc_status_t mc_primeecho_rewards(const float* scores, const uint8_t* success,
+                                 const int32_t* n_turns, int32_t B, int32_t Kmax, float alpha,
+                                 float beta1, float beta2, float* rewards, void* stream) {
+  if (B < 0 || Kmax < 1) return MC_ERR_INVALID_ARG;
+  if (!finite(alpha) || alpha < 0.0f || alpha > 1.0f || !finite(beta1) || !finite(beta2))
+    return MC_ERR_INVALID_ARG;
+  if (B == 0) return MC_OK;
+  if (!scores || !rewards) return MC_ERR_INVALID_ARG;
+  return from_hip(mc::launch_primeecho(scores, success, n_turns, B, Kmax, alpha, beta1, beta2,
+                                       rewards, static_cast<hipStream_t>(stream)));
 }
 
 mc_status_t mc_check_packing(const int32_t* cu, int32_t B, const int32_t* cg, int32_t NG,

@@ -53,13 +53,24 @@ size_t fwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt);
 size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt);
 size_t loss_workspace(int64_t T, int32_t B, int32_t NG);
 
+// Forward over the vocabulary shard [v_off, v_off + Vs) of V entries.  With
+// part == null: final logp, lse (and entropy if non-null); otherwise the
+// shard's partial [4][T] = (max, sum exp, sum exp * z, target logit or -inf).
 hipError_t launch_fwd(const void* H, const void* W, const int64_t* y, int64_t T, int64_t d,
-                      int64_t V, mc_dtype_t dt, float* logp, float* lse, void* ws,
+                      int64_t Vs, int64_t v_off, int64_t V, mc_dtype_t dt, float* logp,
+                      float* lse, float* entropy, float* part, bool with_u, void* ws,
                       hipStream_t s);
+hipError_t launch_merge(const float* parts, int S, const int64_t* y, int64_t T, int64_t V,
+                        float* logp, float* lse, float* entropy, hipStream_t s);
 hipError_t launch_bwd(const void* H, const void* W, const int64_t* y, const float* lse,
-                      const float* dlogp, int64_t T, int64_t d, int64_t V, mc_dtype_t dt,
-                      float* dH, float* dW, int flags, void* ws, hipStream_t s);
-hipError_t launch_loss(const float* logp, const float* logp_rollout, const uint8_t* mask,
+                      const float* dlogp, int64_t T, int64_t d, int64_t Vs, int64_t v_off,
+                      int64_t V, mc_dtype_t dt, float* dH, float* dW, int flags, void* ws,
+                      hipStream_t s);
+hipError_t launch_primeecho(const float* scores, const uint8_t* success, const int32_t* n_turns,
+                            int32_t B, int32_t Kmax, float alpha, float beta1, float beta2,
+                            float* rewards, hipStream_t s);
+hipError_t launch_loss(const float* logp, const float* logp_rollout, const float* logp_ref,
+                       const uint8_t* mask,
                        const int32_t* cu_seqlens, const int32_t* cu_groups,
                        const float* rewards, int64_t T, int32_t B, int32_t NG,
                        const mc_rl_params_t& p, const mc_rl_outputs_t& out, void* ws,

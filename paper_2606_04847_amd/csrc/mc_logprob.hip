@@ -26,17 +26,20 @@ __device__ __forceinline__ float half_sum(float x) {
 }
 
 // ---------------------------------------------------------------------------
-// Forward epilogue.  For each of the tile's 256 rows: max and sum of exp over
-// the tile's valid columns -> one (m, s) partial per (vocab tile, row); the
-// target logit z[t, y_t] is written by the one lane that holds it.
+// Forward epilogue.  For each of the tile's 256 rows: max, sum of exp and
+// (optionally) sum of exp * z over the tile's valid columns -> one (m, s, u)
+// partial per (vocab tile, row); the target logit z[t, y_t] is written by the
+// one lane that holds it.  The weight may be a vocabulary shard: column c of
+// this launch is vocabulary entry v_off + c.
 // ---------------------------------------------------------------------------
 struct EpiFwd {
   const int64_t* y;
-  int64_t T, V;
-  float* part_m;   // [nTn][T]
-  float* part_s;   // [nTn][T]
-  float* zy;       // [T]: receives z[t, y_t]
-  static constexpr int kLdsExtra = 256 * 4 + 2 * kWavesN * 256 * 4;
+  int64_t T, Vs, v_off;   // rows, shard width, shard offset
+  float* part_m;          // [nTn][T]
+  float* part_s;          // [nTn][T]
+  float* part_u;          // [nTn][T] or null (no entropy)
+  float* zy;              // [T]: receives z[t, y_t] for targets inside the shard
+  static constexpr int kLdsExtra = 256 * 4 + 3 * kWavesN * 256 * 4;
 
   __device__ void prologue(int64_t m0, int64_t, char* extra) const {
     int* ys = reinterpret_cast<int*>(extra);
@@ -44,8 +47,8 @@ struct EpiFwd {
       const int64_t t = m0 + i;
       int v = -1;
       if (t < T) {
-        const int64_t yy = y[t];
-        if (yy >= 0 && yy < V) v = int(yy);
+        const int64_t yl = y[t] - v_off;
+        if (yl >= 0 && yl < Vs) v = int(yl);
       }
       ys[i] = v;
     }
@@ -56,10 +59,11 @@ struct EpiFwd {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wm = wave_m(), wn = wave_n();
     const int* ys = reinterpret_cast<const int*>(extra);
-    float* red = reinterpret_cast<float*>(extra + 1024);   // [m|s][wn][row]
+    float* red = reinterpret_cast<float*>(extra + 1024);   // [m|s|u][wn][row]
     const int cbase = int(n0) + wn * kWaveCols;
-    const int vlim = int(min<int64_t>(V - cbase, kWaveCols));   // valid columns of this wave
+    const int vlim = int(min<int64_t>(Vs - cbase, kWaveCols));   // valid columns of this wave
     const int cl = lane & 31;
+    const bool with_u = part_u != nullptr;
 #pragma unroll
     for (int i = 0; i < kTM; ++i) {
 #pragma unroll
@@ -70,12 +74,18 @@ struct EpiFwd {
         for (int j = 0; j < kTN; ++j)
           if (j * 32 + cl < vlim) mx = fmaxf(mx, acc[i][j][e]);
         mx = half_max(mx);
-        float s = 0.0f;
+        float s = 0.0f, u = 0.0f;
         const float mb = mx * kLog2e;
 #pragma unroll
-        for (int j = 0; j < kTN; ++j)
-          if (j * 32 + cl < vlim) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
+        for (int j = 0; j < kTN; ++j) {
+          if (j * 32 + cl < vlim) {
+            const float x = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
+            s += x;
+            u = fmaf(x, acc[i][j][e], u);
+          }
+        }
         s = half_sum(s);
+        if (with_u) u = half_sum(u);
         const int yl = ys[r] - cbase;
         if (yl >= 0 && yl < kWaveCols && (yl & 31) == cl) {
           const int jj = yl >> 5;
@@ -87,6 +97,7 @@ struct EpiFwd {
         if (cl == 0) {
           red[(0 * kWavesN + wn) * 256 + r] = mx;
           red[(1 * kWavesN + wn) * 256 + r] = s;
+          red[(2 * kWavesN + wn) * 256 + r] = u;
         }
       }
     }
@@ -97,63 +108,125 @@ struct EpiFwd {
       float M = red[r];
 #pragma unroll
       for (int w = 1; w < kWavesN; ++w) M = fmaxf(M, red[w * 256 + r]);
-      float S = 0.0f;
+      float S = 0.0f, U = 0.0f;
 #pragma unroll
       for (int w = 0; w < kWavesN; ++w) {
         const float mw = red[w * 256 + r];
-        if (mw != kNegInf)
-          S += red[(kWavesN + w) * 256 + r] * __builtin_amdgcn_exp2f((mw - M) * kLog2e);
+        if (mw != kNegInf) {
+          const float f = __builtin_amdgcn_exp2f((mw - M) * kLog2e);
+          S += red[(kWavesN + w) * 256 + r] * f;
+          U += red[(2 * kWavesN + w) * 256 + r] * f;
+        }
       }
       part_m[int64_t(tn) * T + t] = M;
       part_s[int64_t(tn) * T + t] = S;
+      if (with_u) part_u[int64_t(tn) * T + t] = U;
     }
   }
 };
 
-// Merge of the per-vocab-tile partials, in tile order: lse = m + log s and
-// logp = z_y - lse (0 for ignored targets).  64 rows per block, 8 waves
-// stride over the tiles, then wave 0 folds the 8 running pairs in order.
-__global__ __launch_bounds__(512) void k_lse_merge(const float* __restrict__ pm,
-                                                   const float* __restrict__ ps, int nT,
-                                                   int64_t T, const int64_t* __restrict__ y,
-                                                   int64_t V, float* __restrict__ logp,
-                                                   float* __restrict__ lse) {
-  __shared__ float sm[8][64], ss[8][64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int64_t t = int64_t(blockIdx.x) * 64 + lane;
-  float M = kNegInf, S = 0.0f;
-  if (t < T) {
-    for (int j = w; j < nT; j += 8) {
-      const float m = pm[int64_t(j) * T + t], s = ps[int64_t(j) * T + t];
-      if (m > M) {
-        S = S * expf(M - m) + s;
-        M = m;
-      } else {
-        S += s * expf(m - M);
-      }
+// Running (max, sum exp, sum exp * z) triple, folded in a fixed order.
+struct Lse3 {
+  float m = kNegInf, s = 0.0f, u = 0.0f;
+  __device__ void add(float m2, float s2, float u2) {
+    if (m2 == kNegInf) return;
+    if (m2 > m) {
+      const float f = expf(m - m2);
+      s = s * f + s2;
+      u = u * f + u2;
+      m = m2;
+    } else {
+      const float f = expf(m2 - m);
+      s += s2 * f;
+      u += u2 * f;
     }
   }
-  sm[w][lane] = M;
-  ss[w][lane] = S;
-  __syncthreads();
-  if (w == 0 && t < T) {
-    M = sm[0][lane];
-    S = ss[0][lane];
-    for (int k = 1; k < 8; ++k) {
-      const float m = sm[k][lane], s = ss[k][lane];
-      if (m == kNegInf) continue;
-      if (m > M) {
-        S = S * expf(M - m) + s;
-        M = m;
-      } else {
-        S += s * expf(m - M);
-      }
+};
+
+// Fold the per-vocab-tile partials of 64 rows in tile order: 8 waves stride
+// over the tiles, then wave 0 folds the 8 running triples in order.
+__device__ __forceinline__ Lse3 fold_tiles(const float* __restrict__ pm,
+                                           const float* __restrict__ ps,
+                                           const float* __restrict__ pu, int nT, int64_t T,
+                                           int64_t t, float (*sh)[8][64]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  Lse3 acc;
+  if (t < T)
+    for (int j = w; j < nT; j += 8) {
+      const int64_t o = int64_t(j) * T + t;
+      acc.add(pm[o], ps[o], pu ? pu[o] : 0.0f);
     }
-    const float l = M + logf(S);
+  sh[0][w][lane] = acc.m;
+  sh[1][w][lane] = acc.s;
+  sh[2][w][lane] = acc.u;
+  __syncthreads();
+  Lse3 out;
+  if (w == 0)
+    for (int k = 0; k < 8; ++k) out.add(sh[0][k][lane], sh[1][k][lane], sh[2][k][lane]);
+  return out;
+}
+
+// Final merge: lse = m + log s, logp = z_y - lse (0 for an ignored target),
+// entropy = lse - u / s (the expectation of z under the softmax).
+__global__ __launch_bounds__(512) void k_lse_merge(const float* __restrict__ pm,
+                                                   const float* __restrict__ ps,
+                                                   const float* __restrict__ pu, int nT,
+                                                   int64_t T, const int64_t* __restrict__ y,
+                                                   int64_t V, float* __restrict__ logp,
+                                                   float* __restrict__ lse,
+                                                   float* __restrict__ entropy) {
+  __shared__ float sh[3][8][64];
+  const int64_t t = int64_t(blockIdx.x) * 64 + (threadIdx.x & 63);
+  const Lse3 r = fold_tiles(pm, ps, pu, nT, T, t, sh);
+  if ((threadIdx.x >> 6) == 0 && t < T) {
+    const float l = r.m + logf(r.s);
     lse[t] = l;
     const int64_t yy = y[t];
     logp[t] = (yy >= 0 && yy < V) ? logp[t] - l : 0.0f;
+    if (entropy) entropy[t] = l - r.u / r.s;
   }
+}
+
+// Shard partial: (m, s, u, z_y or -inf) of this vocabulary shard per row,
+// part = [4][T]; z_y was written into part[3] by the GEMM epilogue.
+__global__ __launch_bounds__(512) void k_shard_partial(const float* __restrict__ pm,
+                                                       const float* __restrict__ ps,
+                                                       const float* __restrict__ pu, int nT,
+                                                       int64_t T, const int64_t* __restrict__ y,
+                                                       int64_t v_off, int64_t Vs,
+                                                       float* __restrict__ part) {
+  __shared__ float sh[3][8][64];
+  const int64_t t = int64_t(blockIdx.x) * 64 + (threadIdx.x & 63);
+  const Lse3 r = fold_tiles(pm, ps, pu, nT, T, t, sh);
+  if ((threadIdx.x >> 6) == 0 && t < T) {
+    part[t] = r.m;
+    part[T + t] = r.s;
+    part[2 * T + t] = r.u;
+    const int64_t yl = y[t] - v_off;
+    if (!(yl >= 0 && yl < Vs)) part[3 * T + t] = kNegInf;
+  }
+}
+
+// Merge of S shard partials (shard order) into lse, logp and entropy.
+__global__ __launch_bounds__(256) void k_shard_merge(const float* __restrict__ parts, int S,
+                                                     int64_t T, const int64_t* __restrict__ y,
+                                                     int64_t V, float* __restrict__ logp,
+                                                     float* __restrict__ lse,
+                                                     float* __restrict__ entropy) {
+  const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  Lse3 r;
+  float zy = kNegInf;
+  for (int k = 0; k < S; ++k) {
+    const float* p = parts + int64_t(k) * 4 * T;
+    r.add(p[t], p[T + t], p[2 * T + t]);
+    zy = fmaxf(zy, p[3 * T + t]);
+  }
+  const float l = r.m + logf(r.s);
+  lse[t] = l;
+  const int64_t yy = y[t];
+  logp[t] = (yy >= 0 && yy < V) ? zy - l : 0.0f;
+  if (entropy) entropy[t] = l - r.u / r.s;
 }
 
 // ---------------------------------------------------------------------------
@@ -166,7 +239,8 @@ struct EpiProbs {
   const int64_t* y;
   const float* lse;
   const float* dlogp;
-  int64_t Tn, V, width, ld, pld;   // ld: padded chunk width; pld: padded token count
+  int64_t Tn, V, width, ld, pld;   // V: full vocabulary (target validity); ld: padded chunk
+                                   // width; pld: padded token count
   T* P;                            // panel layout (see Lay::TileTK)
   static constexpr int64_t kPanel = 128 / sizeof(T);
   static constexpr int kLdsExtra = 2 * 256 * 4;
@@ -252,10 +326,10 @@ template <typename T>
 __global__ __launch_bounds__(256) void k_onehot_dh(const T* __restrict__ W,
                                                    const int64_t* __restrict__ y,
                                                    const float* __restrict__ dlogp,
-                                                   int64_t d, int64_t V,
+                                                   int64_t d, int64_t v_off, int64_t V,
                                                    float* __restrict__ dH) {
   const int64_t t = blockIdx.x;
-  const int64_t yy = y[t];
+  const int64_t yy = y[t] - v_off;
   if (yy < 0 || yy >= V) return;
   const float g = dlogp[t];
   const T* w = W + yy * d;
@@ -269,11 +343,11 @@ __global__ void k_fill_i32(int* __restrict__ p, int64_t n, int v) {
   if (i < n) p[i] = v;
 }
 
-__global__ void k_hist(const int64_t* __restrict__ y, int64_t T, int64_t V,
+__global__ void k_hist(const int64_t* __restrict__ y, int64_t T, int64_t v_off, int64_t V,
                        int* __restrict__ counts) {
   const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (t >= T) return;
-  const int64_t yy = y[t];
+  const int64_t yy = y[t] - v_off;
   if (yy >= 0 && yy < V) atomicAdd(counts + yy, 1);
 }
 
@@ -303,23 +377,23 @@ __global__ __launch_bounds__(1024) void k_scan(const int* __restrict__ counts, i
   if (tid == 1023) offsets[V] = part[1023];
 }
 
-__global__ void k_bucket_fill(const int64_t* __restrict__ y, int64_t T, int64_t V,
-                              const int* __restrict__ offsets, int* __restrict__ cursor,
-                              int* __restrict__ unsorted) {
+__global__ void k_bucket_fill(const int64_t* __restrict__ y, int64_t T, int64_t v_off,
+                              int64_t V, const int* __restrict__ offsets,
+                              int* __restrict__ cursor, int* __restrict__ unsorted) {
   const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (t >= T) return;
-  const int64_t yy = y[t];
+  const int64_t yy = y[t] - v_off;
   if (yy < 0 || yy >= V) return;
   unsorted[offsets[yy] + atomicAdd(cursor + yy, 1)] = int(t);
 }
 
 // Place each token at its rank among the tokens of its bucket (ascending t).
-__global__ void k_bucket_rank(const int64_t* __restrict__ y, int64_t T, int64_t V,
-                              const int* __restrict__ offsets,
+__global__ void k_bucket_rank(const int64_t* __restrict__ y, int64_t T, int64_t v_off,
+                              int64_t V, const int* __restrict__ offsets,
                               const int* __restrict__ unsorted, int* __restrict__ sorted) {
   const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (t >= T) return;
-  const int64_t yy = y[t];
+  const int64_t yy = y[t] - v_off;
   if (yy < 0 || yy >= V) return;
   const int b = offsets[yy], e = offsets[yy + 1];
   int rank = 0;
@@ -335,11 +409,12 @@ __global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
                                                    const float* __restrict__ dlogp,
                                                    const int* __restrict__ offsets,
                                                    const int* __restrict__ sorted, int64_t d,
-                                                   int64_t V, float* __restrict__ dW) {
+                                                   int64_t v_off, int64_t V,
+                                                   float* __restrict__ dW) {
   const int p = blockIdx.x;
   if (p >= offsets[V]) return;
   const int t0 = sorted[p];
-  const int64_t v = y[t0];
+  const int64_t v = y[t0] - v_off;
   const int b = offsets[v], e = offsets[v + 1];
   if (p != b) return;
   float* o = dW + v * d;
@@ -379,45 +454,59 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand 
   gemm_body<T, Lay::TileVT, Lay::MNMajor>(A, B, K, nTm, nTn, epi, lds);
 }
 
+// Forward over a vocabulary shard [v_off, v_off + Vs) of a V-entry vocabulary
+// (the whole vocabulary when v_off = 0, Vs = V).  part == null: final lse,
+// logp (and entropy when given); otherwise the shard's partial [4][T].
 template <typename T>
-hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_t d,
-                    int64_t V, float* logp, float* lse, void* ws, hipStream_t s) {
-  const int nTm = int(cdiv(Tn, kBM)), nTn = int(cdiv(V, kBN));
+hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_t d, int64_t Vs,
+                    int64_t v_off, int64_t V, float* logp, float* lse, float* entropy,
+                    float* part, bool with_u, void* ws, hipStream_t s) {
+  const int nTm = int(cdiv(Tn, kBM)), nTn = int(cdiv(Vs, kBN));
   Carve cv(ws);
   float* pm = cv.take<float>(size_t(nTn) * Tn);
   float* ps = cv.take<float>(size_t(nTn) * Tn);
+  float* pu = cv.take<float>(size_t(nTn) * Tn);
+  if (!with_u) pu = nullptr;
   const double es = sizeof(T);
-  Operand A{H, d, Tn, d}, B{W, d, V, d};
+  Operand A{H, d, Tn, d}, B{W, d, Vs, d};
   if (!operand_in_bounds<T, Lay::KMajor>(A, size_t(Tn) * d * sizeof(T)) ||
-      !operand_in_bounds<T, Lay::KMajor>(B, size_t(V) * d * sizeof(T)))
+      !operand_in_bounds<T, Lay::KMajor>(B, size_t(Vs) * d * sizeof(T)))
     return hipErrorInvalidValue;
-  EpiFwd epi{y, Tn, V, pm, ps, logp};
+  EpiFwd epi{y, Tn, Vs, v_off, pm, ps, pu, part ? part + 3 * Tn : logp};
   {
-    ProfScope ps_(s, "logprob_fwd_gemm", 2.0 * Tn * d * V,
-                  es * (double(Tn) * d + double(V) * d) + 12.0 * Tn);
+    ProfScope ps_(s, "logprob_fwd_gemm", 2.0 * Tn * d * Vs,
+                  es * (double(Tn) * d + double(Vs) * d) + 12.0 * Tn);
     hipLaunchKernelGGL(k_fwd_logits_lse<T>, dim3(nTm * nTn), dim3(kThreads), 0,
                        s, A, B, d, nTm, nTn, epi);
   }
   {
-    ProfScope ps_(s, "logprob_fwd_merge", 0.0, 8.0 * nTn * Tn + 20.0 * Tn);
-    hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(Tn, 64)), dim3(512), 0, s, pm, ps, nTn, Tn, y, V,
-                       logp, lse);
+    ProfScope ps_(s, "logprob_fwd_merge", 0.0, (with_u ? 12.0 : 8.0) * nTn * Tn + 24.0 * Tn);
+    if (part)
+      hipLaunchKernelGGL(k_shard_partial, dim3(cdiv(Tn, 64)), dim3(512), 0, s, pm, ps, pu, nTn,
+                         Tn, y, v_off, Vs, part);
+    else
+      hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(Tn, 64)), dim3(512), 0, s, pm, ps, pu, nTn, Tn,
+                         y, V, logp, lse, entropy);
   }
   return hipGetLastError();
 }
 
+// Backward over a vocabulary shard [v_off, v_off + Vs) of a V-entry
+// vocabulary: dH receives this shard's part of G W (the shards' parts sum to
+// dH), dW the shard's rows.  A target outside [0, V) is an ignored token; a
+// target outside the shard contributes only the softmax part here.
 template <typename T>
 hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
-                    const float* dlogp, int64_t Tn, int64_t d, int64_t V, float* dH, float* dW,
-                    int flags, void* ws, hipStream_t s) {
-  const int64_t chunk = bwd_chunk_cols(Tn, V, sizeof(T));
-  const int64_t ld = int64_t(align_up(size_t(min(chunk, V)), 64));
+                    const float* dlogp, int64_t Tn, int64_t d, int64_t Vs, int64_t v_off,
+                    int64_t V, float* dH, float* dW, int flags, void* ws, hipStream_t s) {
+  const int64_t chunk = bwd_chunk_cols(Tn, Vs, sizeof(T));
+  const int64_t ld = int64_t(align_up(size_t(min(chunk, Vs)), 64));
   const int64_t pld = cdiv(Tn, 64) * 64;
   Carve cv(ws);
   T* P = cv.take<T>(size_t(pld) * ld);
-  int* counts = cv.take<int>(V);
-  int* cursor = cv.take<int>(V);
-  int* offsets = cv.take<int>(V + 1);
+  int* counts = cv.take<int>(Vs);
+  int* cursor = cv.take<int>(Vs);
+  int* offsets = cv.take<int>(Vs + 1);
   int* unsorted = cv.take<int>(Tn);
   int* sorted = cv.take<int>(Tn);
   const int nTm = int(cdiv(Tn, kBM));
@@ -425,22 +514,22 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
 
   const double es = sizeof(T);
   if (dW) {
-    ProfScope ps_(s, "logprob_bwd_bucket", 0.0, 32.0 * Tn + 16.0 * V);
-    const int nb = int(cdiv(V, 256)), tb = int(cdiv(Tn, 256));
-    hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, counts, V, 0);
-    hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, cursor, V, 0);
-    hipLaunchKernelGGL(k_hist, dim3(tb), dim3(256), 0, s, y, Tn, V, counts);
-    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, counts, V, offsets);
-    hipLaunchKernelGGL(k_bucket_fill, dim3(tb), dim3(256), 0, s, y, Tn, V, offsets, cursor,
-                       unsorted);
-    hipLaunchKernelGGL(k_bucket_rank, dim3(tb), dim3(256), 0, s, y, Tn, V, offsets, unsorted,
-                       sorted);
+    ProfScope ps_(s, "logprob_bwd_bucket", 0.0, 32.0 * Tn + 16.0 * Vs);
+    const int nb = int(cdiv(Vs, 256)), tb = int(cdiv(Tn, 256));
+    hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, counts, Vs, 0);
+    hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, cursor, Vs, 0);
+    hipLaunchKernelGGL(k_hist, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, counts);
+    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, counts, Vs, offsets);
+    hipLaunchKernelGGL(k_bucket_fill, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, offsets,
+                       cursor, unsorted);
+    hipLaunchKernelGGL(k_bucket_rank, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, offsets,
+                       unsorted, sorted);
   }
-  for (int64_t v0 = 0; v0 < V; v0 += chunk) {
-    const int64_t width = min(chunk, V - v0);
+  for (int64_t v0 = 0; v0 < Vs; v0 += chunk) {
+    const int64_t width = min(chunk, Vs - v0);
     const int64_t ldc = int64_t(align_up(size_t(width), 64));   // padded width of this chunk
     const T* Wc = W + v0 * d;
-    const size_t wc_bytes = size_t(V - v0) * d * sizeof(T);
+    const size_t wc_bytes = size_t(Vs - v0) * d * sizeof(T);
     const size_t p_bytes = size_t(pld) * ld * sizeof(T);
     {
       Operand A{H, d, Tn, d}, B{Wc, d, width, d};
@@ -484,12 +573,13 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   }
   if (dH) {
     ProfScope ps_(s, "logprob_bwd_onehot_dh", 2.0 * Tn * d, (es + 8.0) * Tn * d);
-    hipLaunchKernelGGL(k_onehot_dh<T>, dim3(Tn), dim3(256), 0, s, W, y, dlogp, d, V, dH);
+    hipLaunchKernelGGL(k_onehot_dh<T>, dim3(Tn), dim3(256), 0, s, W, y, dlogp, d, v_off, Vs,
+                       dH);
   }
   if (dW) {
     ProfScope ps_(s, "logprob_bwd_onehot_dw", 2.0 * Tn * d, (es + 8.0) * Tn * d);
     hipLaunchKernelGGL(k_onehot_dw<T>, dim3(Tn), dim3(256), 0, s, H, y, dlogp, offsets, sorted,
-                       d, V, dW);
+                       d, v_off, Vs, dW);
   }
   return hipGetLastError();
 }
@@ -507,7 +597,7 @@ int64_t bwd_chunk_cols(int64_t T, int64_t V, size_t esize) {
 
 size_t fwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t) {
   const size_t n = size_t(cdiv(V, kBN)) * size_t(T);
-  return 2 * align_up(n * sizeof(float), kWsAlign);
+  return 3 * align_up(n * sizeof(float), kWsAlign);
 }
 
 size_t bwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t dt) {
@@ -522,23 +612,33 @@ size_t bwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t dt) {
 }
 
 hipError_t launch_fwd(const void* H, const void* W, const int64_t* y, int64_t T, int64_t d,
-                      int64_t V, mc_dtype_t dt, float* logp, float* lse, void* ws,
+                      int64_t Vs, int64_t v_off, int64_t V, mc_dtype_t dt, float* logp,
+                      float* lse, float* entropy, float* part, bool with_u, void* ws,
                       hipStream_t s) {
   if (dt == MC_BF16)
-    return fwd_impl(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W), y, T, d, V,
-                    logp, lse, ws, s);
-  return fwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, T, d, V, logp,
-                  lse, ws, s);
+    return fwd_impl(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W), y, T, d, Vs,
+                    v_off, V, logp, lse, entropy, part, with_u, ws, s);
+  return fwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, T, d, Vs, v_off,
+                  V, logp, lse, entropy, part, with_u, ws, s);
+}
+
+hipError_t launch_merge(const float* parts, int S, const int64_t* y, int64_t T, int64_t V,
+                        float* logp, float* lse, float* entropy, hipStream_t s) {
+  ProfScope ps_(s, "logprob_merge_shards", 0.0, 16.0 * S * T + 20.0 * T);
+  hipLaunchKernelGGL(k_shard_merge, dim3(cdiv(T, 256)), dim3(256), 0, s, parts, S, T, y, V, logp,
+                     lse, entropy);
+  return hipGetLastError();
 }
 
 hipError_t launch_bwd(const void* H, const void* W, const int64_t* y, const float* lse,
-                      const float* dlogp, int64_t T, int64_t d, int64_t V, mc_dtype_t dt,
-                      float* dH, float* dW, int flags, void* ws, hipStream_t s) {
+                      const float* dlogp, int64_t T, int64_t d, int64_t Vs, int64_t v_off,
+                      int64_t V, mc_dtype_t dt, float* dH, float* dW, int flags, void* ws,
+                      hipStream_t s) {
   if (dt == MC_BF16)
     return bwd_impl(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W), y, lse, dlogp,
-                    T, d, V, dH, dW, flags, ws, s);
+                    T, d, Vs, v_off, V, dH, dW, flags, ws, s);
   return bwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, lse, dlogp, T,
-                  d, V, dH, dW, flags, ws, s);
+                  d, Vs, v_off, V, dH, dW, flags, ws, s);
 }
 
 }  // namespace mc

@@ -157,13 +157,15 @@ __global__ __launch_bounds__(256) void k_count(const long long* __restrict__ gro
 }
 
 // Phase 3: per-token surrogate and gradient (Eq. 17); per-sequence sums.
+// With a reference policy, the KL term beta * k3 (k3 = e^r - r - 1,
+// r = logp_ref - logp) joins the same token mean.
 __global__ __launch_bounds__(kLossThreads) void k_surrogate(
     const float* __restrict__ logp, const float* __restrict__ lr,
-    const uint8_t* __restrict__ mask, const int32_t* __restrict__ cu,
-    const int32_t* __restrict__ cg, int64_t T, int B, int NG, mc_rl_params_t p,
-    const uint8_t* __restrict__ seq_mask, const double* __restrict__ adv_d,
+    const float* __restrict__ lref, const uint8_t* __restrict__ mask,
+    const int32_t* __restrict__ cu, const int32_t* __restrict__ cg, int64_t T, int B, int NG,
+    mc_rl_params_t p, const uint8_t* __restrict__ seq_mask, const double* __restrict__ adv_d,
     const long long* __restrict__ n_valid, float* __restrict__ dlogp,
-    double* __restrict__ seq_sum, int* __restrict__ seq_clip) {
+    double* __restrict__ seq_sum, int* __restrict__ seq_clip, double* __restrict__ seq_kl) {
   const int g = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   bool bad = false;
@@ -177,59 +179,105 @@ __global__ __launch_bounds__(kLossThreads) void k_surrogate(
     seq_bounds(cu, i, B, T, s, e, bad);
     const bool keep = seq_mask[i] != 0 && N > 0;
     const double A = adv_d[i];
-    double sum = 0.0;
+    const double beta = double(p.kl_beta);
+    const bool with_kl = lref != nullptr && beta != 0.0;
+    double sum = 0.0, kl = 0.0;
     int nclip = 0;
     for (int64_t t = s + lane; t < e; t += 64) {
       float out = 0.0f;
       const bool valid = mask ? mask[t] != 0 : true;
       if (keep && valid) {
-        const double rho = exp(double(logp[t]) - double(lr[t]));
+        const double lp = double(logp[t]);
+        const double rho = exp(lp - double(lr[t]));
         const double un = rho * A;
         const double cl = fmin(fmax(rho, lo), hi) * A;
         sum += fmin(un, cl);
-        if (un <= cl) out = float(-un * invN);
+        double g = 0.0;
+        if (un <= cl) g = -un;
         else nclip += 1;
+        if (with_kl) {
+          const double r = double(lref[t]) - lp;
+          const double er = exp(r);
+          kl += er - r - 1.0;
+          g += beta * (1.0 - er);
+        }
+        out = float(g * invN);
       }
       dlogp[t] = out;
     }
     sum = wave_sum(sum);
+    kl = wave_sum(kl);
     nclip = wave_sum(nclip);
     if (lane == 0) {
       seq_sum[i] = sum;
       seq_clip[i] = nclip;
+      seq_kl[i] = kl;
     }
   }
 }
 
-// Phase 4: loss = -(1/N) sum_i seq_sum_i and the clip fraction.
+// Phase 4: loss = -(1/N) sum_i seq_sum_i (+ beta * KL), the clip fraction and
+// the mean KL estimate.
 __global__ __launch_bounds__(256) void k_finish(const double* __restrict__ seq_sum,
-                                                const int* __restrict__ seq_clip, int B,
-                                                const long long* __restrict__ n_valid,
+                                                const int* __restrict__ seq_clip,
+                                                const double* __restrict__ seq_kl, int B,
+                                                float beta, const long long* __restrict__ n_valid,
                                                 float* __restrict__ loss,
-                                                float* __restrict__ clip_frac) {
-  __shared__ double ps[256];
+                                                float* __restrict__ clip_frac,
+                                                float* __restrict__ kl_out) {
+  __shared__ double ps[256], pk[256];
   __shared__ long long pc[256];
-  double s = 0.0;
+  double s = 0.0, k = 0.0;
   long long c = 0;
   for (int i = threadIdx.x; i < B; i += 256) {
     s += seq_sum[i];
+    k += seq_kl[i];
     c += seq_clip[i];
   }
   ps[threadIdx.x] = s;
+  pk[threadIdx.x] = k;
   pc[threadIdx.x] = c;
   __syncthreads();
   for (int off = 128; off > 0; off >>= 1) {
     if (threadIdx.x < off) {
       ps[threadIdx.x] += ps[threadIdx.x + off];
+      pk[threadIdx.x] += pk[threadIdx.x + off];
       pc[threadIdx.x] += pc[threadIdx.x + off];
     }
     __syncthreads();
   }
   if (threadIdx.x == 0) {
     const long long N = *n_valid;
-    *loss = N > 0 ? float(-ps[0] / double(N)) : 0.0f;
+    const double kl = N > 0 ? pk[0] / double(N) : 0.0;
+    *loss = N > 0 ? float(-ps[0] / double(N) + double(beta) * kl) : 0.0f;
     if (clip_frac) *clip_frac = N > 0 ? float(double(pc[0]) / double(N)) : 0.0f;
+    if (kl_out) *kl_out = float(kl);
   }
+}
+
+// PrimeEcho trajectory reward (Eq. 9-10): R = alpha s_1 + (1 - alpha) max_k s_k
+// + beta1 [success_1] + beta2 [not success_1 and success_2].  One thread per
+// trajectory; K_i is clamped into [1, Kmax].
+__global__ __launch_bounds__(256) void k_primeecho(const float* __restrict__ scores,
+                                                   const uint8_t* __restrict__ success,
+                                                   const int32_t* __restrict__ n_turns, int B,
+                                                   int Kmax, float alpha, float beta1,
+                                                   float beta2, float* __restrict__ rewards) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B) return;
+  int K = n_turns ? n_turns[i] : Kmax;
+  K = K < 1 ? 1 : (K > Kmax ? Kmax : K);
+  const float* sc = scores + int64_t(i) * Kmax;
+  const double first = double(sc[0]);
+  double best = first;
+  for (int k = 1; k < K; ++k) best = fmax(best, double(sc[k]));
+  double b = 0.0;
+  if (success) {
+    const uint8_t* su = success + int64_t(i) * Kmax;
+    if (su[0]) b = double(beta1);
+    else if (K >= 2 && su[1]) b = double(beta2);
+  }
+  rewards[i] = float(double(alpha) * first + (1.0 - double(alpha)) * best + b);
 }
 
 }  // namespace
@@ -244,13 +292,24 @@ size_t loss_workspace(int64_t T, int32_t B, int32_t NG) {
   n += align_up(b * 8, kWsAlign);                 // adv_d
   n += align_up(b * 8, kWsAlign);                 // seq_sum
   n += align_up(b * 4, kWsAlign);                 // seq_clip
+  n += align_up(b * 8, kWsAlign);                 // seq_kl
   n += align_up(g * 8, kWsAlign);                 // group_n
   n += align_up(8, kWsAlign);                     // n_valid
   n += align_up(4, kWsAlign);                     // err
   return n;
 }
 
-hipError_t launch_loss(const float* logp, const float* logp_rollout, const uint8_t* mask,
+hipError_t launch_primeecho(const float* scores, const uint8_t* success, const int32_t* n_turns,
+                            int32_t B, int32_t Kmax, float alpha, float beta1, float beta2,
+                            float* rewards, hipStream_t s) {
+  if (B == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_primeecho, dim3(cdiv(B, 256)), dim3(256), 0, s, scores, success, n_turns,
+                     B, Kmax, alpha, beta1, beta2, rewards);
+  return hipGetLastError();
+}
+
+hipError_t launch_loss(const float* logp, const float* logp_rollout, const float* logp_ref,
+                       const uint8_t* mask,
                        const int32_t* cu_seqlens, const int32_t* cu_groups,
                        const float* rewards, int64_t T, int32_t B, int32_t NG,
                        const mc_rl_params_t& p, const mc_rl_outputs_t& out, void* ws,
@@ -265,6 +324,7 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const uint8
   double* adv_d = cv.take<double>(b);
   double* seq_sum = cv.take<double>(b);
   int* seq_clip = cv.take<int>(b);
+  double* seq_kl = cv.take<double>(b);
   long long* group_n = cv.take<long long>(g);
   long long* w_n = cv.take<long long>(1);
   int32_t* w_err = cv.take<int32_t>(1);
@@ -287,10 +347,10 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const uint8
   hipLaunchKernelGGL(k_count, dim3(1), dim3(256), 0, s, group_n, NG, n_valid);
   if (NG > 0)
     hipLaunchKernelGGL(k_surrogate, dim3(NG), dim3(kLossThreads), 0, s, logp, logp_rollout,
-                       mask, cu_seqlens, cu_groups, T, B, NG, p, o.seq_mask, adv_d, n_valid,
-                       out.dlogp, seq_sum, seq_clip);
-  hipLaunchKernelGGL(k_finish, dim3(1), dim3(256), 0, s, seq_sum, seq_clip, B, n_valid, out.loss,
-                     out.clip_frac);
+                       logp_ref, mask, cu_seqlens, cu_groups, T, B, NG, p, o.seq_mask, adv_d,
+                       n_valid, out.dlogp, seq_sum, seq_clip, seq_kl);
+  hipLaunchKernelGGL(k_finish, dim3(1), dim3(256), 0, s, seq_sum, seq_clip, seq_kl, B,
+                     p.kl_beta, n_valid, out.loss, out.clip_frac, out.kl);
   return hipGetLastError();
 }
 

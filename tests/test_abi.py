@@ -48,7 +48,7 @@ def test_status_strings_and_version(lib):
 def fwd(lib, T=16, d=64, V=100, dt=BF16, H=FAKE, W=FAKE, y=FAKE, lp=FAKE, ls=FAKE,
         ws=FAKE_WS, nbytes=None):
     need = lib.mc_logprob_fwd_workspace_size(max(T, 0), d, V, dt)
-    return lib.mc_logprob_fwd(H, W, y, T, d, V, dt, lp, ls, ws,
+    return lib.mc_logprob_fwd(H, W, y, T, d, V, dt, lp, ls, None, ws,
                               need if nbytes is None else nbytes, None)
 
 
@@ -104,11 +104,11 @@ def test_bwd_argument_checks(lib):
 
 def loss(lib, T=10, B=2, NG=1, params=None, out=None, ws=FAKE_WS, nbytes=None, **ptrs):
     p = params or binding.RLParams().to_c()
-    o = out or binding.RLOutputsC(FAKE, FAKE, *([None] * 8))
+    o = out or binding.RLOutputsC(FAKE, FAKE, *([None] * 9))
     need = lib.mc_rl_loss_workspace_size(T, B, NG)
     args = dict(logp=FAKE, lr=FAKE, mask=None, cu=FAKE, cg=FAKE, rw=FAKE)
     args.update(ptrs)
-    return lib.mc_rl_loss(args["logp"], args["lr"], args["mask"], args["cu"], args["cg"],
+    return lib.mc_rl_loss(args["logp"], args["lr"], None, args["mask"], args["cu"], args["cg"],
                           args["rw"], T, B, NG, ctypes.byref(p), ctypes.byref(o), ws,
                           need if nbytes is None else nbytes, None)
 
@@ -116,6 +116,7 @@ def loss(lib, T=10, B=2, NG=1, params=None, out=None, ws=FAKE_WS, nbytes=None, *
 @pytest.mark.parametrize("field,value", [
     ("eps_low", 1.0), ("eps_low", -0.1), ("eps_high", -0.5), ("delta", -1.0),
     ("delta", float("nan")), ("adv_eps", float("inf")), ("std_ddof", 2), ("filter", 3),
+    ("kl_beta", -0.1), ("kl_beta", float("nan")),
 ])
 def test_loss_parameter_checks(lib, field, value):
     p = binding.RLParams().to_c()
@@ -130,9 +131,9 @@ def test_loss_argument_checks(lib):
     assert loss(lib, logp=None) == INVALID
     assert loss(lib, cu=None) == INVALID
     assert loss(lib, rw=None) == INVALID
-    o = binding.RLOutputsC(None, FAKE, *([None] * 8))
+    o = binding.RLOutputsC(None, FAKE, *([None] * 9))
     assert loss(lib, out=o) == INVALID                # loss output is required
-    o = binding.RLOutputsC(FAKE, None, *([None] * 8))
+    o = binding.RLOutputsC(FAKE, None, *([None] * 9))
     assert loss(lib, out=o) == INVALID                # dlogp output is required
     assert loss(lib, nbytes=1) == WS
 
@@ -146,3 +147,24 @@ def test_host_packing_check(lib):
     assert not binding.check_packing(good_cu, np.array([0, 1, 2]), 7)    # groups end != B
     assert not binding.check_packing(good_cu, np.array([0, 2, 1, 3]), 7)
     assert binding.check_packing(np.array([0]), np.array([0]), 0)         # empty batch
+
+
+def test_shard_and_primeecho_argument_checks(lib):
+    need = lib.mc_logprob_fwd_workspace_size(16, 64, 100, BF16)
+    call = lambda vs, off, vt: lib.mc_logprob_fwd_shard(FAKE, FAKE, FAKE, 16, 64, vs, off, vt,
+                                                        BF16, FAKE, FAKE_WS, need, None)
+    assert call(100, -1, 300) == INVALID        # negative offset
+    assert call(100, 250, 300) == INVALID       # shard past the vocabulary
+    assert call(100, 0, 50) == INVALID          # vocabulary smaller than the shard
+    assert lib.mc_logprob_merge_shards(FAKE, 0, FAKE, 16, 100, FAKE, FAKE, None, None) == INVALID
+    assert lib.mc_logprob_merge_shards(None, 2, FAKE, 16, 100, FAKE, FAKE, None, None) == INVALID
+    bneed = lib.mc_logprob_bwd_workspace_size(16, 64, 100, BF16)
+    assert lib.mc_logprob_bwd_shard(FAKE, FAKE, FAKE, FAKE, FAKE, 16, 64, 100, 201, 300, BF16,
+                                    FAKE, FAKE, 0, FAKE_WS, bneed, None) == INVALID
+    pe = lambda B, K, a, b1: lib.mc_primeecho_rewards(FAKE, None, None, B, K, a, b1, 0.0, FAKE,
+                                                      None)
+    assert pe(4, 0, 0.75, 0.0) == INVALID       # Kmax < 1
+    assert pe(-1, 3, 0.75, 0.0) == INVALID
+    assert pe(4, 3, 1.5, 0.0) == INVALID        # alpha outside [0, 1]
+    assert pe(4, 3, 0.5, float("inf")) == INVALID
+    assert pe(0, 3, 0.5, 0.0) == OK             # no trajectories: no-op
