@@ -106,6 +106,9 @@ template <typename T, Lay L> struct LayMath {
   }
 };
 
+constexpr uint32_t kBufRange = 0x7ffffff0u;   // records of every operand resource
+constexpr uint32_t kBufOut = 0x80000000u;     // an offset past the range: reads zero
+
 // Host-side check used before every launch: the last in-range chunk of the
 // operand (offsets grow with r and k in every layout) lies inside `bytes`,
 // and the per-thread 32-bit offsets of one tile cannot overflow.
@@ -121,7 +124,7 @@ inline bool operand_in_bounds(const Operand& op, size_t bytes) {
   const int64_t span = (L == Lay::KMajor) ? 256 * op.ld * M::es
                        : (L == Lay::MNMajor) ? M::KT * op.ld * M::es
                        : (L == Lay::TileVT) ? 256 * op.ld * M::es : 256 * M::BV * M::es;
-  return last >= 0 && size_t(last) + 16 <= bytes && span < (int64_t(1) << 32);
+  return last >= 0 && size_t(last) + 16 <= bytes && span + 16 <= int64_t(kBufRange);
 }
 
 __device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
@@ -150,16 +153,21 @@ __device__ __forceinline__ void tile_of(int bid, int nTm, int nTn, int& tm, int&
 // ---------------------------------------------------------------------------
 // Global -> register -> LDS copy of one 256-row x 128-byte operand stage.
 // Every copy keeps a uniform 64-bit tile base and per-thread 32-bit offsets
-// computed once per tile.  An out-of-range chunk is read from a 16-byte
-// constant of zeros instead: the address is selected, never the loaded value,
-// so nothing waits on a load before its data is needed in LDS.
+// computed once per tile, and reads through a buffer resource rebased at
+// each K stage.  An out-of-range chunk gets an offset past the resource's
+// range, which the hardware's range check turns into zeros without touching
+// memory: only the 32-bit offset is selected, never the loaded value, so
+// nothing waits on a load before its data is needed in LDS.
 // ---------------------------------------------------------------------------
-// (global address space, like the operands, so the selected pointer stays a
-// global one and the copies use global loads; nothing ever writes it)
-static __device__ __attribute__((aligned(16))) uint32_t kZeroChunk[4] = {0u, 0u, 0u, 0u};
 
-__device__ __forceinline__ const char* zero_chunk() {
-  return reinterpret_cast<const char*>(kZeroChunk);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const char* base) {
+  // raw (stride 0) resource; 0x00020000 is the gfx9 untyped-buffer word 3
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), (short)0, int(kBufRange),
+                                           0x00020000);
+}
+
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
 template <typename T, Lay L, bool KC = KContig<L>::value> struct StageCopy;
@@ -190,12 +198,12 @@ template <typename T, Lay L> struct StageCopy<T, L, true> {
     }
   }
   __device__ __forceinline__ void load(int64_t kt) {
-    const char* sb = tb + kt * step;
+    const __amdgpu_buffer_rsrc_t rs = stage_rsrc(tb + kt * step);
     const bool kok = kt * M::KT + kc < K;
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
       const bool ok = kok && ((rowok >> i) & 1u);
-      r[i] = *reinterpret_cast<const u32x4*>(ok ? sb + off[i] : zero_chunk());
+      r[i] = buf_load16(rs, ok ? off[i] : kBufOut);
     }
   }
   __device__ __forceinline__ void store(char* lds, int tid) const {
@@ -228,12 +236,12 @@ template <Lay L> struct StageCopy<bf16_t, L, false> {
     mnok = r0 + (tid & 31) * 8 < op.rows;
   }
   __device__ __forceinline__ void load(int64_t kt) {
-    const char* sb = tb + kt * step;
+    const __amdgpu_buffer_rsrc_t rs = stage_rsrc(tb + kt * step);
     const int64_t k0 = kt * M::KT + kb;
 #pragma unroll
     for (int i = 0; i < KB; ++i) {
       const bool ok = mnok && (k0 + i < K);
-      r[i] = *reinterpret_cast<const u32x4*>(ok ? sb + off0 + i * dk_bytes : zero_chunk());
+      r[i] = buf_load16(rs, ok ? off0 + i * dk_bytes : kBufOut);
     }
   }
   __device__ __forceinline__ void store(char* lds, int tid) const {
@@ -287,15 +295,14 @@ template <Lay L> struct StageCopy<float, L, false> {
     dk_bytes = M::rel(op, (tid & 63) * 4, kb[0] + 1) - off0[0];
   }
   __device__ __forceinline__ void load(int64_t kt) {
-    const char* sb = tb + kt * step;
+    const __amdgpu_buffer_rsrc_t rs = stage_rsrc(tb + kt * step);
 #pragma unroll
     for (int h = 0; h < NB; ++h) {
       const int64_t k0 = kt * M::KT + kb[h];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const bool ok = mnok[h] && (k0 + i < K);
-        r[4 * h + i] =
-            *reinterpret_cast<const u32x4*>(ok ? sb + off0[h] + i * dk_bytes : zero_chunk());
+        r[4 * h + i] = buf_load16(rs, ok ? off0[h] + i * dk_bytes : kBufOut);
       }
     }
   }
