@@ -10,8 +10,9 @@
 // global->LDS copy and the 16-byte fragment reads of the MFMA loop avoid bank
 // conflicts.  An operand that is contiguous along M/N in memory is transposed
 // in registers on its way to LDS, so every contraction runs the same inner
-// loop.  Two LDS stages: the global loads of step k+2 are in flight while
-// step k is multiplied.
+// loop.  Two LDS stages.  K-contiguous operands are copied straight from
+// global memory into LDS (step k+1 in flight while step k is multiplied);
+// the register-staged copies keep the loads of step k+2 in flight.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -390,10 +391,108 @@ __device__ __forceinline__ void mfma_stage(Acc& acc, const char* ldsA, const cha
   Mfma<T>::step(acc, a1, b1);
 }
 
-// Full K loop for the tile at (m0, n0).  `lds` holds kLdsGemm bytes.
+// ---------------------------------------------------------------------------
+// Direct global->LDS copy (buffer_load ... lds) of one K-contiguous operand
+// stage.  One wave instruction fills 1 KiB of LDS (8 tile rows of 128 bytes),
+// lane i writing the 16 bytes at offset 16 i; each lane therefore loads the
+// global chunk that the swizzle assigns to its slot.  No registers hold the
+// data, and the copy of stage k+1 overlaps the MFMAs of stage k.
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <typename T, Lay L> struct DmaCopy {
+  using M = LayMath<T, L>;
+  static constexpr int E = Elem<T>::kChunk;
+  static constexpr int NI = kBM / 8 / (kThreads / 64);   // 1 KiB groups per wave
+  const char* tb;
+  int64_t step, K;
+  uint32_t off[NI];
+  int kc[NI];
+  uint32_t rowok;
+  int grp0;
+  __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
+    tb = static_cast<const char*>(op.ptr) + M::tile_base(op, r0);
+    step = M::stage_step(op);
+    K = op.K;
+    const int lane = tid & 63;
+    grp0 = (tid >> 6) * NI;
+    rowok = 0;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int row = 8 * (grp0 + i) + (lane >> 3);
+      kc[i] = ((lane & 7) ^ swz(row)) * E;
+      off[i] = M::rel(op, row, kc[i]);
+      if (r0 + row < op.rows) rowok |= 1u << i;
+    }
+  }
+  __device__ __forceinline__ void issue(int64_t kt, char* lds) const {
+    const __amdgpu_buffer_rsrc_t rs = stage_rsrc(tb + kt * step);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const bool ok = ((rowok >> i) & 1u) && (kt * M::KT + kc[i] < K);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(lds + (grp0 + i) * 1024), 16,
+                                               ok ? off[i] : kBufOut, 0, 0, 0);
+    }
+  }
+};
+
+// All of this wave's direct copies have landed, then a workgroup barrier.
+// The barrier carries no memory fence (the fence of __syncthreads would wait
+// for every copy in flight); the empty asm statements keep the compiler from
+// moving LDS accesses across it.
+__device__ __forceinline__ void dma_wait_barrier() {
+  __builtin_amdgcn_s_waitcnt(0x3f70);   // vmcnt(0), other counters unconstrained
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <typename T, Lay LA, Lay LB>
+__device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operand& B, int64_t m0,
+                                                  int64_t n0, int64_t K, char* lds, Acc& acc) {
+  constexpr int KT = kRowBytes / sizeof(T);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % kWavesM, wn = wave / kWavesM;
+  const int64_t nk = (K + KT - 1) / KT;
+
+#pragma unroll
+  for (int i = 0; i < kTM; ++i)
+#pragma unroll
+    for (int j = 0; j < kTN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+  DmaCopy<T, LA> ca;
+  DmaCopy<T, LB> cb;
+  ca.init(A, m0, tid);
+  cb.init(B, n0, tid);
+  ca.issue(0, lds);
+  cb.issue(0, lds + kStageBytes);
+  for (int64_t kt = 0; kt < nk; ++kt) {
+    char* cur = lds + (kt & 1) * (2 * kStageBytes);
+    char* nxt = lds + ((kt + 1) & 1) * (2 * kStageBytes);
+    // stage kt is in LDS for every wave, and every wave is done with kt-1
+    dma_wait_barrier();
+    if (kt + 1 < nk) {
+      ca.issue(kt + 1, nxt);
+      cb.issue(kt + 1, nxt + kStageBytes);
+    }
+    mfma_stage<T>(acc, cur, cur + kStageBytes, wm, wn, lane);
+  }
+  __syncthreads();
+}
+
+// Full K loop for the tile at (m0, n0).  `lds` holds kLdsGemm bytes.  Both
+// operands K-contiguous: direct copies; otherwise register-staged copies.
 template <typename T, Lay LA, Lay LB>
 __device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B, int64_t m0,
                                               int64_t n0, int64_t K, char* lds, Acc& acc) {
+  if constexpr (KContig<LA>::value && KContig<LB>::value) {
+    gemm_mainloop_dma<T, LA, LB>(A, B, m0, n0, K, lds, acc);
+    return;
+  }
   constexpr int KT = kRowBytes / sizeof(T);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
