@@ -26,7 +26,7 @@
  *               enqueued on it and the call returns without waiting; buffers
  *               must stay valid until the stream has finished the work.
  *   Layout      Matrices are row-major and contiguous, 16-byte aligned.
- *               d must be a multiple of 8.
+ *               d must be a multiple of 8 and at most 4194240 (64 x 65535).
  *   Errors      Scalar and pointer arguments are checked on the host before any
  *               launch; a bad argument returns an error code and enqueues
  *               nothing.  A launch failure returns MC_ERR_HIP.  No exception or

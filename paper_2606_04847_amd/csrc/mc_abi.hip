@@ -12,12 +12,13 @@ namespace {
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 constexpr int64_t kMaxDim = (int64_t(1) << 31) - 1;
+constexpr int64_t kMaxD = int64_t(64) * 65535;   // transposes tile d over grid y
 
 mc_status_t check_dims(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   if (T < 0 || d < 1 || V < 1) return MC_ERR_INVALID_ARG;
   if (dt != MC_F32 && dt != MC_BF16) return MC_ERR_UNSUPPORTED;
   if (d % 8 != 0) return MC_ERR_UNSUPPORTED;
-  if (T > kMaxDim || V > kMaxDim - 256 || d > kMaxDim) return MC_ERR_UNSUPPORTED;
+  if (T > kMaxDim || V > kMaxDim - 256 || d > kMaxD) return MC_ERR_UNSUPPORTED;
   // one launch must stay below 2^31 workgroups
   if (mc::cdiv(T, 256) * mc::cdiv(V, 256) > kMaxDim) return MC_ERR_UNSUPPORTED;
   return MC_OK;

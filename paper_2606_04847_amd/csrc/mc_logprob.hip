@@ -338,6 +338,54 @@ __global__ __launch_bounds__(256) void k_onehot_dh(const T* __restrict__ W,
 }
 
 // --- deterministic bucketing of tokens by target (for the one-hot part of dW)
+// out[c][r] = in[r][c] for r < rows, c < cols, and out[c][r] = 0 for
+// rows <= r < 64 ceil(rows / 64) (ld_out covers that padding; cols, ld_in and
+// ld_out are multiples of 8).  The zero padding matters: a K-contiguous
+// operand is copied in 16-byte chunks, so up to the next multiple of 8 (bf16)
+// past K is read.  64 x 64 tiles through LDS (grid x over row tiles, y over
+// column tiles); 16-byte global accesses along both rows.  Gives the
+// backward's contractions over the vocabulary and over tokens operands that
+// run along K.
+template <typename T>
+__global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ in, int64_t rows,
+                                                   int64_t cols, int64_t ld_in,
+                                                   T* __restrict__ out, int64_t ld_out) {
+  constexpr int V = 16 / sizeof(T);   // elements per 16-byte access
+  constexpr int P = 64 + V;           // padded LDS row (elements)
+  __shared__ __attribute__((aligned(16))) T tile[64 * P];
+  const int64_t r0 = int64_t(blockIdx.x) * 64, c0 = int64_t(blockIdx.y) * 64;
+  const int t = threadIdx.x;
+  // load 64 rows x 64 columns (zeros outside): each thread 16 consecutive
+  // columns of one row
+  {
+    const int rr = t >> 2, cc = (t & 3) * 16;
+    const int64_t r = r0 + rr;
+#pragma unroll
+    for (int h = 0; h < 16 / V; ++h) {
+      const int64_t c = c0 + cc + h * V;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (r < rows && c < cols) v = *reinterpret_cast<const u32x4*>(in + r * ld_in + c);
+      *reinterpret_cast<u32x4*>(&tile[rr * P + cc + h * V]) = v;
+    }
+  }
+  __syncthreads();
+  // store 64 output rows (input columns) x 64 output columns (input rows,
+  // the padding included)
+  {
+    const int oc = t >> 2, orr = (t & 3) * 16;
+    const int64_t c = c0 + oc;
+    if (c >= cols) return;
+    T* o = out + c * ld_out + r0 + orr;
+#pragma unroll
+    for (int h = 0; h < 16 / V; ++h) {
+      T v[V];
+#pragma unroll
+      for (int e = 0; e < V; ++e) v[e] = tile[(orr + h * V + e) * P + oc];
+      *reinterpret_cast<u32x4*>(o + h * V) = __builtin_bit_cast(u32x4, v);
+    }
+  }
+}
+
 __global__ void k_fill_i32(int* __restrict__ p, int64_t n, int v) {
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i < n) p[i] = v;
@@ -445,13 +493,13 @@ template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand B, int64_t K,
                                                              int nTm, int nTn, EpiStore epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiStore::kLdsExtra];
-  gemm_body<T, Lay::TileTK, Lay::MNMajor>(A, B, K, nTm, nTn, epi, lds);
+  gemm_body<T, Lay::TileTK, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
 }
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand B, int64_t K,
                                                              int nTm, int nTn, EpiStore epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiStore::kLdsExtra];
-  gemm_body<T, Lay::TileVT, Lay::MNMajor>(A, B, K, nTm, nTn, epi, lds);
+  gemm_body<T, Lay::TileVT, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
 }
 
 // Forward over a vocabulary shard [v_off, v_off + Vs) of a V-entry vocabulary
@@ -504,6 +552,8 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   const int64_t pld = cdiv(Tn, 64) * 64;
   Carve cv(ws);
   T* P = cv.take<T>(size_t(pld) * ld);
+  T* Wt = cv.take<T>(size_t(d) * ld);    // [d x chunk] transpose of W's chunk rows
+  T* Ht = cv.take<T>(size_t(d) * pld);   // [d x T] transpose of H
   int* counts = cv.take<int>(Vs);
   int* cursor = cv.take<int>(Vs);
   int* offsets = cv.take<int>(Vs + 1);
@@ -544,10 +594,17 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                          dim3(kThreads), 0, s, A, B, d, nTm, nTn, epi);
     }
     if (dH) {
-      // dH (+)= P~ Wc : M = T, N = d, K = chunk columns
-      Operand A{P, pld, Tn, ldc}, B{Wc, d, d, width};
+      // dH (+)= P~ Wc : M = T, N = d, K = chunk columns, with Wc^T [d x ldc]
+      // so that both operands run along K
+      {
+        ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(width) * d);
+        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(width, 64), cdiv(d, 64)), dim3(256), 0, s,
+                           Wc, width, d, d, Wt, ldc);
+      }
+      Operand A{P, pld, Tn, ldc}, B{Wt, ldc, d, width};   // ldc = 64 ceil(width / 64)
       if (!operand_in_bounds<T, Lay::TileTK>(A, p_bytes) ||
-          !operand_in_bounds<T, Lay::MNMajor>(B, wc_bytes))
+          !operand_in_bounds<T, Lay::KMajor>(B, size_t(d) * ldc * sizeof(T)) ||
+          width > ldc || size_t(d) * ldc > size_t(d) * ld)
         return hipErrorInvalidValue;
       EpiStore epi{dH, d, Tn, d, (v0 > 0 || (flags & MC_BWD_ACCUMULATE_DHIDDEN)) ? 1 : 0};
       ProfScope ps_(s, "logprob_bwd_dhidden", 2.0 * Tn * d * width,
@@ -557,10 +614,16 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                          dim3(kThreads), 0, s, A, B, ldc, nTm, nTd, epi);
     }
     if (dW) {
-      // dW[chunk] (+)= P~^T H : M = chunk columns, N = d, K = T
-      Operand A{P, pld, ldc, Tn}, B{H, d, d, Tn};
+      // dW[chunk] (+)= P~^T H : M = chunk columns, N = d, K = T, with H^T
+      // [d x pld] (made once) so that the N operand runs along K
+      if (v0 == 0) {
+        ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(Tn) * d);
+        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(Tn, 64), cdiv(d, 64)), dim3(256), 0, s,
+                           H, Tn, d, d, Ht, pld);
+      }
+      Operand A{P, pld, ldc, Tn}, B{Ht, pld, d, Tn};   // pld = 64 ceil(Tn / 64)
       if (!operand_in_bounds<T, Lay::TileVT>(A, p_bytes) ||
-          !operand_in_bounds<T, Lay::MNMajor>(B, size_t(Tn) * d * sizeof(T)))
+          !operand_in_bounds<T, Lay::KMajor>(B, size_t(d) * pld * sizeof(T)))
         return hipErrorInvalidValue;
       EpiStore epi{dW + v0 * d, d, width, d, (flags & MC_BWD_ACCUMULATE_DWEIGHT) ? 1 : 0};
       const int nTv = int(cdiv(width, kBM));
@@ -600,11 +663,14 @@ size_t fwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t) {
   return 3 * align_up(n * sizeof(float), kWsAlign);
 }
 
-size_t bwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t dt) {
+size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   const size_t es = dt == MC_BF16 ? 2 : 4;
   const int64_t chunk = bwd_chunk_cols(T, V, es);
   const size_t ld = align_up(size_t(std::min(chunk, V)), 64);
-  size_t n = align_up(size_t(cdiv(T, 64)) * 64 * ld * es, kWsAlign);
+  const size_t pld = size_t(cdiv(T, 64)) * 64;
+  size_t n = align_up(pld * ld * es, kWsAlign);
+  n += align_up(size_t(d) * ld * es, kWsAlign);
+  n += align_up(size_t(d) * pld * es, kWsAlign);
   n += 2 * align_up(size_t(V) * 4, kWsAlign);
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);

@@ -9,10 +9,10 @@
 // chunk index is XOR-swizzled with the row so that the 16-byte writes of the
 // global->LDS copy and the 16-byte fragment reads of the MFMA loop avoid bank
 // conflicts.  An operand that is contiguous along M/N in memory is transposed
-// in registers on its way to LDS, so every contraction runs the same inner
-// loop.  Two LDS stages.  K-contiguous operands are copied straight from
-// global memory into LDS (step k+1 in flight while step k is multiplied);
-// the register-staged copies keep the loads of step k+2 in flight.
+// in registers on its way to LDS (fp32), or copied as is and read back with
+// the transposing LDS read (bf16).  Two LDS stages.  Direct global->LDS
+// copies keep step k+1 in flight while step k is multiplied; the
+// register-staged copies (fp32 M/N-contiguous operands) keep step k+2.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -55,7 +55,12 @@ template <> struct Elem<bf16_t> { static constexpr int kChunk = 8; };
 template <> struct Elem<float> { static constexpr int kChunk = 4; };
 
 // Operand of a contraction C[m][n] = sum_k A[m][k] B[n][k].  For A the "rows"
-// are M, for B they are N.  Rows >= rows and k >= K read as zero.  The layout
+// are M, for B they are N.  Rows >= rows and k >= K read as zero, at the
+// granularity of a 16-byte chunk: a K-contiguous operand's chunk is copied
+// whole when its first element is below K, so up to the next multiple of the
+// chunk (8 bf16, 4 fp32) past K must be readable and hold zeros (or K be a
+// multiple of it); an M/N-contiguous operand's chunk is taken whole when its
+// first row is below `rows`, with the same rule along the rows.  The layout
 // is a template policy of the copy (see below); `ld` is its stride parameter.
 struct Operand {
   const void* ptr;
@@ -362,31 +367,65 @@ template <> struct Mfma<float> {
   }
 };
 
-template <typename T>
+// LDS format of one operand stage.  K: 256 rows of 128 bytes of K (the
+// register-staged copies and the direct copies of K-contiguous operands).
+// MN (bf16 only): 64 K rows of 256 elements along M/N, 512 bytes each, the
+// 16-byte chunk index XOR-ed with 4 (k & 3); fragments are read with the
+// transposing LDS read.
+enum class Stg { K, MN };
+
+__device__ __forceinline__ int lds_off_mn(int k, int m) {
+  return k * (kBM * 2) + (((m >> 3) ^ ((k & 3) << 2)) << 4) + ((m & 7) << 1);
+}
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4_t;
+
+// One 32 x 16 MFMA operand fragment (lane l: row l % 32, k = 8 (l / 32) + 0..7)
+// from an MN stage.  ds_read_b64_tr_b16 hands lane i of each 16-lane group
+// element i % 4 of the 8-byte pieces loaded by lanes 4 e + i / 4 (e = 0..3) of
+// that group; so lane s loads 4 consecutive rows at one k, and after the
+// exchange each lane holds 4 consecutive k of one row.  Two reads give 8.
+__device__ __forceinline__ u32x4 read_frag_mn(const char* base, int row0, int kk, int lane) {
+  const int g = lane >> 4, s = lane & 15;
+  const int k = 16 * kk + 8 * (g >> 1) + (s >> 2);
+  const int m = row0 + 16 * (g & 1) + 4 * (s & 3);
+  const char* p = base + lds_off_mn(k, m);
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)p);
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(p + 4 * kBM * 2));
+  const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+  return u32x4{a[0], a[1], b[0], b[1]};
+}
+
+template <Stg S>
+__device__ __forceinline__ u32x4 read_frag(const char* base, int row0, int kk, int lane) {
+  if constexpr (S == Stg::K)
+    return *reinterpret_cast<const u32x4*>(base +
+                                           lds_off(row0 + (lane & 31), 2 * kk + (lane >> 5)));
+  else
+    return read_frag_mn(base, row0, kk, lane);
+}
+
+template <typename T, Stg SA, Stg SB>
 __device__ __forceinline__ void read_frags(u32x4 (&a)[kTM], u32x4 (&b)[kTN], const char* ldsA,
                                            const char* ldsB, int wm, int wn, int lane, int kk) {
-  const int c = 2 * kk + (lane >> 5);
 #pragma unroll
-  for (int i = 0; i < kTM; ++i)
-    a[i] = *reinterpret_cast<const u32x4*>(
-        ldsA + lds_off(wm * kWaveRows + i * 32 + (lane & 31), c));
+  for (int i = 0; i < kTM; ++i) a[i] = read_frag<SA>(ldsA, wm * kWaveRows + i * 32, kk, lane);
 #pragma unroll
-  for (int j = 0; j < kTN; ++j)
-    b[j] = *reinterpret_cast<const u32x4*>(
-        ldsB + lds_off(wn * kWaveCols + j * 32 + (lane & 31), c));
+  for (int j = 0; j < kTN; ++j) b[j] = read_frag<SB>(ldsB, wn * kWaveCols + j * 32, kk, lane);
 }
 
 // The fragments of slice kk+1 are requested before the MFMAs of slice kk.
-template <typename T>
+template <typename T, Stg SA = Stg::K, Stg SB = Stg::K>
 __device__ __forceinline__ void mfma_stage(Acc& acc, const char* ldsA, const char* ldsB, int wm,
                                            int wn, int lane) {
   u32x4 a0[kTM], b0[kTN], a1[kTM], b1[kTN];
-  read_frags<T>(a0, b0, ldsA, ldsB, wm, wn, lane, 0);
-  read_frags<T>(a1, b1, ldsA, ldsB, wm, wn, lane, 1);
+  read_frags<T, SA, SB>(a0, b0, ldsA, ldsB, wm, wn, lane, 0);
+  read_frags<T, SA, SB>(a1, b1, ldsA, ldsB, wm, wn, lane, 1);
   Mfma<T>::step(acc, a0, b0);
-  read_frags<T>(a0, b0, ldsA, ldsB, wm, wn, lane, 2);
+  read_frags<T, SA, SB>(a0, b0, ldsA, ldsB, wm, wn, lane, 2);
   Mfma<T>::step(acc, a1, b1);
-  read_frags<T>(a1, b1, ldsA, ldsB, wm, wn, lane, 3);
+  read_frags<T, SA, SB>(a1, b1, ldsA, ldsB, wm, wn, lane, 3);
   Mfma<T>::step(acc, a0, b0);
   Mfma<T>::step(acc, a1, b1);
 }
@@ -398,9 +437,53 @@ __device__ __forceinline__ void mfma_stage(Acc& acc, const char* ldsA, const cha
 // global chunk that the swizzle assigns to its slot.  No registers hold the
 // data, and the copy of stage k+1 overlaps the MFMAs of stage k.
 // ---------------------------------------------------------------------------
-typedef __attribute__((address_space(3))) void lds_void_t;
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
-template <typename T, Lay L> struct DmaCopy {
+// Buffer resource words of a raw (stride 0) view starting at `base`, forced
+// into scalar registers (the base is uniform across the wave by construction).
+__device__ __forceinline__ i32x4 dma_rsrc(const char* base) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane(int(uint32_t(a)));
+  r[1] = __builtin_amdgcn_readfirstlane(int(uint32_t(a >> 32) & 0xffffu));
+  r[2] = int(kBufRange);
+  r[3] = 0x00020000;
+  return r;
+}
+
+// LDS byte address of a (wave-uniform) pointer into the workgroup's LDS.
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  return __builtin_amdgcn_readfirstlane(
+      uint32_t(uintptr_t((__attribute__((address_space(3))) const char*)p)));
+}
+
+// One 16-byte-per-lane direct load into LDS: lane i's chunk lands at
+// m0 + 16 i.  Issued from inline asm so that the compiler's wait insertion
+// does not serialise later LDS reads behind the copy; the loops that issue
+// these wait for them explicitly (vmcnt) before their barrier, and no
+// compiler-generated vector-memory load is outstanding meanwhile.
+// The compiler inserts no hazard padding before an asm statement, so the
+// statement carries its own: a VALU write of an SGPR (the readfirstlane of
+// the resource words) needs 5 wait states before a vector-memory
+// instruction reads that SGPR, and an SALU write of m0 needs 1 before the
+// LDS-direct load.
+__device__ __forceinline__ void dma16(const i32x4& rs, uint32_t voff, uint32_t m0) {
+  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :: "v"(voff), "s"(rs), "{m0}"(m0) : "memory");
+}
+
+// The same base pointer with both halves forced into scalar registers.
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  const uint64_t lo = uint32_t(__builtin_amdgcn_readfirstlane(int(uint32_t(a))));
+  const uint64_t hi = uint32_t(__builtin_amdgcn_readfirstlane(int(uint32_t(a >> 32))));
+  return reinterpret_cast<const char*>((hi << 32) | lo);
+}
+
+// kAsm: issue through dma16 (loops that also use the transposing LDS read,
+// which the compiler would otherwise order behind every copy in flight);
+// otherwise through the compiler builtin.
+template <typename T, Lay L, bool kAsm> struct DmaCopy {
   using M = LayMath<T, L>;
   static constexpr int E = Elem<T>::kChunk;
   static constexpr int NI = kBM / 8 / (kThreads / 64);   // 1 KiB groups per wave
@@ -415,7 +498,7 @@ template <typename T, Lay L> struct DmaCopy {
     step = M::stage_step(op);
     K = op.K;
     const int lane = tid & 63;
-    grp0 = (tid >> 6) * NI;
+    grp0 = __builtin_amdgcn_readfirstlane(tid >> 6) * NI;
     rowok = 0;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
@@ -426,15 +509,75 @@ template <typename T, Lay L> struct DmaCopy {
     }
   }
   __device__ __forceinline__ void issue(int64_t kt, char* lds) const {
-    const __amdgpu_buffer_rsrc_t rs = stage_rsrc(tb + kt * step);
+    if constexpr (kAsm) {
+      const i32x4 rs = dma_rsrc(tb + kt * step);
+      const uint32_t m0 = lds_addr(lds) + grp0 * 1024;
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const bool ok = ((rowok >> i) & 1u) && (kt * M::KT + kc[i] < K);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(lds + (grp0 + i) * 1024), 16,
-                                               ok ? off[i] : kBufOut, 0, 0, 0);
+      for (int i = 0; i < NI; ++i) {
+        const bool ok = ((rowok >> i) & 1u) && (kt * M::KT + kc[i] < K);
+        dma16(rs, ok ? off[i] : kBufOut, m0 + i * 1024);
+      }
+    } else {
+      const __amdgpu_buffer_rsrc_t rs = stage_rsrc(uniform_ptr(tb + kt * step));
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const bool ok = ((rowok >> i) & 1u) && (kt * M::KT + kc[i] < K);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rs, (__attribute__((address_space(3))) void*)(lds + (grp0 + i) * 1024), 16,
+            ok ? off[i] : kBufOut, 0, 0, 0);
+      }
     }
   }
 };
+
+// Direct copy of one M/N-contiguous bf16 operand stage into the MN format:
+// one wave instruction fills 1 KiB (two K rows of 256 elements); lane i
+// writes slot i % 32 of K row 2 g + i / 32 and loads the 8-element chunk
+// that the swizzle assigns to that slot.
+template <Lay L> struct DmaCopyMN {
+  using M = LayMath<bf16_t, L>;
+  static constexpr int NI = kStageBytes / 1024 / (kThreads / 64);   // 1 KiB groups per wave
+  const char* tb;
+  int64_t step, K;
+  uint32_t off[NI];
+  int kr[NI];
+  uint32_t mok;
+  int grp0;
+  __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
+    tb = static_cast<const char*>(op.ptr) + M::tile_base(op, r0);
+    step = M::stage_step(op);
+    K = op.K;
+    const int lane = tid & 63;
+    grp0 = __builtin_amdgcn_readfirstlane(tid >> 6) * NI;
+    mok = 0;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int k = 2 * (grp0 + i) + (lane >> 5);
+      const int c = (lane & 31) ^ ((k & 3) << 2);
+      kr[i] = k;
+      off[i] = M::rel(op, 8 * c, k);
+      if (r0 + 8 * c < op.rows) mok |= 1u << i;
+    }
+  }
+  __device__ __forceinline__ void issue(int64_t kt, char* lds) const {
+    const i32x4 rs = dma_rsrc(tb + kt * step);
+    const uint32_t m0 = lds_addr(lds) + grp0 * 1024;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const bool ok = ((mok >> i) & 1u) && (kt * M::KT + kr[i] < K);
+      dma16(rs, ok ? off[i] : kBufOut, m0 + i * 1024);
+    }
+  }
+};
+
+template <typename T, Lay L> struct DmaOf {
+  static constexpr Stg stg = KContig<L>::value ? Stg::K : Stg::MN;
+};
+template <typename T, Lay L, bool kAsm, bool KC = KContig<L>::value> struct DmaSel;
+template <typename T, Lay L, bool kAsm> struct DmaSel<T, L, kAsm, true> {
+  typedef DmaCopy<T, L, kAsm> type;
+};
+template <Lay L, bool kAsm> struct DmaSel<bf16_t, L, kAsm, false> { typedef DmaCopyMN<L> type; };
 
 // All of this wave's direct copies have landed, then a workgroup barrier.
 // The barrier carries no memory fence (the fence of __syncthreads would wait
@@ -464,8 +607,9 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-  DmaCopy<T, LA> ca;
-  DmaCopy<T, LB> cb;
+  constexpr bool kAsm = !(KContig<LA>::value && KContig<LB>::value);
+  typename DmaSel<T, LA, kAsm>::type ca;
+  typename DmaSel<T, LB, kAsm>::type cb;
   ca.init(A, m0, tid);
   cb.init(B, n0, tid);
   ca.issue(0, lds);
@@ -479,20 +623,16 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
       ca.issue(kt + 1, nxt);
       cb.issue(kt + 1, nxt + kStageBytes);
     }
-    mfma_stage<T>(acc, cur, cur + kStageBytes, wm, wn, lane);
+    mfma_stage<T, DmaOf<T, LA>::stg, DmaOf<T, LB>::stg>(acc, cur, cur + kStageBytes, wm, wn,
+                                                         lane);
   }
   __syncthreads();
 }
 
-// Full K loop for the tile at (m0, n0).  `lds` holds kLdsGemm bytes.  Both
-// operands K-contiguous: direct copies; otherwise register-staged copies.
+// Full K loop with register-staged copies (loads of step k+2 in flight).
 template <typename T, Lay LA, Lay LB>
-__device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B, int64_t m0,
-                                              int64_t n0, int64_t K, char* lds, Acc& acc) {
-  if constexpr (KContig<LA>::value && KContig<LB>::value) {
-    gemm_mainloop_dma<T, LA, LB>(A, B, m0, n0, K, lds, acc);
-    return;
-  }
+__device__ __forceinline__ void gemm_mainloop_reg(const Operand& A, const Operand& B, int64_t m0,
+                                                  int64_t n0, int64_t K, char* lds, Acc& acc) {
   constexpr int KT = kRowBytes / sizeof(T);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -534,6 +674,18 @@ __device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B
     }
     __syncthreads();
   }
+}
+
+// Full K loop for the tile at (m0, n0).  `lds` holds kLdsGemm bytes.  bf16,
+// or fp32 with both operands K-contiguous: direct copies; otherwise (fp32
+// M/N-contiguous operands) register-staged copies.
+template <typename T, Lay LA, Lay LB>
+__device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B, int64_t m0,
+                                              int64_t n0, int64_t K, char* lds, Acc& acc) {
+  if constexpr ((KContig<LA>::value && KContig<LB>::value) || sizeof(T) == 2)
+    gemm_mainloop_dma<T, LA, LB>(A, B, m0, n0, K, lds, acc);
+  else
+    gemm_mainloop_reg<T, LA, LB>(A, B, m0, n0, K, lds, acc);
 }
 
 // This lane's wave coordinates, and the row / column (within the tile) of

@@ -174,6 +174,48 @@ def test_determinism_bit_identical():
         assert np.array_equal(a[k], b[k]), k
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_workspace_contents_do_not_matter(dtype):
+    # The ABI promises that workspace contents on entry do not matter.  A
+    # workspace of 0xFF bytes (NaN in both dtypes) must give results
+    # bit-identical to a zeroed one.  The shape is ragged everywhere
+    # (T, V and the shard widths are not multiples of 8) so every padded
+    # region of every transient operand is exercised.
+    mc = _mc()
+    lib = mc.load_library()
+    d, V = 136, 1003
+    case = small_case(scaled_config(1, d=d, V=V, dtype=dtype, seed=61))   # T = 613
+    H, W, y = device_tensors(case)
+    T = H.shape[0]
+    code = 1 if dtype == "bf16" else 0
+    rng = np.random.default_rng(62)
+    dl = torch.from_numpy((rng.standard_normal(T) * 1e-2).astype(np.float32)).cuda()
+
+    def ws(nbytes, fill):
+        return torch.full((max(int(nbytes), 1),), fill, dtype=torch.uint8, device="cuda")
+
+    outs = []
+    for fill in (0, 255):
+        f_ws = ws(lib.mc_logprob_fwd_workspace_size(T, d, V, code), fill)
+        logp, lse = mc.logprob_fwd(H, W, y, workspace=f_ws)
+        b_ws = ws(lib.mc_logprob_bwd_workspace_size(T, d, V, code), fill)
+        dH, dW = mc.logprob_bwd(H, W, y, lse, dl, workspace=b_ws)
+        Ws = W[300:1003].contiguous()
+        s_ws = ws(lib.mc_logprob_bwd_workspace_size(T, d, Ws.shape[0], code), fill)
+        sh, sw = mc.logprob_bwd_shard(H, Ws, y, lse, dl, 300, V, workspace=s_ws)
+        torch.cuda.synchronize()
+        outs.append((logp, lse, dH, dW, sh, sw))
+    for a, b in zip(*outs):
+        assert torch.isfinite(b).all()
+        assert torch.equal(a, b)
+    lo, so = oracle.logprob_fwd(case["H"], case["W"], case["y"])
+    dH_o, dW_o = oracle.logprob_bwd(case["H"], case["W"], case["y"], so,
+                                    dl.cpu().numpy().astype(np.float64))
+    assert np.max(np.abs(outs[1][0].cpu().numpy() - lo)) <= LOGP_ATOL
+    assert rel_fro(outs[1][2].cpu().numpy(), dH_o) <= GRAD_RTOL
+    assert rel_fro(outs[1][3].cpu().numpy(), dW_o) <= GRAD_RTOL
+
+
 # ---------------------------------------------------------------------------
 # mc_rl_loss alone: identical fp32 inputs on both sides
 # ---------------------------------------------------------------------------
