@@ -14,37 +14,49 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
 
-__device__ __forceinline__ float half_max(float x) {
-#pragma unroll
-  for (int m = 16; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m));
-  return x;
+// Combine x over lanes l and l ^ 32 (the two halves of a 32 x 32 accumulator
+// block hold alternate groups of 4 rows of the same column).  With both
+// operands equal, v_permlane32_swap leaves (x[l % 32], x[l % 32 + 32]) in
+// every lane.
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
+                                                  __builtin_bit_cast(uint32_t, x), false, false);
+  return fmaxf(__builtin_bit_cast(float, uint32_t(r[0])), __builtin_bit_cast(float, uint32_t(r[1])));
 }
-__device__ __forceinline__ float half_sum(float x) {
-#pragma unroll
-  for (int m = 16; m >= 1; m >>= 1) x += __shfl_xor(x, m);
-  return x;
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
+                                                  __builtin_bit_cast(uint32_t, x), false, false);
+  return __builtin_bit_cast(float, uint32_t(r[0])) + __builtin_bit_cast(float, uint32_t(r[1]));
+}
+
+// Row (within the wave's 64) of accumulator element e of block i in this lane.
+__device__ __forceinline__ int wrow(int i, int e, int lane) {
+  return i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
 }
 
 // ---------------------------------------------------------------------------
-// Forward epilogue.  For each of the tile's 256 rows: max, sum of exp and
-// (optionally) sum of exp * z over the tile's valid columns -> one (m, s, u)
-// partial per (vocab tile, row); the target logit z[t, y_t] is written by the
-// one lane that holds it.  The weight may be a vocabulary shard: column c of
-// this launch is vocabulary entry v_off + c.
+// Forward epilogue.  The tile's rows are vocabulary entries (M) and its
+// columns tokens (N), so each lane holds, for each of its kTN token columns,
+// 32 of the wave's 64 vocabulary rows and its partner lane (l ^ 32) the other
+// 32.  Per token: max, sum of exp and (optionally) sum of exp * z over the
+// tile's valid rows -> one (m, s, u) partial per (vocab tile, token); the
+// target logit z[t, y_t] is written by the one lane that holds it.  The
+// weight may be a vocabulary shard: row r of this launch is vocabulary entry
+// v_off + r.
 // ---------------------------------------------------------------------------
 struct EpiFwd {
   const int64_t* y;
-  int64_t T, Vs, v_off;   // rows, shard width, shard offset
-  float* part_m;          // [nTn][T]
-  float* part_s;          // [nTn][T]
-  float* part_u;          // [nTn][T] or null (no entropy)
+  int64_t T, Vs, v_off;   // tokens, shard width, shard offset
+  float* part_m;          // [nTv][T]
+  float* part_s;          // [nTv][T]
+  float* part_u;          // [nTv][T] or null (no entropy)
   float* zy;              // [T]: receives z[t, y_t] for targets inside the shard
-  static constexpr int kLdsExtra = 256 * 4 + 3 * kWavesN * 256 * 4;
+  static constexpr int kLdsExtra = 256 * 4 + 3 * kWavesM * 256 * 4;
 
-  __device__ void prologue(int64_t m0, int64_t, char* extra) const {
+  __device__ void prologue(int64_t, int64_t n0, char* extra) const {
     int* ys = reinterpret_cast<int*>(extra);
-    for (int i = threadIdx.x; i < kBM; i += kThreads) {
-      const int64_t t = m0 + i;
+    for (int i = threadIdx.x; i < kBN; i += kThreads) {
+      const int64_t t = n0 + i;
       int v = -1;
       if (t < T) {
         const int64_t yl = y[t] - v_off;
@@ -54,73 +66,87 @@ struct EpiFwd {
     }
   }
 
-  __device__ void epilogue(Acc& acc, int, int tn, int64_t m0, int64_t n0, char*,
+  // max / sum exp / sum exp z of block column j over this lane's rows; kFull:
+  // all 64 rows of the wave are valid (no per-element mask)
+  template <bool kFull>
+  __device__ __forceinline__ void column(const Acc& acc, int j, int vlim, int lane, bool with_u,
+                                         float& mx, float& s, float& u) const {
+    mx = kNegInf;
+#pragma unroll
+    for (int i = 0; i < kTM; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (kFull || wrow(i, e, lane) < vlim) mx = fmaxf(mx, acc[i][j][e]);
+    mx = pair_max(mx);
+    const float mb = mx * kLog2e;
+    s = 0.0f;
+    u = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kTM; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (kFull || wrow(i, e, lane) < vlim) {
+          const float x = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
+          s += x;
+          if (with_u) u = fmaf(x, acc[i][j][e], u);
+        }
+    s = pair_sum(s);
+    if (with_u) u = pair_sum(u);
+  }
+
+  __device__ void epilogue(Acc& acc, int tm, int, int64_t m0, int64_t n0, char*,
                            char* extra) const {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wm = wave_m(), wn = wave_n();
     const int* ys = reinterpret_cast<const int*>(extra);
-    float* red = reinterpret_cast<float*>(extra + 1024);   // [m|s|u][wn][row]
-    const int cbase = int(n0) + wn * kWaveCols;
-    const int vlim = int(min<int64_t>(Vs - cbase, kWaveCols));   // valid columns of this wave
-    const int cl = lane & 31;
+    float* red = reinterpret_cast<float*>(extra + 1024);   // [m|s|u][wm][token]
+    const int64_t rbase = m0 + wm * kWaveRows;              // first vocab row of this wave
+    const int vlim = int(min<int64_t>(Vs - rbase, kWaveRows));
     const bool with_u = part_u != nullptr;
 #pragma unroll
-    for (int i = 0; i < kTM; ++i) {
+    for (int j = 0; j < kTN; ++j) {
+      const int tl = wn * kWaveCols + j * 32 + (lane & 31);   // token within the tile
+      float mx, s, u;
+      if (vlim >= kWaveRows) column<true>(acc, j, vlim, lane, with_u, mx, s, u);
+      else column<false>(acc, j, vlim, lane, with_u, mx, s, u);
+      // target logit: row yw of this wave, held by the lane of half (yw >> 2) & 1
+      const int yw = ys[tl] - int(rbase);
+      if (yw >= 0 && yw < kWaveRows && ((yw >> 2) & 1) == (lane >> 5)) {
+        const int ii = yw >> 5, ee = 4 * ((yw & 31) >> 3) + (yw & 3);
+        float z = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int r = acc_row(wm, i, e, lane);
-        float mx = kNegInf;
+        for (int i = 0; i < kTM; ++i)
 #pragma unroll
-        for (int j = 0; j < kTN; ++j)
-          if (j * 32 + cl < vlim) mx = fmaxf(mx, acc[i][j][e]);
-        mx = half_max(mx);
-        float s = 0.0f, u = 0.0f;
-        const float mb = mx * kLog2e;
-#pragma unroll
-        for (int j = 0; j < kTN; ++j) {
-          if (j * 32 + cl < vlim) {
-            const float x = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
-            s += x;
-            u = fmaf(x, acc[i][j][e], u);
-          }
-        }
-        s = half_sum(s);
-        if (with_u) u = half_sum(u);
-        const int yl = ys[r] - cbase;
-        if (yl >= 0 && yl < kWaveCols && (yl & 31) == cl) {
-          const int jj = yl >> 5;
-          float z = acc[i][0][e];
-#pragma unroll
-          for (int j = 1; j < kTN; ++j) z = jj == j ? acc[i][j][e] : z;
-          zy[m0 + r] = z;
-        }
-        if (cl == 0) {
-          red[(0 * kWavesN + wn) * 256 + r] = mx;
-          red[(1 * kWavesN + wn) * 256 + r] = s;
-          red[(2 * kWavesN + wn) * 256 + r] = u;
-        }
+          for (int e = 0; e < 16; ++e)
+            if (i == ii && e == ee) z = acc[i][j][e];
+        zy[n0 + tl] = z;
+      }
+      if (lane < 32) {
+        red[(0 * kWavesM + wm) * 256 + tl] = mx;
+        red[(1 * kWavesM + wm) * 256 + tl] = s;
+        red[(2 * kWavesM + wm) * 256 + tl] = u;
       }
     }
     __syncthreads();
-    for (int r = tid; r < kBM; r += kThreads) {
-      const int64_t t = m0 + r;
+    for (int tl = tid; tl < kBN; tl += kThreads) {
+      const int64_t t = n0 + tl;
       if (t >= T) continue;
-      float M = red[r];
+      float M = red[tl];
 #pragma unroll
-      for (int w = 1; w < kWavesN; ++w) M = fmaxf(M, red[w * 256 + r]);
+      for (int w = 1; w < kWavesM; ++w) M = fmaxf(M, red[w * 256 + tl]);
       float S = 0.0f, U = 0.0f;
 #pragma unroll
-      for (int w = 0; w < kWavesN; ++w) {
-        const float mw = red[w * 256 + r];
+      for (int w = 0; w < kWavesM; ++w) {
+        const float mw = red[w * 256 + tl];
         if (mw != kNegInf) {
           const float f = __builtin_amdgcn_exp2f((mw - M) * kLog2e);
-          S += red[(kWavesN + w) * 256 + r] * f;
-          U += red[(2 * kWavesN + w) * 256 + r] * f;
+          S += red[(kWavesM + w) * 256 + tl] * f;
+          U += red[(2 * kWavesM + w) * 256 + tl] * f;
         }
       }
-      part_m[int64_t(tn) * T + t] = M;
-      part_s[int64_t(tn) * T + t] = S;
-      if (with_u) part_u[int64_t(tn) * T + t] = U;
+      part_m[int64_t(tm) * T + t] = M;
+      part_s[int64_t(tm) * T + t] = S;
+      if (with_u) part_u[int64_t(tm) * T + t] = U;
     }
   }
 };
@@ -230,9 +256,11 @@ __global__ __launch_bounds__(256) void k_shard_merge(const float* __restrict__ p
 }
 
 // ---------------------------------------------------------------------------
-// Backward, step 1: recompute the logits of a vocabulary chunk and write the
-// transient operand P~[t, v] = -dlogp_t exp(z_tv - lse_t) (zero for ignored
-// rows and for the padding columns [chunk, ld)).
+// Backward, step 1: recompute the logits of a vocabulary chunk (tile rows =
+// chunk columns v, tile columns = tokens t) and write the transient operand
+// P~[t, v] = -dlogp_t exp(z_tv - lse_t) (zero for ignored tokens and for the
+// padding columns [width, ld)) in the panel layout.  A lane holds 4
+// consecutive v of one token per (block, e / 4): one 4-element store.
 // ---------------------------------------------------------------------------
 template <typename T>
 struct EpiProbs {
@@ -245,11 +273,11 @@ struct EpiProbs {
   static constexpr int64_t kPanel = 128 / sizeof(T);
   static constexpr int kLdsExtra = 2 * 256 * 4;
 
-  __device__ void prologue(int64_t m0, int64_t, char* extra) const {
+  __device__ void prologue(int64_t, int64_t n0, char* extra) const {
     float* l2 = reinterpret_cast<float*>(extra);
     float* g = l2 + 256;
-    for (int i = threadIdx.x; i < kBM; i += kThreads) {
-      const int64_t t = m0 + i;
+    for (int i = threadIdx.x; i < kBN; i += kThreads) {
+      const int64_t t = n0 + i;
       float a = 0.0f, b = 0.0f;
       if (t < Tn) {
         const int64_t yy = y[t];
@@ -268,21 +296,30 @@ struct EpiProbs {
     const float* l2 = reinterpret_cast<const float*>(extra);
     const float* g = l2 + 256;
 #pragma unroll
-    for (int i = 0; i < kTM; ++i) {
+    for (int j = 0; j < kTN; ++j) {
+      const int tl = wn * kWaveCols + j * 32 + (lane & 31);
+      const int64_t t = n0 + tl;
+      if (t >= Tn) continue;
+      const float lb = l2[tl], gs = g[tl];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int r = acc_row(wm, i, e, lane);
-        const int64_t t = m0 + r;
-        if (t >= Tn) continue;
-        const float lb = l2[r], gs = g[r];
+      for (int i = 0; i < kTM; ++i) {
 #pragma unroll
-        for (int j = 0; j < kTN; ++j) {
-          const int64_t c = n0 + acc_col(wn, j, lane);
-          if (c < ld) {
-            const float p = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -lb));
-            P[(c / kPanel) * pld * kPanel + t * kPanel + c % kPanel] =
-                T(c < width ? gs * p : 0.0f);
+        for (int q = 0; q < 4; ++q) {
+          // rows c .. c+3 of the chunk (c a multiple of 4, ld a multiple of 64)
+          const int64_t c = m0 + wm * kWaveRows + wrow(i, 4 * q, lane);
+          if (c >= ld) continue;
+          T v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float p =
+                __builtin_amdgcn_exp2f(fmaf(acc[i][j][4 * q + e], kLog2e, -lb));
+            v[e] = T(c + e < width ? gs * p : 0.0f);
           }
+          T* dst = P + (c / kPanel) * pld * kPanel + t * kPanel + c % kPanel;
+          if constexpr (sizeof(T) == 2)
+            *reinterpret_cast<u32x2*>(dst) = __builtin_bit_cast(u32x2, v);
+          else
+            *reinterpret_cast<u32x4*>(dst) = __builtin_bit_cast(u32x4, v);
         }
       }
     }
@@ -509,31 +546,32 @@ template <typename T>
 hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_t d, int64_t Vs,
                     int64_t v_off, int64_t V, float* logp, float* lse, float* entropy,
                     float* part, bool with_u, void* ws, hipStream_t s) {
-  const int nTm = int(cdiv(Tn, kBM)), nTn = int(cdiv(Vs, kBN));
+  // tile rows: vocabulary (the weight's rows), tile columns: tokens
+  const int nTv = int(cdiv(Vs, kBM)), nTt = int(cdiv(Tn, kBN));
   Carve cv(ws);
-  float* pm = cv.take<float>(size_t(nTn) * Tn);
-  float* ps = cv.take<float>(size_t(nTn) * Tn);
-  float* pu = cv.take<float>(size_t(nTn) * Tn);
+  float* pm = cv.take<float>(size_t(nTv) * Tn);
+  float* ps = cv.take<float>(size_t(nTv) * Tn);
+  float* pu = cv.take<float>(size_t(nTv) * Tn);
   if (!with_u) pu = nullptr;
   const double es = sizeof(T);
-  Operand A{H, d, Tn, d}, B{W, d, Vs, d};
-  if (!operand_in_bounds<T, Lay::KMajor>(A, size_t(Tn) * d * sizeof(T)) ||
-      !operand_in_bounds<T, Lay::KMajor>(B, size_t(Vs) * d * sizeof(T)))
+  Operand A{W, d, Vs, d}, B{H, d, Tn, d};
+  if (!operand_in_bounds<T, Lay::KMajor>(A, size_t(Vs) * d * sizeof(T)) ||
+      !operand_in_bounds<T, Lay::KMajor>(B, size_t(Tn) * d * sizeof(T)))
     return hipErrorInvalidValue;
   EpiFwd epi{y, Tn, Vs, v_off, pm, ps, pu, part ? part + 3 * Tn : logp};
   {
     ProfScope ps_(s, "logprob_fwd_gemm", 2.0 * Tn * d * Vs,
                   es * (double(Tn) * d + double(Vs) * d) + 12.0 * Tn);
-    hipLaunchKernelGGL(k_fwd_logits_lse<T>, dim3(nTm * nTn), dim3(kThreads), 0,
-                       s, A, B, d, nTm, nTn, epi);
+    hipLaunchKernelGGL(k_fwd_logits_lse<T>, dim3(nTv * nTt), dim3(kThreads), 0,
+                       s, A, B, d, nTv, nTt, epi);
   }
   {
-    ProfScope ps_(s, "logprob_fwd_merge", 0.0, (with_u ? 12.0 : 8.0) * nTn * Tn + 24.0 * Tn);
+    ProfScope ps_(s, "logprob_fwd_merge", 0.0, (with_u ? 12.0 : 8.0) * nTv * Tn + 24.0 * Tn);
     if (part)
-      hipLaunchKernelGGL(k_shard_partial, dim3(cdiv(Tn, 64)), dim3(512), 0, s, pm, ps, pu, nTn,
+      hipLaunchKernelGGL(k_shard_partial, dim3(cdiv(Tn, 64)), dim3(512), 0, s, pm, ps, pu, nTv,
                          Tn, y, v_off, Vs, part);
     else
-      hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(Tn, 64)), dim3(512), 0, s, pm, ps, pu, nTn, Tn,
+      hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(Tn, 64)), dim3(512), 0, s, pm, ps, pu, nTv, Tn,
                          y, V, logp, lse, entropy);
   }
   return hipGetLastError();
@@ -582,16 +620,17 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
     const size_t wc_bytes = size_t(Vs - v0) * d * sizeof(T);
     const size_t p_bytes = size_t(pld) * ld * sizeof(T);
     {
-      Operand A{H, d, Tn, d}, B{Wc, d, width, d};
-      if (!operand_in_bounds<T, Lay::KMajor>(A, size_t(Tn) * d * sizeof(T)) ||
-          !operand_in_bounds<T, Lay::KMajor>(B, wc_bytes) || ldc > ld)
+      // tile rows: chunk columns (up to the padded width ldc), tile columns: tokens
+      Operand A{Wc, d, width, d}, B{H, d, Tn, d};
+      if (!operand_in_bounds<T, Lay::KMajor>(A, wc_bytes) ||
+          !operand_in_bounds<T, Lay::KMajor>(B, size_t(Tn) * d * sizeof(T)) || ldc > ld)
         return hipErrorInvalidValue;
       EpiProbs<T> epi{y, lse, dlogp, Tn, V, width, ldc, pld, P};
-      const int nTn = int(cdiv(ldc, kBN));
+      const int nTv = int(cdiv(ldc, kBM)), nTt = int(cdiv(Tn, kBN));
       ProfScope ps_(s, "logprob_bwd_probs", 2.0 * Tn * d * width,
                     es * (double(Tn) * d + double(width) * d + double(Tn) * width) + 16.0 * Tn);
-      hipLaunchKernelGGL(k_bwd_probs<T>, dim3(nTm * nTn),
-                         dim3(kThreads), 0, s, A, B, d, nTm, nTn, epi);
+      hipLaunchKernelGGL(k_bwd_probs<T>, dim3(nTv * nTt),
+                         dim3(kThreads), 0, s, A, B, d, nTv, nTt, epi);
     }
     if (dH) {
       // dH (+)= P~ Wc : M = T, N = d, K = chunk columns, with Wc^T [d x ldc]
