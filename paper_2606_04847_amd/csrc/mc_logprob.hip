@@ -12,6 +12,12 @@ namespace mc {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+// Integer min / clamp (the device min/max overloads of int64 go through fp64).
+__device__ __forceinline__ int64_t imin(int64_t a, int64_t b) { return a < b ? a : b; }
+__device__ __forceinline__ int clamp_rows(int64_t n, int hi) {
+  return n <= 0 ? 0 : (n >= hi ? hi : int(n));
+}
 constexpr float kNegInf = -__builtin_huge_valf();
 
 // Combine x over lanes l and l ^ 32 (the two halves of a 32 x 32 accumulator
@@ -101,7 +107,7 @@ struct EpiFwd {
     const int* ys = reinterpret_cast<const int*>(extra);
     float* red = reinterpret_cast<float*>(extra + 1024);   // [m|s|u][wm][token]
     const int64_t rbase = m0 + wm * kWaveRows;              // first vocab row of this wave
-    const int vlim = int(min<int64_t>(Vs - rbase, kWaveRows));
+    const int vlim = clamp_rows(Vs - rbase, kWaveRows);
     const bool with_u = part_u != nullptr;
 #pragma unroll
     for (int j = 0; j < kTN; ++j) {
@@ -260,7 +266,9 @@ __global__ __launch_bounds__(256) void k_shard_merge(const float* __restrict__ p
 // chunk columns v, tile columns = tokens t) and write the transient operand
 // P~[t, v] = -dlogp_t exp(z_tv - lse_t) (zero for ignored tokens and for the
 // padding columns [width, ld)) in the panel layout.  A lane holds 4
-// consecutive v of one token per (block, e / 4): one 4-element store.
+// consecutive v of one token per (block, e / 4).  bf16: the tile is staged in
+// the (then idle) LDS operand buffers and written as whole 128-byte panel
+// rows; fp32: 4-element stores straight to memory.
 // ---------------------------------------------------------------------------
 template <typename T>
 struct EpiProbs {
@@ -289,12 +297,18 @@ struct EpiProbs {
     }
   }
 
-  __device__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char*,
-                           char* extra) const {
-    const int lane = threadIdx.x & 63;
-    const int wm = wave_m(), wn = wave_n();
-    const float* l2 = reinterpret_cast<const float*>(extra);
-    const float* g = l2 + 256;
+  // Element (t, v) of the tile staged in LDS (bf16): four 32 KiB panels of
+  // 256 token rows x 128 bytes, the 16-byte chunk index XOR-ed with t & 7.
+  __device__ static int stage_off(int v, int t) {
+    return (v >> 6) * 32768 + t * 128 + ((((v & 63) >> 3) ^ (t & 7)) << 4) + ((v & 7) << 1);
+  }
+
+  // P~ of this lane's elements.  vlim: valid rows (v < width) of the wave,
+  // llim: rows below ld (a multiple of 4); kFull: all 64 rows valid.
+  template <bool kFull>
+  __device__ __forceinline__ void values(const Acc& acc, char* lds, int lane, int wm, int wn,
+                                         const float* l2, const float* g, int vlim, int llim,
+                                         int64_t m0, int64_t n0) const {
 #pragma unroll
     for (int j = 0; j < kTN; ++j) {
       const int tl = wn * kWaveCols + j * 32 + (lane & 31);
@@ -305,22 +319,53 @@ struct EpiProbs {
       for (int i = 0; i < kTM; ++i) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          // rows c .. c+3 of the chunk (c a multiple of 4, ld a multiple of 64)
-          const int64_t c = m0 + wm * kWaveRows + wrow(i, 4 * q, lane);
-          if (c >= ld) continue;
-          T v[4];
+          const int r = wrow(i, 4 * q, lane);   // first of 4 consecutive rows of the wave
+          if (!kFull && r >= llim) continue;
+          f32x4 p;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float p =
-                __builtin_amdgcn_exp2f(fmaf(acc[i][j][4 * q + e], kLog2e, -lb));
-            v[e] = T(c + e < width ? gs * p : 0.0f);
+            p[e] = gs * __builtin_amdgcn_exp2f(fmaf(acc[i][j][4 * q + e], kLog2e, -lb));
+            if (!kFull && r + e >= vlim) p[e] = 0.0f;
           }
-          T* dst = P + (c / kPanel) * pld * kPanel + t * kPanel + c % kPanel;
-          if constexpr (sizeof(T) == 2)
-            *reinterpret_cast<u32x2*>(dst) = __builtin_bit_cast(u32x2, v);
-          else
-            *reinterpret_cast<u32x4*>(dst) = __builtin_bit_cast(u32x4, v);
+          const int vr = wm * kWaveRows + r;   // row of the tile
+          if constexpr (sizeof(T) == 2) {
+            typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+            *reinterpret_cast<u32x2*>(lds + stage_off(vr, tl)) =
+                __builtin_bit_cast(u32x2, __builtin_convertvector(p, bf16x4));
+          } else {
+            const int64_t c = m0 + vr;
+            T* dst = P + (c / kPanel) * pld * kPanel + t * kPanel + c % kPanel;
+            *reinterpret_cast<f32x4*>(dst) = p;
+          }
         }
+      }
+    }
+  }
+
+  __device__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char* lds,
+                           char* extra) const {
+    const int lane = threadIdx.x & 63;
+    const int wm = wave_m(), wn = wave_n();
+    const float* l2 = reinterpret_cast<const float*>(extra);
+    const float* g = l2 + 256;
+    const int64_t rb = m0 + wm * kWaveRows;
+    const int vlim = clamp_rows(width - rb, kWaveRows);
+    const int llim = clamp_rows(ld - rb, kWaveRows);
+    if (vlim == kWaveRows)
+      values<true>(acc, lds, lane, wm, wn, l2, g, vlim, llim, m0, n0);
+    else
+      values<false>(acc, lds, lane, wm, wn, l2, g, vlim, llim, m0, n0);
+    if constexpr (sizeof(T) == 2) {
+      // each panel's 256 token rows are 32 KiB of contiguous memory: 16-byte
+      // stores, eight lanes per 128-byte row
+      __syncthreads();
+      for (int k = threadIdx.x; k < 4 * 256 * 8; k += kThreads) {
+        const int pn = k >> 11, tl = (k >> 3) & 255, ch = k & 7;
+        const int64_t t = n0 + tl, c = m0 + pn * 64;
+        if (t >= Tn || c >= ld) continue;
+        const u32x4 val = *reinterpret_cast<const u32x4*>(
+            lds + pn * 32768 + tl * 128 + ((ch ^ (tl & 7)) << 4));
+        *reinterpret_cast<u32x4*>(P + (c / kPanel) * pld * kPanel + t * kPanel + ch * 8) = val;
       }
     }
   }
@@ -443,7 +488,7 @@ __global__ __launch_bounds__(1024) void k_scan(const int* __restrict__ counts, i
   __shared__ int part[1024];
   const int tid = threadIdx.x;
   const int64_t seg = (V + 1023) / 1024;
-  const int64_t b = min<int64_t>(V, tid * seg), e = min<int64_t>(V, b + seg);
+  const int64_t b = imin(V, tid * seg), e = imin(V, b + seg);
   int s = 0;
   for (int64_t i = b; i < e; ++i) s += counts[i];
   part[tid] = s;
