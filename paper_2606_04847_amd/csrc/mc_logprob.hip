@@ -20,31 +20,40 @@ __device__ __forceinline__ int clamp_rows(int64_t n, int hi) {
 }
 constexpr float kNegInf = -__builtin_huge_valf();
 
-// Combine x over lanes l and l ^ 32 (the two halves of a 32 x 32 accumulator
-// block hold alternate groups of 4 rows of the same column).  With both
-// operands equal, v_permlane32_swap leaves (x[l % 32], x[l % 32 + 32]) in
-// every lane.
-__device__ __forceinline__ float pair_max(float x) {
+// Combine x over the four lanes l % 16 + 16 g (g = 0..3): the four 16-lane
+// groups of a 16 x 16 accumulator block hold rows 4 g .. 4 g + 3 of the same
+// column.  With both operands equal, v_permlane32_swap leaves
+// (x[l % 32], x[l % 32 + 32]) in every lane, and v_permlane16_swap the pair
+// (x[l], x[l ^ 16]) ordered by row parity.
+__device__ __forceinline__ float quad_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
                                                   __builtin_bit_cast(uint32_t, x), false, false);
-  return fmaxf(__builtin_bit_cast(float, uint32_t(r[0])), __builtin_bit_cast(float, uint32_t(r[1])));
+  const float y = fmaxf(__builtin_bit_cast(float, uint32_t(r[0])),
+                        __builtin_bit_cast(float, uint32_t(r[1])));
+  const auto q = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(uint32_t, y),
+                                                  __builtin_bit_cast(uint32_t, y), false, false);
+  return fmaxf(__builtin_bit_cast(float, uint32_t(q[0])), __builtin_bit_cast(float, uint32_t(q[1])));
 }
-__device__ __forceinline__ float pair_sum(float x) {
+__device__ __forceinline__ float quad_sum(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
                                                   __builtin_bit_cast(uint32_t, x), false, false);
-  return __builtin_bit_cast(float, uint32_t(r[0])) + __builtin_bit_cast(float, uint32_t(r[1]));
+  const float y = __builtin_bit_cast(float, uint32_t(r[0])) + __builtin_bit_cast(float, uint32_t(r[1]));
+  const auto q = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(uint32_t, y),
+                                                  __builtin_bit_cast(uint32_t, y), false, false);
+  return __builtin_bit_cast(float, uint32_t(q[0])) + __builtin_bit_cast(float, uint32_t(q[1]));
 }
 
-// Row (within the wave's 64) of accumulator element e of block i in this lane.
+// Row (within the wave's kWaveRows) of accumulator element e of block i in
+// this lane.
 __device__ __forceinline__ int wrow(int i, int e, int lane) {
-  return i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+  return i * 16 + 4 * (lane >> 4) + e;
 }
 
 // ---------------------------------------------------------------------------
 // Forward epilogue.  The tile's rows are vocabulary entries (M) and its
 // columns tokens (N), so each lane holds, for each of its kTN token columns,
-// 32 of the wave's 64 vocabulary rows and its partner lane (l ^ 32) the other
-// 32.  Per token: max, sum of exp and (optionally) sum of exp * z over the
+// 32 of the wave's 128 vocabulary rows and the three lanes l ^ 16, l ^ 32,
+// l ^ 48 the other 96.  Per token: max, sum of exp and (optionally) sum of exp * z over the
 // tile's valid rows -> one (m, s, u) partial per (vocab tile, token); the
 // target logit z[t, y_t] is written by the one lane that holds it.  The
 // weight may be a vocabulary shard: row r of this launch is vocabulary entry
@@ -81,23 +90,23 @@ struct EpiFwd {
 #pragma unroll
     for (int i = 0; i < kTM; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e)
+      for (int e = 0; e < 4; ++e)
         if (kFull || wrow(i, e, lane) < vlim) mx = fmaxf(mx, acc[i][j][e]);
-    mx = pair_max(mx);
+    mx = quad_max(mx);
     const float mb = mx * kLog2e;
     s = 0.0f;
     u = 0.0f;
 #pragma unroll
     for (int i = 0; i < kTM; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e)
+      for (int e = 0; e < 4; ++e)
         if (kFull || wrow(i, e, lane) < vlim) {
           const float x = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
           s += x;
           if (with_u) u = fmaf(x, acc[i][j][e], u);
         }
-    s = pair_sum(s);
-    if (with_u) u = pair_sum(u);
+    s = quad_sum(s);
+    if (with_u) u = quad_sum(u);
   }
 
   __device__ void epilogue(Acc& acc, int tm, int, int64_t m0, int64_t n0, char*,
@@ -111,23 +120,23 @@ struct EpiFwd {
     const bool with_u = part_u != nullptr;
 #pragma unroll
     for (int j = 0; j < kTN; ++j) {
-      const int tl = wn * kWaveCols + j * 32 + (lane & 31);   // token within the tile
+      const int tl = wn * kWaveCols + j * 16 + (lane & 15);   // token within the tile
       float mx, s, u;
       if (vlim >= kWaveRows) column<true>(acc, j, vlim, lane, with_u, mx, s, u);
       else column<false>(acc, j, vlim, lane, with_u, mx, s, u);
-      // target logit: row yw of this wave, held by the lane of half (yw >> 2) & 1
+      // target logit: row yw of this wave, held by the lane of group (yw >> 2) & 3
       const int yw = ys[tl] - int(rbase);
-      if (yw >= 0 && yw < kWaveRows && ((yw >> 2) & 1) == (lane >> 5)) {
-        const int ii = yw >> 5, ee = 4 * ((yw & 31) >> 3) + (yw & 3);
+      if (yw >= 0 && yw < kWaveRows && ((yw >> 2) & 3) == (lane >> 4)) {
+        const int ii = yw >> 4, ee = yw & 3;
         float z = 0.0f;
 #pragma unroll
         for (int i = 0; i < kTM; ++i)
 #pragma unroll
-          for (int e = 0; e < 16; ++e)
+          for (int e = 0; e < 4; ++e)
             if (i == ii && e == ee) z = acc[i][j][e];
         zy[n0 + tl] = z;
       }
-      if (lane < 32) {
+      if (lane < 16) {
         red[(0 * kWavesM + wm) * 256 + tl] = mx;
         red[(1 * kWavesM + wm) * 256 + tl] = s;
         red[(2 * kWavesM + wm) * 256 + tl] = u;
@@ -266,7 +275,7 @@ __global__ __launch_bounds__(256) void k_shard_merge(const float* __restrict__ p
 // chunk columns v, tile columns = tokens t) and write the transient operand
 // P~[t, v] = -dlogp_t exp(z_tv - lse_t) (zero for ignored tokens and for the
 // padding columns [width, ld)) in the panel layout.  A lane holds 4
-// consecutive v of one token per (block, e / 4).  bf16: the tile is staged in
+// consecutive v of one token per accumulator block.  bf16: the tile is staged in
 // the (then idle) LDS operand buffers and written as whole 128-byte panel
 // rows; fp32: 4-element stores straight to memory.
 // ---------------------------------------------------------------------------
@@ -304,27 +313,26 @@ struct EpiProbs {
   }
 
   // P~ of this lane's elements.  vlim: valid rows (v < width) of the wave,
-  // llim: rows below ld (a multiple of 4); kFull: all 64 rows valid.
+  // llim: rows below ld (a multiple of 4); kFull: all kWaveRows rows valid.
   template <bool kFull>
   __device__ __forceinline__ void values(const Acc& acc, char* lds, int lane, int wm, int wn,
                                          const float* l2, const float* g, int vlim, int llim,
                                          int64_t m0, int64_t n0) const {
 #pragma unroll
     for (int j = 0; j < kTN; ++j) {
-      const int tl = wn * kWaveCols + j * 32 + (lane & 31);
+      const int tl = wn * kWaveCols + j * 16 + (lane & 15);
       const int64_t t = n0 + tl;
       if (t >= Tn) continue;
       const float lb = l2[tl], gs = g[tl];
 #pragma unroll
       for (int i = 0; i < kTM; ++i) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int r = wrow(i, 4 * q, lane);   // first of 4 consecutive rows of the wave
+        {
+          const int r = wrow(i, 0, lane);   // first of the 4 consecutive rows of block i
           if (!kFull && r >= llim) continue;
           f32x4 p;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            p[e] = gs * __builtin_amdgcn_exp2f(fmaf(acc[i][j][4 * q + e], kLog2e, -lb));
+            p[e] = gs * __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -lb));
             if (!kFull && r + e >= vlim) p[e] = 0.0f;
           }
           const int vr = wm * kWaveRows + r;   // row of the tile
@@ -385,7 +393,7 @@ struct EpiStore {
 #pragma unroll
     for (int i = 0; i < kTM; ++i) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
+      for (int e = 0; e < 4; ++e) {
         const int64_t r = m0 + acc_row(wm, i, e, lane);
         if (r >= rows) continue;
         float* crow = C + r * ldc;

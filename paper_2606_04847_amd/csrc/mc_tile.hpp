@@ -1,6 +1,8 @@
 // MFMA tile core for gfx950 (CDNA4): a 256 x 256 output tile per workgroup of
 // kWavesM x kWavesN wave64s (two waves per SIMD), each owning a
-// kWaveRows x kWaveCols sub-tile held as 32 x 32 fp32 accumulator blocks.
+// kWaveRows x kWaveCols sub-tile held as 16 x 16 fp32 accumulator blocks
+// (v_mfma_f32_16x16x32_bf16: at equal issue rate it sustains a markedly
+// higher throughput than the 32 x 32 form on realistic data on this part).
 // With two waves per SIMD, one wave's MFMAs run while the other waits on
 // memory or a barrier.
 //
@@ -31,24 +33,25 @@ constexpr int kBM = 256;                       // tile rows (M)
 constexpr int kBN = 256;                       // tile columns (N)
 constexpr int kRowBytes = 128;                 // K bytes per tile row per stage
 #ifndef MC_WAVES_M
-#define MC_WAVES_M 4
+#define MC_WAVES_M 2
 #endif
 #ifndef MC_WAVES_N
-#define MC_WAVES_N 2
+#define MC_WAVES_N 4
 #endif
 constexpr int kWavesM = MC_WAVES_M;            // waves along M
 constexpr int kWavesN = MC_WAVES_N;            // waves along N
 constexpr int kThreads = 64 * kWavesM * kWavesN;
-constexpr int kWaveRows = kBM / kWavesM;       // 64
-constexpr int kWaveCols = kBN / kWavesN;       // 128
-constexpr int kTM = kWaveRows / 32;            // 32-row accumulator blocks per wave
-constexpr int kTN = kWaveCols / 32;            // 32-column accumulator blocks per wave
+constexpr int kWaves = kWavesM * kWavesN;
+constexpr int kWaveRows = kBM / kWavesM;       // 128
+constexpr int kWaveCols = kBN / kWavesN;       // 64
+constexpr int kTM = kWaveRows / 16;            // 16-row accumulator blocks per wave
+constexpr int kTN = kWaveCols / 16;            // 16-column accumulator blocks per wave
 constexpr int kStageBytes = kBM * kRowBytes;   // 32 KiB per operand per stage
 constexpr int kLdsGemm = 4 * kStageBytes;      // 2 operands x 2 stages
 constexpr int kGroupM = 8;                     // tile rows per scheduling group
 constexpr int kXcds = 8;                       // MI355X: 8 XCDs, workgroup i -> XCD i % 8
 
-typedef f32x16 Acc[kTM][kTN];
+typedef f32x4 Acc[kTM][kTN];
 
 template <typename T> struct Elem;
 template <> struct Elem<bf16_t> { static constexpr int kChunk = 8; };
@@ -133,24 +136,25 @@ inline bool operand_in_bounds(const Operand& op, size_t bytes) {
   return last >= 0 && size_t(last) + 16 <= bytes && span + 16 <= int64_t(kBufRange);
 }
 
-__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 2)) & 7; }
 __device__ __forceinline__ int lds_off(int r, int c) {
   return r * kRowBytes + ((c ^ swz(r)) << 4);
 }
 
 // Workgroup id -> (tile row, tile column).  The first 8*floor(n/8) ids are
 // regrouped so that each XCD receives a contiguous run of logical tiles; the
-// logical order walks kGroupM tile rows before moving to the next tile column,
+// logical order walks group_m tile rows before moving to the next tile column,
 // so the 32 workgroups resident on one XCD share a few operand panels in its L2.
-__device__ __forceinline__ void tile_of(int bid, int nTm, int nTn, int& tm, int& tn) {
+__device__ __forceinline__ void tile_of(int bid, int nTm, int nTn, int group_m, int& tm,
+                                        int& tn) {
   const int total = nTm * nTn;
   const int q = total / kXcds;
   int L = bid;
   if (bid < q * kXcds) L = (bid % kXcds) * q + bid / kXcds;
-  const int group = kGroupM * nTn;
+  const int group = group_m * nTn;
   const int g = L / group;
-  const int first = g * kGroupM;
-  const int gm = min(nTm - first, kGroupM);
+  const int first = g * group_m;
+  const int gm = min(nTm - first, group_m);
   const int r = L - g * group;
   tm = first + r % gm;
   tn = r / gm;
@@ -341,12 +345,13 @@ template <> struct Mfma<bf16_t> {
     for (int i = 0; i < kTM; ++i)
 #pragma unroll
       for (int j = 0; j < kTN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             __builtin_bit_cast(bf16x8, a[i]), __builtin_bit_cast(bf16x8, b[j]), acc[i][j], 0, 0, 0);
   }
 };
 
-// fp32: each 16-byte chunk holds 4 K values, consumed by 4 MFMAs of K = 2.
+// fp32: each 16-byte chunk holds 4 K values, consumed by 4 MFMAs of K = 4
+// (element e of lane group g is k = 4 g + e of the step; A and B agree).
 // (The chunks are bit-cast to float vectors as a whole: bit-casting a single
 // element of an integer vector compiles to element 0 with this toolchain.)
 template <> struct Mfma<float> {
@@ -363,33 +368,39 @@ template <> struct Mfma<float> {
       for (int i = 0; i < kTM; ++i)
 #pragma unroll
         for (int j = 0; j < kTN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][e], bf[j][e], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i][e], bf[j][e], acc[i][j], 0, 0, 0);
   }
 };
 
 // LDS format of one operand stage.  K: 256 rows of 128 bytes of K (the
 // register-staged copies and the direct copies of K-contiguous operands).
 // MN (bf16 only): 64 K rows of 256 elements along M/N, 512 bytes each, the
-// 16-byte chunk index XOR-ed with 4 (k & 3); fragments are read with the
+// 16-byte chunk index XOR-ed with mn_swz(k); fragments are read with the
 // transposing LDS read.
 enum class Stg { K, MN };
 
+// The 8 K rows one half-wave of a transposing fragment read touches
+// (k0 + {0..3, 8..11}) get 8 distinct chunk offsets, so its 16 chunks fall
+// in distinct bank groups.
+__device__ __forceinline__ int mn_swz(int k) { return ((k & 3) << 2) | (((k >> 3) & 1) << 1); }
+
 __device__ __forceinline__ int lds_off_mn(int k, int m) {
-  return k * (kBM * 2) + (((m >> 3) ^ ((k & 3) << 2)) << 4) + ((m & 7) << 1);
+  return k * (kBM * 2) + (((m >> 3) ^ mn_swz(k)) << 4) + ((m & 7) << 1);
 }
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4_t;
 
-// One 32 x 16 MFMA operand fragment (lane l: row l % 32, k = 8 (l / 32) + 0..7)
-// from an MN stage.  ds_read_b64_tr_b16 hands lane i of each 16-lane group
-// element i % 4 of the 8-byte pieces loaded by lanes 4 e + i / 4 (e = 0..3) of
-// that group; so lane s loads 4 consecutive rows at one k, and after the
-// exchange each lane holds 4 consecutive k of one row.  Two reads give 8.
-__device__ __forceinline__ u32x4 read_frag_mn(const char* base, int row0, int kk, int lane) {
+// One 16 x 32 MFMA operand fragment (lane l: row l % 16, k = 8 (l / 16) + 0..7
+// of K step ks) from an MN stage.  ds_read_b64_tr_b16 hands lane i of each
+// 16-lane group element i % 4 of the 8-byte pieces loaded by lanes
+// 4 e + i / 4 (e = 0..3) of that group; so lane s loads 4 consecutive rows at
+// one k, and after the exchange each lane holds 4 consecutive k of one row.
+// Two reads give 8.
+__device__ __forceinline__ u32x4 read_frag_mn(const char* base, int row0, int ks, int lane) {
   const int g = lane >> 4, s = lane & 15;
-  const int k = 16 * kk + 8 * (g >> 1) + (s >> 2);
-  const int m = row0 + 16 * (g & 1) + 4 * (s & 3);
+  const int k = 32 * ks + 8 * g + (s >> 2);
+  const int m = row0 + 4 * (s & 3);
   const char* p = base + lds_off_mn(k, m);
   const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)p);
   const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(p + 4 * kBM * 2));
@@ -397,36 +408,35 @@ __device__ __forceinline__ u32x4 read_frag_mn(const char* base, int row0, int kk
   return u32x4{a[0], a[1], b[0], b[1]};
 }
 
+// Fragment of K step ks (32 bf16 or 16 fp32 of the stage's 128 bytes):
+// lane l reads row row0 + l % 16, 16-byte chunk 4 ks + l / 16.
 template <Stg S>
-__device__ __forceinline__ u32x4 read_frag(const char* base, int row0, int kk, int lane) {
+__device__ __forceinline__ u32x4 read_frag(const char* base, int row0, int ks, int lane) {
   if constexpr (S == Stg::K)
     return *reinterpret_cast<const u32x4*>(base +
-                                           lds_off(row0 + (lane & 31), 2 * kk + (lane >> 5)));
+                                           lds_off(row0 + (lane & 15), 4 * ks + (lane >> 4)));
   else
-    return read_frag_mn(base, row0, kk, lane);
+    return read_frag_mn(base, row0, ks, lane);
 }
 
 template <typename T, Stg SA, Stg SB>
 __device__ __forceinline__ void read_frags(u32x4 (&a)[kTM], u32x4 (&b)[kTN], const char* ldsA,
-                                           const char* ldsB, int wm, int wn, int lane, int kk) {
+                                           const char* ldsB, int wm, int wn, int lane, int ks) {
 #pragma unroll
-  for (int i = 0; i < kTM; ++i) a[i] = read_frag<SA>(ldsA, wm * kWaveRows + i * 32, kk, lane);
+  for (int i = 0; i < kTM; ++i) a[i] = read_frag<SA>(ldsA, wm * kWaveRows + i * 16, ks, lane);
 #pragma unroll
-  for (int j = 0; j < kTN; ++j) b[j] = read_frag<SB>(ldsB, wn * kWaveCols + j * 32, kk, lane);
+  for (int j = 0; j < kTN; ++j) b[j] = read_frag<SB>(ldsB, wn * kWaveCols + j * 16, ks, lane);
 }
 
-// The fragments of slice kk+1 are requested before the MFMAs of slice kk.
+// The two K steps of one stage; the fragments of step 1 are requested
+// behind the MFMAs of step 0.
 template <typename T, Stg SA = Stg::K, Stg SB = Stg::K>
 __device__ __forceinline__ void mfma_stage(Acc& acc, const char* ldsA, const char* ldsB, int wm,
                                            int wn, int lane) {
   u32x4 a0[kTM], b0[kTN], a1[kTM], b1[kTN];
   read_frags<T, SA, SB>(a0, b0, ldsA, ldsB, wm, wn, lane, 0);
+  Mfma<T>::step(acc, a0, b0);
   read_frags<T, SA, SB>(a1, b1, ldsA, ldsB, wm, wn, lane, 1);
-  Mfma<T>::step(acc, a0, b0);
-  read_frags<T, SA, SB>(a0, b0, ldsA, ldsB, wm, wn, lane, 2);
-  Mfma<T>::step(acc, a1, b1);
-  read_frags<T, SA, SB>(a1, b1, ldsA, ldsB, wm, wn, lane, 3);
-  Mfma<T>::step(acc, a0, b0);
   Mfma<T>::step(acc, a1, b1);
 }
 
@@ -553,7 +563,7 @@ template <Lay L> struct DmaCopyMN {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int k = 2 * (grp0 + i) + (lane >> 5);
-      const int c = (lane & 31) ^ ((k & 3) << 2);
+      const int c = (lane & 31) ^ mn_swz(k);
       kr[i] = k;
       off[i] = M::rel(op, 8 * c, k);
       if (r0 + 8 * c < op.rows) mok |= 1u << i;
@@ -590,10 +600,14 @@ __device__ __forceinline__ void dma_wait_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Direct-copy K loop: the copy of step k+1 is issued right after the barrier
+// that makes step k visible (and releases the buffer of step k-1), and runs
+// under the MFMAs of step k.
 template <typename T, Lay LA, Lay LB>
 __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operand& B, int64_t m0,
                                                   int64_t n0, int64_t K, char* lds, Acc& acc) {
   constexpr int KT = kRowBytes / sizeof(T);
+  constexpr Stg SA = DmaOf<T, LA>::stg, SB = DmaOf<T, LB>::stg;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -603,9 +617,7 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
 #pragma unroll
   for (int i = 0; i < kTM; ++i)
 #pragma unroll
-    for (int j = 0; j < kTN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    for (int j = 0; j < kTN; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
   constexpr bool kAsm = !(KContig<LA>::value && KContig<LB>::value);
   typename DmaSel<T, LA, kAsm>::type ca;
@@ -617,14 +629,12 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
   for (int64_t kt = 0; kt < nk; ++kt) {
     char* cur = lds + (kt & 1) * (2 * kStageBytes);
     char* nxt = lds + ((kt + 1) & 1) * (2 * kStageBytes);
-    // stage kt is in LDS for every wave, and every wave is done with kt-1
     dma_wait_barrier();
     if (kt + 1 < nk) {
       ca.issue(kt + 1, nxt);
       cb.issue(kt + 1, nxt + kStageBytes);
     }
-    mfma_stage<T, DmaOf<T, LA>::stg, DmaOf<T, LB>::stg>(acc, cur, cur + kStageBytes, wm, wn,
-                                                         lane);
+    mfma_stage<T, SA, SB>(acc, cur, cur + kStageBytes, wm, wn, lane);
   }
   __syncthreads();
 }
@@ -643,9 +653,7 @@ __device__ __forceinline__ void gemm_mainloop_reg(const Operand& A, const Operan
 #pragma unroll
   for (int i = 0; i < kTM; ++i)
 #pragma unroll
-    for (int j = 0; j < kTN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    for (int j = 0; j < kTN; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
   StageCopy<T, LA> ca;
   StageCopy<T, LB> cb;
@@ -693,10 +701,10 @@ __device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B
 __device__ __forceinline__ int wave_m() { return (threadIdx.x >> 6) % kWavesM; }
 __device__ __forceinline__ int wave_n() { return (threadIdx.x >> 6) / kWavesM; }
 __device__ __forceinline__ int acc_row(int wm, int i, int e, int lane) {
-  return wm * kWaveRows + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+  return wm * kWaveRows + i * 16 + 4 * (lane >> 4) + e;
 }
 __device__ __forceinline__ int acc_col(int wn, int j, int lane) {
-  return wn * kWaveCols + j * 32 + (lane & 31);
+  return wn * kWaveCols + j * 16 + (lane & 15);
 }
 
 // Body of every tiled contraction kernel: Epi provides prologue(m0, n0,
@@ -705,9 +713,10 @@ __device__ __forceinline__ int acc_col(int wn, int j, int lane) {
 // a __global__ function of its own name (so profiles name the role).
 template <typename T, Lay LA, Lay LB, class Epi>
 __device__ __forceinline__ void gemm_body(const Operand& A, const Operand& B, int64_t K, int nTm,
-                                          int nTn, const Epi& epi, char* lds) {
+                                          int nTn, const Epi& epi, char* lds,
+                                          int group_m = kGroupM) {
   int tm, tn;
-  tile_of(blockIdx.x, nTm, nTn, tm, tn);
+  tile_of(blockIdx.x, nTm, nTn, group_m, tm, tn);
   const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
   char* extra = lds + kLdsGemm;
   epi.prologue(m0, n0, extra);
