@@ -410,11 +410,22 @@ __device__ __forceinline__ u32x4 read_frag_mn(const char* base, int row0, int ks
 
 // Fragment of K step ks (32 bf16 or 16 fp32 of the stage's 128 bytes):
 // lane l reads row row0 + l % 16, 16-byte chunk 4 ks + l / 16.
+// For a K stage the lane's part of the address depends only on ks and on
+// the parity of the 16-row block (rows 32 apart share the swizzle), so the
+// blocks of a wave differ by compile-time offsets.
+__device__ __forceinline__ int kfrag_lane_off(int ks, int par, int lane) {
+  const int x = lane & 15, c = 4 * ks + (lane >> 4);
+  const int sw = ((x & 7) ^ ((4 * par + (x >> 2)) & 7)) & 7;   // swz(32 q + 16 par + x)
+  return x * kRowBytes + ((c ^ sw) << 4);
+}
+
+// row0 (a multiple of 16): first row of the block; wave bases are multiples
+// of 32.
 template <Stg S>
 __device__ __forceinline__ u32x4 read_frag(const char* base, int row0, int ks, int lane) {
   if constexpr (S == Stg::K)
-    return *reinterpret_cast<const u32x4*>(base +
-                                           lds_off(row0 + (lane & 15), 4 * ks + (lane >> 4)));
+    return *reinterpret_cast<const u32x4*>(base + row0 * kRowBytes +
+                                           kfrag_lane_off(ks, (row0 >> 4) & 1, lane));
   else
     return read_frag_mn(base, row0, ks, lane);
 }
@@ -493,48 +504,54 @@ __device__ __forceinline__ const char* uniform_ptr(const char* p) {
 // kAsm: issue through dma16 (loops that also use the transposing LDS read,
 // which the compiler would otherwise order behind every copy in flight);
 // otherwise through the compiler builtin.
+// Wave w copies the 1 KiB groups w + kWaves i (i = 0..NI-1).  Groups kWaves
+// apart are 8 kWaves = 64 rows apart, where both swizzles repeat, so every
+// group of a wave has the same lane -> chunk pattern: one offset register,
+// a constant stride per group, one K bound.
 template <typename T, Lay L, bool kAsm> struct DmaCopy {
   using M = LayMath<T, L>;
   static constexpr int E = Elem<T>::kChunk;
-  static constexpr int NI = kBM / 8 / (kThreads / 64);   // 1 KiB groups per wave
+  static constexpr int NI = kBM / 8 / kWaves;   // 1 KiB groups per wave
+  static_assert(8 * kWaves % 32 == 0, "group stride must keep the row swizzle");
   const char* tb;
   int64_t step, K;
-  uint32_t off[NI];
-  int kc[NI];
+  uint32_t off0, istride;
+  int kc;
   uint32_t rowok;
-  int grp0;
+  int grp;
   __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
     tb = static_cast<const char*>(op.ptr) + M::tile_base(op, r0);
     step = M::stage_step(op);
     K = op.K;
     const int lane = tid & 63;
-    grp0 = __builtin_amdgcn_readfirstlane(tid >> 6) * NI;
+    grp = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int row = 8 * grp + (lane >> 3);
+    kc = ((lane & 7) ^ swz(row)) * E;
+    off0 = M::rel(op, row, kc);
+    istride = M::rel(op, row + 8 * kWaves, kc) - off0;
     rowok = 0;
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int row = 8 * (grp0 + i) + (lane >> 3);
-      kc[i] = ((lane & 7) ^ swz(row)) * E;
-      off[i] = M::rel(op, row, kc[i]);
-      if (r0 + row < op.rows) rowok |= 1u << i;
-    }
+    for (int i = 0; i < NI; ++i)
+      if (r0 + row + 8 * kWaves * i < op.rows) rowok |= 1u << i;
   }
   __device__ __forceinline__ void issue(int64_t kt, char* lds) const {
+    const bool kok = kt * M::KT + kc < K;
     if constexpr (kAsm) {
       const i32x4 rs = dma_rsrc(tb + kt * step);
-      const uint32_t m0 = lds_addr(lds) + grp0 * 1024;
+      const uint32_t m0 = lds_addr(lds) + grp * 1024;
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
-        const bool ok = ((rowok >> i) & 1u) && (kt * M::KT + kc[i] < K);
-        dma16(rs, ok ? off[i] : kBufOut, m0 + i * 1024);
+        const bool ok = kok && ((rowok >> i) & 1u);
+        dma16(rs, ok ? off0 + i * istride : kBufOut, m0 + i * kWaves * 1024);
       }
     } else {
       const __amdgpu_buffer_rsrc_t rs = stage_rsrc(uniform_ptr(tb + kt * step));
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
-        const bool ok = ((rowok >> i) & 1u) && (kt * M::KT + kc[i] < K);
+        const bool ok = kok && ((rowok >> i) & 1u);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            rs, (__attribute__((address_space(3))) void*)(lds + (grp0 + i) * 1024), 16,
-            ok ? off[i] : kBufOut, 0, 0, 0);
+            rs, (__attribute__((address_space(3))) void*)(lds + (grp + i * kWaves) * 1024), 16,
+            ok ? off0 + i * istride : kBufOut, 0, 0, 0);
       }
     }
   }
@@ -543,39 +560,37 @@ template <typename T, Lay L, bool kAsm> struct DmaCopy {
 // Direct copy of one M/N-contiguous bf16 operand stage into the MN format:
 // one wave instruction fills 1 KiB (two K rows of 256 elements); lane i
 // writes slot i % 32 of K row 2 g + i / 32 and loads the 8-element chunk
-// that the swizzle assigns to that slot.
+// that the swizzle assigns to that slot.  Wave w takes the groups
+// w + kWaves i: K rows 16 i apart, where mn_swz repeats.
 template <Lay L> struct DmaCopyMN {
   using M = LayMath<bf16_t, L>;
-  static constexpr int NI = kStageBytes / 1024 / (kThreads / 64);   // 1 KiB groups per wave
+  static constexpr int NI = kStageBytes / 1024 / kWaves;   // 1 KiB groups per wave
+  static_assert(2 * kWaves % 16 == 0, "group stride must keep the K-row swizzle");
   const char* tb;
   int64_t step, K;
-  uint32_t off[NI];
-  int kr[NI];
-  uint32_t mok;
-  int grp0;
+  uint32_t off0, istride;
+  int k0;
+  bool mok;
+  int grp;
   __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
     tb = static_cast<const char*>(op.ptr) + M::tile_base(op, r0);
     step = M::stage_step(op);
     K = op.K;
     const int lane = tid & 63;
-    grp0 = __builtin_amdgcn_readfirstlane(tid >> 6) * NI;
-    mok = 0;
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int k = 2 * (grp0 + i) + (lane >> 5);
-      const int c = (lane & 31) ^ mn_swz(k);
-      kr[i] = k;
-      off[i] = M::rel(op, 8 * c, k);
-      if (r0 + 8 * c < op.rows) mok |= 1u << i;
-    }
+    grp = __builtin_amdgcn_readfirstlane(tid >> 6);
+    k0 = 2 * grp + (lane >> 5);
+    const int c = (lane & 31) ^ mn_swz(k0);
+    off0 = M::rel(op, 8 * c, k0);
+    istride = M::rel(op, 8 * c, k0 + 2 * kWaves) - off0;
+    mok = r0 + 8 * c < op.rows;
   }
   __device__ __forceinline__ void issue(int64_t kt, char* lds) const {
     const i32x4 rs = dma_rsrc(tb + kt * step);
-    const uint32_t m0 = lds_addr(lds) + grp0 * 1024;
+    const uint32_t m0 = lds_addr(lds) + grp * 1024;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const bool ok = ((mok >> i) & 1u) && (kt * M::KT + kr[i] < K);
-      dma16(rs, ok ? off[i] : kBufOut, m0 + i * 1024);
+      const bool ok = mok && (kt * M::KT + k0 + 2 * kWaves * i < K);
+      dma16(rs, ok ? off0 + i * istride : kBufOut, m0 + i * kWaves * 1024);
     }
   }
 };
@@ -600,9 +615,14 @@ __device__ __forceinline__ void dma_wait_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Direct-copy K loop: the copy of step k+1 is issued right after the barrier
-// that makes step k visible (and releases the buffer of step k-1), and runs
-// under the MFMAs of step k.
+// Direct-copy K loop.  Two LDS stages, copies two steps ahead, one barrier
+// per step placed between the two K sub-steps of a stage:
+//   read sub-step 1 of stage k | MFMAs of sub-step 0 of stage k |
+//   wait (this wave's copies of stage k+1 landed, its reads of stage k done),
+//   barrier | copy stage k+2 into stage k's buffer | read sub-step 0 of
+//   stage k+1 | MFMAs of sub-step 1 of stage k
+// so the MFMAs after the barrier already have their fragments in registers
+// while the next stage's first reads are in flight.
 template <typename T, Lay LA, Lay LB>
 __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operand& B, int64_t m0,
                                                   int64_t n0, int64_t K, char* lds, Acc& acc) {
@@ -618,23 +638,67 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
   for (int i = 0; i < kTM; ++i)
 #pragma unroll
     for (int j = 0; j < kTN; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  if (nk <= 0) return;
 
   constexpr bool kAsm = !(KContig<LA>::value && KContig<LB>::value);
-  typename DmaSel<T, LA, kAsm>::type ca;
-  typename DmaSel<T, LB, kAsm>::type cb;
+  using CA = typename DmaSel<T, LA, kAsm>::type;
+  using CB = typename DmaSel<T, LB, kAsm>::type;
+  CA ca;
+  CB cb;
   ca.init(A, m0, tid);
   cb.init(B, n0, tid);
   ca.issue(0, lds);
   cb.issue(0, lds + kStageBytes);
+  if constexpr (kAsm) {
+    // A transposing-read operand needs per-block fragment addresses; without
+    // the spare registers for the cross-barrier prefetch, one barrier at the
+    // top of each step: it publishes step k and releases step k-1's buffer.
+    for (int64_t kt = 0; kt < nk; ++kt) {
+      char* cur = lds + (kt & 1) * (2 * kStageBytes);
+      char* nxt = lds + ((kt + 1) & 1) * (2 * kStageBytes);
+      dma_wait_barrier();
+      if (kt + 1 < nk) {
+        ca.issue(kt + 1, nxt);
+        cb.issue(kt + 1, nxt + kStageBytes);
+      }
+      mfma_stage<T, SA, SB>(acc, cur, cur + kStageBytes, wm, wn, lane);
+    }
+    __syncthreads();
+    return;
+  }
+  if (nk > 1) {
+    ca.issue(1, lds + 2 * kStageBytes);
+    cb.issue(1, lds + 3 * kStageBytes);
+    // stage 0 landed; the CA::NI + CB::NI copies of stage 1 may be in flight
+    static_assert(CA::NI + CB::NI <= 15, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt(0x3f70 | (CA::NI + CB::NI));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  } else {
+    dma_wait_barrier();
+  }
+  u32x4 a0[kTM], b0[kTN], a1[kTM], b1[kTN];
+  read_frags<T, SA, SB>(a0, b0, lds, lds + kStageBytes, wm, wn, lane, 0);
   for (int64_t kt = 0; kt < nk; ++kt) {
     char* cur = lds + (kt & 1) * (2 * kStageBytes);
     char* nxt = lds + ((kt + 1) & 1) * (2 * kStageBytes);
-    dma_wait_barrier();
-    if (kt + 1 < nk) {
-      ca.issue(kt + 1, nxt);
-      cb.issue(kt + 1, nxt + kStageBytes);
+    read_frags<T, SA, SB>(a1, b1, cur, cur + kStageBytes, wm, wn, lane, 1);
+    Mfma<T>::step(acc, a0, b0);
+    // this wave: copies of stage kt+1 landed, reads of stage kt returned;
+    // nothing is scheduled across the barrier
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + 2 < nk) {
+      ca.issue(kt + 2, cur);
+      cb.issue(kt + 2, cur + kStageBytes);
     }
-    mfma_stage<T, SA, SB>(acc, cur, cur + kStageBytes, wm, wn, lane);
+    if (kt + 1 < nk) read_frags<T, SA, SB>(a0, b0, nxt, nxt + kStageBytes, wm, wn, lane, 0);
+    Mfma<T>::step(acc, a1, b1);
   }
   __syncthreads();
 }
