@@ -1,10 +1,13 @@
 #!/usr/bin/env python3
 """Throughput of the fused RL log-prob step on one MI355X.
 
-One step = mc_logprob_fwd (LM-head GEMM + online log-sum-exp + target
-gather) -> mc_rl_loss (ratios, MirrorPop filter, group advantages, clipped
-surrogate, dlogp) -> mc_logprob_bwd (dHidden and dW), on one stream, over
-one packed batch of synthetic inputs already resident in HBM.
+One step = mc_logprob_fwd_cached (LM-head GEMM + online log-sum-exp +
+target gather, keeping the softmax cache) -> mc_rl_loss (ratios, MirrorPop
+filter, group advantages, clipped surrogate, dlogp) ->
+mc_logprob_bwd_cached (dHidden and dW from the cache), on one stream, over
+one packed batch of synthetic inputs already resident in HBM.  With
+--recompute the step uses mc_logprob_fwd / mc_logprob_bwd instead (the
+backward recomputes the logits).
 
 Default workload: T = 16384 packed tokens (256 sequences in 32 groups of 8,
 lengths 8-2048, 70% of tokens masked, 10% of sequences drifted), d = 4096,
@@ -117,6 +120,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--recompute", action="store_true",
+                    help="time the recompute path (mc_logprob_fwd / mc_logprob_bwd) instead "
+                         "of the softmax-cache path")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy three times (calibrates the "
                          "FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
@@ -144,10 +150,17 @@ def main():
     cfg, s, H, W, y, lr, st = build_inputs(args.config, dev)
     T, d, V = s.T, cfg["d"], cfg["V"]
 
-    ws_f = torch.empty(mc.load_library().mc_logprob_fwd_workspace_size(T, d, V, 1),
-                       dtype=torch.uint8, device=dev)
-    ws_b = torch.empty(mc.load_library().mc_logprob_bwd_workspace_size(T, d, V, 1),
-                       dtype=torch.uint8, device=dev)
+    lib = mc.load_library()
+    ws_f = torch.empty(lib.mc_logprob_fwd_workspace_size(T, d, V, 1), dtype=torch.uint8,
+                       device=dev)
+    if args.recompute:
+        ws_b = torch.empty(lib.mc_logprob_bwd_workspace_size(T, d, V, 1), dtype=torch.uint8,
+                           device=dev)
+        cache = None
+    else:
+        ws_b = torch.empty(lib.mc_logprob_bwd_cached_workspace_size(T, d, V, 1),
+                           dtype=torch.uint8, device=dev)
+        cache = mc.softmax_cache(H, W)
     logp = torch.empty(T, dtype=torch.float32, device=dev)
     lse = torch.empty(T, dtype=torch.float32, device=dev)
     dH = torch.empty(T, d, dtype=torch.float32, device=dev)
@@ -155,9 +168,16 @@ def main():
     params = mc.RLParams()
 
     def step():
-        mc.logprob_fwd(H, W, y, logp=logp, lse=lse, workspace=ws_f)
+        if cache is None:
+            mc.logprob_fwd(H, W, y, logp=logp, lse=lse, workspace=ws_f)
+        else:
+            mc.logprob_fwd_cached(H, W, y, cache, logp=logp, lse=lse, workspace=ws_f)
         out = mc.rl_loss(logp, lr, st["mask"], st["cu"], st["cg"], st["rewards"], params)
-        mc.logprob_bwd(H, W, y, lse, out["dlogp"], dhidden=dH, dweight=dW, workspace=ws_b)
+        if cache is None:
+            mc.logprob_bwd(H, W, y, lse, out["dlogp"], dhidden=dH, dweight=dW, workspace=ws_b)
+        else:
+            mc.logprob_bwd_cached(H, W, y, lse, out["dlogp"], cache, dhidden=dH, dweight=dW,
+                                  workspace=ws_b)
         return out
 
     for _ in range(args.warmup):
@@ -219,7 +239,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": workload_name(cfg, s), "T": T, "d": d, "V": V,
-                   "sequences": s.B, "groups": s.NG, "parallelism": "none (1 GPU)"},
+                   "sequences": s.B, "groups": s.NG, "parallelism": "none (1 GPU)",
+                   "backward": "recompute logits" if args.recompute else "softmax cache"},
         "mfma_frac": tflops / PEAK_BF16_TFLOPS,
         "counted_tflops": tflops,
         "roofline": roofline,

@@ -180,6 +180,41 @@ mc_status_t mc_logprob_bwd_shard(const void* hidden, const void* weight_shard,
                                  size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Forward and backward with a softmax cache: the same quantities as
+ * mc_logprob_fwd / mc_logprob_bwd (the numerator of Eq. 4 and its
+ * gradient), with the backward reading what the forward kept instead of
+ * recomputing the logits.  The forward stores, in `cache`,
+ *   E[t, v] = exp(z[t, v] - c_b[t])   (dtype, vocabulary panels)
+ *   c_b[t]  = max of z[t, .] over block b of 128 vocabulary entries (fp32)
+ * and the backward turns E, in place, into the softmax part of G and runs
+ * the two contractions on it.  E adds one rounding to the dtype before the
+ * final one of the softmax operand (bf16: each element of that operand is
+ * within 2^-8 relative of its exact value instead of 2^-9).
+ *   cache     device, 256-byte aligned, at least mc_logprob_cache_size bytes;
+ *             owned by the caller; written by mc_logprob_fwd_cached and
+ *             consumed (overwritten) by one mc_logprob_bwd_cached call with
+ *             the same hidden, weight, targets and shapes.  Its contents
+ *             between the two calls must not be touched.
+ *   The forward takes the workspace of mc_logprob_fwd
+ *   (mc_logprob_fwd_workspace_size); the backward takes
+ *   mc_logprob_bwd_cached_workspace_size bytes.  Errors as for the plain
+ *   entry points; a missing or short cache returns MC_ERR_WORKSPACE.
+ * ------------------------------------------------------------------------ */
+size_t mc_logprob_cache_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dtype);
+mc_status_t mc_logprob_fwd_cached(const void* hidden, const void* weight,
+                                  const int64_t* targets, int64_t T, int64_t d, int64_t V,
+                                  mc_dtype_t dtype, float* logp, float* lse, float* entropy,
+                                  void* cache, size_t cache_bytes, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+size_t mc_logprob_bwd_cached_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dtype);
+mc_status_t mc_logprob_bwd_cached(const void* hidden, const void* weight,
+                                  const int64_t* targets, const float* lse, const float* dlogp,
+                                  int64_t T, int64_t d, int64_t V, mc_dtype_t dtype,
+                                  void* cache, size_t cache_bytes, float* dhidden,
+                                  float* dweight, int32_t flags, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * RL objective over a packed ragged batch (Eq. 3/12, 4, 17-21).
  *   logp          [T]    fp32   trainer log-probs (from mc_logprob_fwd)
  *   logp_rollout  [T]    fp32   rollout log-probs of the same tokens

@@ -10,6 +10,9 @@ from .binding import (  # noqa: F401
     check_packing,
     load_library,
     logprob_bwd,
+    logprob_bwd_cached,
+    logprob_fwd_cached,
+    softmax_cache,
     logprob_bwd_shard,
     logprob_fwd,
     logprob_fwd_shard,

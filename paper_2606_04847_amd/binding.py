@@ -81,7 +81,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mc_status_string.argtypes = [ctypes.c_int]
     lib.mc_version.restype = ctypes.c_char_p
     lib.mc_version.argtypes = []
-    for name in ("mc_logprob_fwd_workspace_size", "mc_logprob_bwd_workspace_size"):
+    for name in ("mc_logprob_fwd_workspace_size", "mc_logprob_bwd_workspace_size",
+                 "mc_logprob_cache_size", "mc_logprob_bwd_cached_workspace_size"):
         f = getattr(lib, name)
         f.restype = _c_sz
         f.argtypes = [_c_i64, _c_i64, _c_i64, ctypes.c_int]
@@ -98,6 +99,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mc_logprob_bwd.restype = ctypes.c_int
     lib.mc_logprob_bwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _c_i64,
                                    ctypes.c_int, _vp, _vp, _c_i32, _vp, _c_sz, _vp]
+    lib.mc_logprob_fwd_cached.restype = ctypes.c_int
+    lib.mc_logprob_fwd_cached.argtypes = [_vp, _vp, _vp, _c_i64, _c_i64, _c_i64, ctypes.c_int,
+                                          _vp, _vp, _vp, _vp, _c_sz, _vp, _c_sz, _vp]
+    lib.mc_logprob_bwd_cached.restype = ctypes.c_int
+    lib.mc_logprob_bwd_cached.argtypes = [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _c_i64,
+                                          ctypes.c_int, _vp, _c_sz, _vp, _vp, _c_i32, _vp,
+                                          _c_sz, _vp]
     lib.mc_logprob_bwd_shard.restype = ctypes.c_int
     lib.mc_logprob_bwd_shard.argtypes = [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_i64, _c_i64,
                                          _c_i64, _c_i64, ctypes.c_int, _vp, _vp, _c_i32, _vp,
@@ -324,6 +332,83 @@ def logprob_bwd(hidden, weight, targets, lse, dlogp, *, dhidden=None, dweight=No
     _check(lib.mc_logprob_bwd(_ptr(hidden), _ptr(weight), _ptr(targets), _ptr(lse), _ptr(dlogp),
                               T, d, V, dt, _ptr(dhidden), _ptr(dweight), flags, _ptr(ws),
                               nbytes, _stream(stream)), "mc_logprob_bwd")
+    return dhidden, dweight
+
+
+def softmax_cache(hidden, weight):
+    """An uninitialised softmax cache for hidden [T,d] and weight [V,d] (see
+    mc_logprob_fwd_cached): a uint8 device tensor of mc_logprob_cache_size bytes."""
+    torch = _torch()
+    lib = load_library()
+    T, d = hidden.shape
+    V = weight.shape[0]
+    n = lib.mc_logprob_cache_size(T, d, V, _dtype_code(hidden))
+    return torch.empty(max(int(n), 1), dtype=torch.uint8, device=hidden.device)
+
+
+def logprob_fwd_cached(hidden, weight, targets, cache, *, logp=None, lse=None, entropy=None,
+                       with_entropy=False, workspace=None, stream=None):
+    """mc_logprob_fwd_cached: logprob_fwd that also fills `cache` (from
+    softmax_cache) for one later logprob_bwd_cached call."""
+    torch = _torch()
+    lib = load_library()
+    _need(hidden.is_cuda and weight.is_cuda and targets.is_cuda, "tensors must be on the GPU")
+    _need(hidden.dtype == weight.dtype, "hidden and weight dtypes differ")
+    _need(targets.dtype == torch.int64, "targets must be int64")
+    _need(hidden.is_contiguous() and weight.is_contiguous() and targets.is_contiguous(),
+          "tensors must be contiguous")
+    T, d = hidden.shape
+    V = weight.shape[0]
+    _need(weight.shape[1] == d and targets.shape == (T,), "shape mismatch")
+    dt = _dtype_code(hidden)
+    dev = hidden.device
+    logp = torch.empty(T, dtype=torch.float32, device=dev) if logp is None else logp
+    lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
+    if with_entropy and entropy is None:
+        entropy = torch.empty(T, dtype=torch.float32, device=dev)
+    need = lib.mc_logprob_fwd_workspace_size(T, d, V, dt)
+    ws, nbytes = _workspace(need, dev, workspace)
+    _check(lib.mc_logprob_fwd_cached(_ptr(hidden), _ptr(weight), _ptr(targets), T, d, V, dt,
+                                     _ptr(logp), _ptr(lse), _ptr(entropy), _ptr(cache),
+                                     cache.numel(), _ptr(ws), nbytes, _stream(stream)),
+           "mc_logprob_fwd_cached")
+    return (logp, lse, entropy) if entropy is not None else (logp, lse)
+
+
+def logprob_bwd_cached(hidden, weight, targets, lse, dlogp, cache, *, dhidden=None,
+                       dweight=None, need_dhidden=True, need_dweight=True,
+                       accumulate_dhidden=False, accumulate_dweight=False, workspace=None,
+                       stream=None):
+    """mc_logprob_bwd_cached: logprob_bwd from the cache the forward filled
+    (the cache is consumed)."""
+    torch = _torch()
+    lib = load_library()
+    T, d = hidden.shape
+    V = weight.shape[0]
+    _need(hidden.dtype == weight.dtype, "hidden and weight dtypes differ")
+    _need(targets.dtype == torch.int64 and lse.dtype == torch.float32
+          and dlogp.dtype == torch.float32, "targets int64, lse/dlogp fp32")
+    for t in (hidden, weight, targets, lse, dlogp, cache):
+        _need(t.is_cuda and t.is_contiguous(), "tensors must be contiguous on the GPU")
+    _need(lse.shape == (T,) and dlogp.shape == (T,) and targets.shape == (T,), "shape mismatch")
+    dt = _dtype_code(hidden)
+    dev = hidden.device
+    if need_dhidden and dhidden is None:
+        dhidden = torch.empty(T, d, dtype=torch.float32, device=dev)
+    if need_dweight and dweight is None:
+        dweight = torch.empty(V, d, dtype=torch.float32, device=dev)
+    if not need_dhidden:
+        dhidden = None
+    if not need_dweight:
+        dweight = None
+    flags = ((MC_BWD_ACCUMULATE_DHIDDEN if accumulate_dhidden else 0)
+             | (MC_BWD_ACCUMULATE_DWEIGHT if accumulate_dweight else 0))
+    need = lib.mc_logprob_bwd_cached_workspace_size(T, d, V, dt)
+    ws, nbytes = _workspace(need, dev, workspace)
+    _check(lib.mc_logprob_bwd_cached(_ptr(hidden), _ptr(weight), _ptr(targets), _ptr(lse),
+                                     _ptr(dlogp), T, d, V, dt, _ptr(cache), cache.numel(),
+                                     _ptr(dhidden), _ptr(dweight), flags, _ptr(ws), nbytes,
+                                     _stream(stream)), "mc_logprob_bwd_cached")
     return dhidden, dweight
 
 

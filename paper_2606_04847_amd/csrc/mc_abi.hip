@@ -109,6 +109,65 @@ size_t mc_logprob_bwd_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t
   return mc::bwd_workspace(T, d, V, dt);
 }
 
+size_t mc_logprob_cache_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
+  if (check_dims(T, d, V, dt) != MC_OK) return 0;
+  return mc::cache_bytes(T, d, V, dt);
+}
+
+mc_status_t mc_logprob_fwd_cached(const void* hidden, const void* weight, const int64_t* targets,
+                                  int64_t T, int64_t d, int64_t V, mc_dtype_t dt, float* logp,
+                                  float* lse, float* entropy, void* cache, size_t cache_bytes,
+                                  void* ws, size_t ws_bytes, void* stream) {
+  mc_status_t st = check_dims(T, d, V, dt);
+  if (st != MC_OK) return st;
+  if (T == 0) return MC_OK;
+  if (!hidden || !weight || !targets || !logp || !lse) return MC_ERR_INVALID_ARG;
+  if (!aligned(hidden, 16) || !aligned(weight, 16) || !aligned(targets, 8) ||
+      !aligned(logp, 4) || !aligned(lse, 4) || (entropy && !aligned(entropy, 4)))
+    return MC_ERR_INVALID_ARG;
+  st = check_ws(cache, cache_bytes, mc::cache_bytes(T, d, V, dt));
+  if (st != MC_OK) return st;
+  st = check_ws(ws, ws_bytes, mc::fwd_workspace(T, d, V, dt));
+  if (st != MC_OK) return st;
+  return from_hip(mc::launch_fwd_cache(hidden, weight, targets, T, d, V, dt, logp, lse, entropy,
+                                       cache, ws, static_cast<hipStream_t>(stream)));
+}
+
+size_t mc_logprob_bwd_cached_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
+  if (check_dims(T, d, V, dt) != MC_OK) return 0;
+  return mc::bwd_cache_workspace(T, d, V, dt);
+}
+
+mc_status_t mc_logprob_bwd_cached(const void* hidden, const void* weight, const int64_t* targets,
+                                  const float* lse, const float* dlogp, int64_t T, int64_t d,
+                                  int64_t V, mc_dtype_t dt, void* cache, size_t cache_bytes,
+                                  float* dhidden, float* dweight, int32_t flags, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  mc_status_t st = check_dims(T, d, V, dt);
+  if (st != MC_OK) return st;
+  if (flags & ~(MC_BWD_ACCUMULATE_DHIDDEN | MC_BWD_ACCUMULATE_DWEIGHT)) return MC_ERR_INVALID_ARG;
+  if (!dhidden && !dweight) return MC_ERR_INVALID_ARG;
+  if (!hidden || !weight) return MC_ERR_INVALID_ARG;
+  if (!aligned(hidden, 16) || !aligned(weight, 16) || (dhidden && !aligned(dhidden, 16)) ||
+      (dweight && !aligned(dweight, 16)))
+    return MC_ERR_INVALID_ARG;
+  if (T == 0) {
+    if (dweight && !(flags & MC_BWD_ACCUMULATE_DWEIGHT))
+      return from_hip(hipMemsetAsync(dweight, 0, size_t(V) * size_t(d) * sizeof(float),
+                                     static_cast<hipStream_t>(stream)));
+    return MC_OK;
+  }
+  if (!targets || !lse || !dlogp) return MC_ERR_INVALID_ARG;
+  if (!aligned(targets, 8) || !aligned(lse, 4) || !aligned(dlogp, 4)) return MC_ERR_INVALID_ARG;
+  st = check_ws(cache, cache_bytes, mc::cache_bytes(T, d, V, dt));
+  if (st != MC_OK) return st;
+  st = check_ws(ws, ws_bytes, mc::bwd_cache_workspace(T, d, V, dt));
+  if (st != MC_OK) return st;
+  return from_hip(mc::launch_bwd_cache(hidden, weight, targets, lse, dlogp, T, d, V, dt, cache,
+                                       dhidden, dweight, flags, ws,
+                                       static_cast<hipStream_t>(stream)));
+}
+
 static mc_status_t bwd_common(const void* hidden, const void* weight, const int64_t* targets,
                               const float* lse, const float* dlogp, int64_t T, int64_t d,
                               int64_t V, int64_t v_offset, int64_t V_total, mc_dtype_t dt,

@@ -51,6 +51,8 @@ class ProfScope {
 
 size_t fwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt);
 size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt);
+size_t cache_bytes(int64_t T, int64_t d, int64_t V, mc_dtype_t dt);
+size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt);
 size_t loss_workspace(int64_t T, int32_t B, int32_t NG);
 
 // Forward over the vocabulary shard [v_off, v_off + Vs) of V entries.  With
@@ -66,6 +68,13 @@ hipError_t launch_bwd(const void* H, const void* W, const int64_t* y, const floa
                       const float* dlogp, int64_t T, int64_t d, int64_t Vs, int64_t v_off,
                       int64_t V, mc_dtype_t dt, float* dH, float* dW, int flags, void* ws,
                       hipStream_t s);
+hipError_t launch_fwd_cache(const void* H, const void* W, const int64_t* y, int64_t T, int64_t d,
+                            int64_t V, mc_dtype_t dt, float* logp, float* lse, float* entropy,
+                            void* cache, void* ws, hipStream_t s);
+hipError_t launch_bwd_cache(const void* H, const void* W, const int64_t* y, const float* lse,
+                            const float* dlogp, int64_t T, int64_t d, int64_t V, mc_dtype_t dt,
+                            void* cache, float* dH, float* dW, int flags, void* ws,
+                            hipStream_t s);
 hipError_t launch_primeecho(const float* scores, const uint8_t* success, const int32_t* n_turns,
                             int32_t B, int32_t Kmax, float alpha, float beta1, float beta2,
                             float* rewards, hipStream_t s);

@@ -50,6 +50,33 @@ __device__ __forceinline__ int wrow(int i, int e, int lane) {
 }
 
 // ---------------------------------------------------------------------------
+// A 256 x 256 bf16 tile (rows: 256 vocabulary entries of a chunk, columns:
+// 256 tokens) staged in the workgroup's LDS operand buffers for stores of
+// whole panel rows: four 32 KiB panels (64 vocabulary entries each) of 256
+// token rows x 128 bytes, the 16-byte chunk index XOR-ed with t & 7.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int panel_stage_off(int v, int t) {
+  return (v >> 6) * 32768 + t * 128 + ((((v & 63) >> 3) ^ (t & 7)) << 4) + ((v & 7) << 1);
+}
+
+// Each panel's 256 token rows are 32 KiB of contiguous memory: 16-byte
+// stores, eight lanes per 128-byte row.  Rows t >= Tn and chunk columns
+// >= ld are skipped.  The caller has synchronised after staging.
+__device__ __forceinline__ void store_staged_panels(const char* lds, bf16_t* P, int64_t m0,
+                                                    int64_t n0, int64_t Tn, int64_t ld,
+                                                    int64_t pld) {
+  constexpr int64_t kPanel = 64;
+  for (int k = threadIdx.x; k < 4 * 256 * 8; k += kThreads) {
+    const int pn = k >> 11, tl = (k >> 3) & 255, ch = k & 7;
+    const int64_t t = n0 + tl, c = m0 + pn * 64;
+    if (t >= Tn || c >= ld) continue;
+    const u32x4 val =
+        *reinterpret_cast<const u32x4*>(lds + pn * 32768 + tl * 128 + ((ch ^ (tl & 7)) << 4));
+    *reinterpret_cast<u32x4*>(P + (c / kPanel) * pld * kPanel + t * kPanel + ch * 8) = val;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Forward epilogue.  The tile's rows are vocabulary entries (M) and its
 // columns tokens (N), so each lane holds, for each of its kTN token columns,
 // 32 of the wave's 128 vocabulary rows and the three lanes l ^ 16, l ^ 32,
@@ -58,22 +85,32 @@ __device__ __forceinline__ int wrow(int i, int e, int lane) {
 // target logit z[t, y_t] is written by the one lane that holds it.  The
 // weight may be a vocabulary shard: row r of this launch is vocabulary entry
 // v_off + r.
+// With a softmax cache (E non-null) the epilogue also keeps what the
+// backward needs instead of recomputing the logits: E[t, v] =
+// exp(z_tv - cm[b][t]) in the kernel dtype, in the panel layout of the
+// backward operand, where cm[b][t] is the max over the wave's block b of 128
+// vocabulary rows (zero for rows >= Vs).
 // ---------------------------------------------------------------------------
+template <typename T>
 struct EpiFwd {
   const int64_t* y;
-  int64_t T, Vs, v_off;   // tokens, shard width, shard offset
-  float* part_m;          // [nTv][T]
-  float* part_s;          // [nTv][T]
-  float* part_u;          // [nTv][T] or null (no entropy)
-  float* zy;              // [T]: receives z[t, y_t] for targets inside the shard
+  int64_t Tn, Vs, v_off;  // tokens, shard width, shard offset
+  float* part_m;          // [nTv][Tn]
+  float* part_s;          // [nTv][Tn]
+  float* part_u;          // [nTv][Tn] or null (no entropy)
+  float* zy;              // [Tn]: receives z[t, y_t] for targets inside the shard
+  T* E;                   // softmax cache: panels [ldE / BV][pld][BV], or null
+  float* cm;              // [2 nTv][Tn] block maxima (with E)
+  int64_t pld, ldE;       // padded token count, padded vocabulary width
   static constexpr int kLdsExtra = 256 * 4 + 3 * kWavesM * 256 * 4;
+  static constexpr int64_t kPanel = 128 / sizeof(T);
 
   __device__ void prologue(int64_t, int64_t n0, char* extra) const {
     int* ys = reinterpret_cast<int*>(extra);
     for (int i = threadIdx.x; i < kBN; i += kThreads) {
       const int64_t t = n0 + i;
       int v = -1;
-      if (t < T) {
+      if (t < Tn) {
         const int64_t yl = y[t] - v_off;
         if (yl >= 0 && yl < Vs) v = int(yl);
       }
@@ -82,10 +119,12 @@ struct EpiFwd {
   }
 
   // max / sum exp / sum exp z of block column j over this lane's rows; kFull:
-  // all 64 rows of the wave are valid (no per-element mask)
-  template <bool kFull>
+  // all rows of the wave are valid (no per-element mask); kStore: also the
+  // softmax cache values of these rows (staged in LDS for bf16)
+  template <bool kFull, bool kStore>
   __device__ __forceinline__ void column(const Acc& acc, int j, int vlim, int lane, bool with_u,
-                                         float& mx, float& s, float& u) const {
+                                         float& mx, float& s, float& u, char* lds, int wm,
+                                         int tl, int64_t m0, int64_t t) const {
     mx = kNegInf;
 #pragma unroll
     for (int i = 0; i < kTM; ++i)
@@ -97,19 +136,37 @@ struct EpiFwd {
     s = 0.0f;
     u = 0.0f;
 #pragma unroll
-    for (int i = 0; i < kTM; ++i)
+    for (int i = 0; i < kTM; ++i) {
+      f32x4 xs;
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
+      for (int e = 0; e < 4; ++e) {
+        xs[e] = 0.0f;
         if (kFull || wrow(i, e, lane) < vlim) {
           const float x = __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
           s += x;
           if (with_u) u = fmaf(x, acc[i][j][e], u);
+          xs[e] = x;
         }
+      }
+      if constexpr (kStore) {
+        const int vr = wm * kWaveRows + wrow(i, 0, lane);   // tile row of element 0
+        if constexpr (sizeof(T) == 2) {
+          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+          *reinterpret_cast<u32x2*>(lds + panel_stage_off(vr, tl)) =
+              __builtin_bit_cast(u32x2, __builtin_convertvector(xs, bf16x4));
+        } else {
+          const int64_t c = m0 + vr;
+          if (t < Tn && c < ldE)
+            *reinterpret_cast<f32x4*>(E + (c / kPanel) * pld * kPanel + t * kPanel + c % kPanel) =
+                xs;
+        }
+      }
+    }
     s = quad_sum(s);
     if (with_u) u = quad_sum(u);
   }
 
-  __device__ void epilogue(Acc& acc, int tm, int, int64_t m0, int64_t n0, char*,
+  __device__ void epilogue(Acc& acc, int tm, int, int64_t m0, int64_t n0, char* lds,
                            char* extra) const {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wm = wave_m(), wn = wave_n();
@@ -121,9 +178,20 @@ struct EpiFwd {
 #pragma unroll
     for (int j = 0; j < kTN; ++j) {
       const int tl = wn * kWaveCols + j * 16 + (lane & 15);   // token within the tile
+      const int64_t t = n0 + tl;
       float mx, s, u;
-      if (vlim >= kWaveRows) column<true>(acc, j, vlim, lane, with_u, mx, s, u);
-      else column<false>(acc, j, vlim, lane, with_u, mx, s, u);
+      if (E != nullptr) {
+        if (vlim >= kWaveRows)
+          column<true, true>(acc, j, vlim, lane, with_u, mx, s, u, lds, wm, tl, m0, t);
+        else
+          column<false, true>(acc, j, vlim, lane, with_u, mx, s, u, lds, wm, tl, m0, t);
+        if (lane < 16 && t < Tn) cm[(int64_t(tm) * kWavesM + wm) * Tn + t] = mx;
+      } else {
+        if (vlim >= kWaveRows)
+          column<true, false>(acc, j, vlim, lane, with_u, mx, s, u, lds, wm, tl, m0, t);
+        else
+          column<false, false>(acc, j, vlim, lane, with_u, mx, s, u, lds, wm, tl, m0, t);
+      }
       // target logit: row yw of this wave, held by the lane of group (yw >> 2) & 3
       const int yw = ys[tl] - int(rbase);
       if (yw >= 0 && yw < kWaveRows && ((yw >> 2) & 3) == (lane >> 4)) {
@@ -143,9 +211,11 @@ struct EpiFwd {
       }
     }
     __syncthreads();
+    if constexpr (sizeof(T) == 2)
+      if (E != nullptr) store_staged_panels(lds, E, m0, n0, Tn, ldE, pld);
     for (int tl = tid; tl < kBN; tl += kThreads) {
       const int64_t t = n0 + tl;
-      if (t >= T) continue;
+      if (t >= Tn) continue;
       float M = red[tl];
 #pragma unroll
       for (int w = 1; w < kWavesM; ++w) M = fmaxf(M, red[w * 256 + tl]);
@@ -159,9 +229,9 @@ struct EpiFwd {
           U += red[(2 * kWavesM + w) * 256 + tl] * f;
         }
       }
-      part_m[int64_t(tm) * T + t] = M;
-      part_s[int64_t(tm) * T + t] = S;
-      if (with_u) part_u[int64_t(tm) * T + t] = U;
+      part_m[int64_t(tm) * Tn + t] = M;
+      part_s[int64_t(tm) * Tn + t] = S;
+      if (with_u) part_u[int64_t(tm) * Tn + t] = U;
     }
   }
 };
@@ -306,12 +376,6 @@ struct EpiProbs {
     }
   }
 
-  // Element (t, v) of the tile staged in LDS (bf16): four 32 KiB panels of
-  // 256 token rows x 128 bytes, the 16-byte chunk index XOR-ed with t & 7.
-  __device__ static int stage_off(int v, int t) {
-    return (v >> 6) * 32768 + t * 128 + ((((v & 63) >> 3) ^ (t & 7)) << 4) + ((v & 7) << 1);
-  }
-
   // P~ of this lane's elements.  vlim: valid rows (v < width) of the wave,
   // llim: rows below ld (a multiple of 4); kFull: all kWaveRows rows valid.
   template <bool kFull>
@@ -338,7 +402,7 @@ struct EpiProbs {
           const int vr = wm * kWaveRows + r;   // row of the tile
           if constexpr (sizeof(T) == 2) {
             typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-            *reinterpret_cast<u32x2*>(lds + stage_off(vr, tl)) =
+            *reinterpret_cast<u32x2*>(lds + panel_stage_off(vr, tl)) =
                 __builtin_bit_cast(u32x2, __builtin_convertvector(p, bf16x4));
           } else {
             const int64_t c = m0 + vr;
@@ -364,17 +428,8 @@ struct EpiProbs {
     else
       values<false>(acc, lds, lane, wm, wn, l2, g, vlim, llim, m0, n0);
     if constexpr (sizeof(T) == 2) {
-      // each panel's 256 token rows are 32 KiB of contiguous memory: 16-byte
-      // stores, eight lanes per 128-byte row
       __syncthreads();
-      for (int k = threadIdx.x; k < 4 * 256 * 8; k += kThreads) {
-        const int pn = k >> 11, tl = (k >> 3) & 255, ch = k & 7;
-        const int64_t t = n0 + tl, c = m0 + pn * 64;
-        if (t >= Tn || c >= ld) continue;
-        const u32x4 val = *reinterpret_cast<const u32x4*>(
-            lds + pn * 32768 + tl * 128 + ((ch ^ (tl & 7)) << 4));
-        *reinterpret_cast<u32x4*>(P + (c / kPanel) * pld * kPanel + t * kPanel + ch * 8) = val;
-      }
+      store_staged_panels(lds, P, m0, n0, Tn, ld, pld);
     }
   }
 };
@@ -567,10 +622,45 @@ __global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
 }
 
 // Named kernels, one per role of the shared tile core.
+// Softmax cache -> backward operand, in place: P~[t, v] = -dlogp_t
+// exp(cm[v / kWaveRows][t] - lse_t) E[t, v] (0 for ignored tokens).  One 16-byte
+// chunk of a panel row per thread (grid-stride): 8 bf16 or 4 fp32 entries of
+// one token, all in one block of kWaveRows rows.
+template <typename T>
+__global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
+                                                        const float* __restrict__ cm,
+                                                        const float* __restrict__ lse,
+                                                        const float* __restrict__ dlogp,
+                                                        const int64_t* __restrict__ y,
+                                                        int64_t Tn, int64_t V, int64_t pld,
+                                                        int64_t ldE) {
+  constexpr int64_t BV = 128 / sizeof(T);    // panel width
+  constexpr int64_t CE = 16 / sizeof(T);     // entries per chunk
+  constexpr int64_t CPR = BV / CE;           // chunks per panel row (8)
+  const int64_t n = (ldE / BV) * Tn * CPR;
+  for (int64_t q = blockIdx.x * int64_t(256) + threadIdx.x; q < n;
+       q += int64_t(gridDim.x) * 256) {
+    const int64_t pn = q / (Tn * CPR);
+    const int64_t r = q - pn * (Tn * CPR);
+    const int64_t t = r / CPR, ch = r % CPR;
+    const int64_t v = pn * BV + ch * CE;
+    const int64_t yy = y[t];
+    const float g = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
+    const float m = cm[(v / kWaveRows) * Tn + t];
+    const float f = (g == 0.0f || m == kNegInf) ? 0.0f : g * __expf(m - lse[t]);
+    T* p = E + pn * pld * BV + t * BV + ch * CE;
+    T vals[CE];
+    *reinterpret_cast<u32x4*>(vals) = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+    for (int e = 0; e < CE; ++e) vals[e] = T(float(vals[e]) * f);
+    *reinterpret_cast<u32x4*>(p) = *reinterpret_cast<const u32x4*>(vals);
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_fwd_logits_lse(Operand A, Operand B, int64_t K,
-                                                                int nTm, int nTn, EpiFwd epi) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiFwd::kLdsExtra];
+                                                                int nTm, int nTn, EpiFwd<T> epi) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiFwd<T>::kLdsExtra];
   gemm_body<T, Lay::KMajor, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
 }
 template <typename T>
@@ -598,7 +688,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand 
 template <typename T>
 hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_t d, int64_t Vs,
                     int64_t v_off, int64_t V, float* logp, float* lse, float* entropy,
-                    float* part, bool with_u, void* ws, hipStream_t s) {
+                    float* part, bool with_u, void* ws, hipStream_t s, T* cacheE = nullptr,
+                    float* cacheM = nullptr) {
   // tile rows: vocabulary (the weight's rows), tile columns: tokens
   const int nTv = int(cdiv(Vs, kBM)), nTt = int(cdiv(Tn, kBN));
   Carve cv(ws);
@@ -611,10 +702,13 @@ hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_
   if (!operand_in_bounds<T, Lay::KMajor>(A, size_t(Vs) * d * sizeof(T)) ||
       !operand_in_bounds<T, Lay::KMajor>(B, size_t(Tn) * d * sizeof(T)))
     return hipErrorInvalidValue;
-  EpiFwd epi{y, Tn, Vs, v_off, pm, ps, pu, part ? part + 3 * Tn : logp};
+  const int64_t pld = cdiv(Tn, 64) * 64, ldE = int64_t(align_up(size_t(Vs), 64));
+  EpiFwd<T> epi{y,  Tn,     Vs,     v_off,  pm,  ps, pu, part ? part + 3 * Tn : logp,
+                cacheE, cacheM, pld, ldE};
   {
     ProfScope ps_(s, "logprob_fwd_gemm", 2.0 * Tn * d * Vs,
-                  es * (double(Tn) * d + double(Vs) * d) + 12.0 * Tn);
+                  es * (double(Tn) * d + double(Vs) * d) + 12.0 * Tn +
+                      (cacheE ? es * double(Tn) * Vs + 8.0 * nTv * Tn : 0.0));
     hipLaunchKernelGGL(k_fwd_logits_lse<T>, dim3(nTv * nTt), dim3(kThreads), 0,
                        s, A, B, d, nTv, nTt, epi);
   }
@@ -637,12 +731,16 @@ hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_
 template <typename T>
 hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                     const float* dlogp, int64_t Tn, int64_t d, int64_t Vs, int64_t v_off,
-                    int64_t V, float* dH, float* dW, int flags, void* ws, hipStream_t s) {
-  const int64_t chunk = bwd_chunk_cols(Tn, Vs, sizeof(T));
+                    int64_t V, float* dH, float* dW, int flags, void* ws, hipStream_t s,
+                    T* cacheE = nullptr, const float* cacheM = nullptr) {
+  // With a softmax cache the whole vocabulary is one chunk and the operand is
+  // the cache itself, normalised in place; otherwise the logits of each chunk
+  // are recomputed.
+  const int64_t chunk = cacheE ? Vs : bwd_chunk_cols(Tn, Vs, sizeof(T));
   const int64_t ld = int64_t(align_up(size_t(min(chunk, Vs)), 64));
   const int64_t pld = cdiv(Tn, 64) * 64;
   Carve cv(ws);
-  T* P = cv.take<T>(size_t(pld) * ld);
+  T* P = cacheE ? cacheE : cv.take<T>(size_t(pld) * ld);
   T* Wt = cv.take<T>(size_t(d) * ld);    // [d x chunk] transpose of W's chunk rows
   T* Ht = cv.take<T>(size_t(d) * pld);   // [d x T] transpose of H
   int* counts = cv.take<int>(Vs);
@@ -672,7 +770,13 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
     const T* Wc = W + v0 * d;
     const size_t wc_bytes = size_t(Vs - v0) * d * sizeof(T);
     const size_t p_bytes = size_t(pld) * ld * sizeof(T);
-    {
+    if (cacheE) {
+      ProfScope ps_(s, "logprob_bwd_cache_probs", 0.0, 2.0 * es * double(Tn) * ldc + 4.0 * Tn * 5);
+      const int64_t chunks = (ldc / (128 / int64_t(sizeof(T)))) * Tn * 8;
+      const int blocks = int(std::min<int64_t>(cdiv(chunks, 256), 256 * 64));
+      hipLaunchKernelGGL(k_cache_to_probs<T>, dim3(blocks), dim3(256), 0, s, P, cacheM, lse, dlogp,
+                         y, Tn, V, pld, ldc);
+    } else {
       // tile rows: chunk columns (up to the padded width ldc), tile columns: tokens
       Operand A{Wc, d, width, d}, B{H, d, Tn, d};
       if (!operand_in_bounds<T, Lay::KMajor>(A, wc_bytes) ||
@@ -755,6 +859,25 @@ size_t fwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t) {
   return 3 * align_up(n * sizeof(float), kWsAlign);
 }
 
+size_t cache_bytes(int64_t T, int64_t, int64_t V, mc_dtype_t dt) {
+  const size_t es = dt == MC_BF16 ? 2 : 4;
+  const size_t pld = size_t(cdiv(T, 64)) * 64, ldE = align_up(size_t(V), 64);
+  return align_up(pld * ldE * es, kWsAlign) +
+         align_up(size_t(cdiv(V, kBM)) * kWavesM * size_t(T) * 4, kWsAlign);
+}
+
+size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
+  const size_t es = dt == MC_BF16 ? 2 : 4;
+  const size_t ld = align_up(size_t(V), 64);
+  const size_t pld = size_t(cdiv(T, 64)) * 64;
+  size_t n = align_up(size_t(d) * ld * es, kWsAlign);
+  n += align_up(size_t(d) * pld * es, kWsAlign);
+  n += 2 * align_up(size_t(V) * 4, kWsAlign);
+  n += align_up(size_t(V + 1) * 4, kWsAlign);
+  n += 2 * align_up(size_t(T) * 4, kWsAlign);
+  return n;
+}
+
 size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   const size_t es = dt == MC_BF16 ? 2 : 4;
   const int64_t chunk = bwd_chunk_cols(T, V, es);
@@ -797,6 +920,51 @@ hipError_t launch_bwd(const void* H, const void* W, const int64_t* y, const floa
                     T, d, Vs, v_off, V, dH, dW, flags, ws, s);
   return bwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, lse, dlogp, T,
                   d, Vs, v_off, V, dH, dW, flags, ws, s);
+}
+
+// Softmax cache layout: E panels [ldE / BV][pld][BV] in the kernel dtype,
+// then the block maxima [2 nTv][T] fp32.
+template <typename T>
+static void carve_cache(void* cache, int64_t T_, int64_t V, T*& E, float*& cm) {
+  Carve cv(cache);
+  const size_t pld = size_t(cdiv(T_, 64)) * 64, ldE = align_up(size_t(V), 64);
+  E = cv.take<T>(pld * ldE);
+  cm = cv.take<float>(size_t(cdiv(V, kBM)) * kWavesM * size_t(T_));
+}
+
+hipError_t launch_fwd_cache(const void* H, const void* W, const int64_t* y, int64_t T, int64_t d,
+                            int64_t V, mc_dtype_t dt, float* logp, float* lse, float* entropy,
+                            void* cache, void* ws, hipStream_t s) {
+  if (dt == MC_BF16) {
+    bf16_t* E;
+    float* cm;
+    carve_cache(cache, T, V, E, cm);
+    return fwd_impl(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W), y, T, d, V,
+                    int64_t(0), V, logp, lse, entropy, nullptr, entropy != nullptr, ws, s, E, cm);
+  }
+  float* E;
+  float* cm;
+  carve_cache(cache, T, V, E, cm);
+  return fwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, T, d, V,
+                  int64_t(0), V, logp, lse, entropy, nullptr, entropy != nullptr, ws, s, E, cm);
+}
+
+hipError_t launch_bwd_cache(const void* H, const void* W, const int64_t* y, const float* lse,
+                            const float* dlogp, int64_t T, int64_t d, int64_t V, mc_dtype_t dt,
+                            void* cache, float* dH, float* dW, int flags, void* ws,
+                            hipStream_t s) {
+  if (dt == MC_BF16) {
+    bf16_t* E;
+    float* cm;
+    carve_cache(cache, T, V, E, cm);
+    return bwd_impl(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W), y, lse, dlogp,
+                    T, d, V, int64_t(0), V, dH, dW, flags, ws, s, E, cm);
+  }
+  float* E;
+  float* cm;
+  carve_cache(cache, T, V, E, cm);
+  return bwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, lse, dlogp, T, d,
+                  V, int64_t(0), V, dH, dW, flags, ws, s, E, cm);
 }
 
 }  // namespace mc

@@ -171,3 +171,27 @@ def test_shard_and_primeecho_argument_checks(lib):
     assert pe(4, 3, 1.5, 0.0) == INVALID        # alpha outside [0, 1]
     assert pe(4, 3, 0.5, float("inf")) == INVALID
     assert pe(0, 3, 0.5, 0.0) == OK             # no trajectories: no-op
+
+
+def test_cached_argument_checks(lib):
+    T, d, V = 16, 64, 100
+    need_c = lib.mc_logprob_cache_size(T, d, V, BF16)
+    need_f = lib.mc_logprob_fwd_workspace_size(T, d, V, BF16)
+    need_b = lib.mc_logprob_bwd_cached_workspace_size(T, d, V, BF16)
+    # the cache holds the padded [T x V] exp operand and the block maxima
+    assert need_c >= 64 * 128 * 2 + 16 * 4 and lib.mc_logprob_cache_size(T, 60, V, BF16) == 0
+    assert 0 < need_b < lib.mc_logprob_bwd_workspace_size(T, d, V, BF16)
+    fwd = lambda cache, cb, ws=FAKE_WS, wb=need_f: lib.mc_logprob_fwd_cached(
+        FAKE, FAKE, FAKE, T, d, V, BF16, FAKE, FAKE, None, cache, cb, ws, wb, None)
+    assert fwd(None, need_c) == WS
+    assert fwd(FAKE_WS, need_c - 1) == WS
+    assert fwd(FAKE_WS + 128, need_c) == WS        # cache not 256-byte aligned
+    assert fwd(FAKE_WS, need_c, wb=1) == WS
+    bwd = lambda cache, cb, flags=0, dh=FAKE: lib.mc_logprob_bwd_cached(
+        FAKE, FAKE, FAKE, FAKE, FAKE, T, d, V, BF16, cache, cb, dh, FAKE, flags, FAKE_WS, need_b,
+        None)
+    assert bwd(None, need_c) == WS
+    assert bwd(FAKE_WS, 0) == WS
+    assert bwd(FAKE_WS, need_c, flags=8) == INVALID
+    assert bwd(FAKE_WS, need_c, dh=FAKE + 4) == INVALID
+
