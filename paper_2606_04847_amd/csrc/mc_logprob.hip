@@ -623,9 +623,12 @@ __global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
 
 // Named kernels, one per role of the shared tile core.
 // Softmax cache -> backward operand, in place: P~[t, v] = -dlogp_t
-// exp(cm[v / kWaveRows][t] - lse_t) E[t, v] (0 for ignored tokens).  One 16-byte
-// chunk of a panel row per thread (grid-stride): 8 bf16 or 4 fp32 entries of
-// one token, all in one block of kWaveRows rows.
+// exp(cm[v / kWaveRows][t] - lse_t) E[t, v] (0 for ignored tokens).
+// Grid: x over blocks of 32 tokens, y over groups of kCachePanels panels
+// from panel pn0; thread = one 16-byte chunk of one row of each of those
+// panels (8 lanes per 128-byte row).  The stream is touched once:
+// non-temporal loads and stores.
+constexpr int kCachePanels = 4;
 template <typename T>
 __global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
                                                         const float* __restrict__ cm,
@@ -633,27 +636,39 @@ __global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
                                                         const float* __restrict__ dlogp,
                                                         const int64_t* __restrict__ y,
                                                         int64_t Tn, int64_t V, int64_t pld,
-                                                        int64_t ldE) {
-  constexpr int64_t BV = 128 / sizeof(T);    // panel width
-  constexpr int64_t CE = 16 / sizeof(T);     // entries per chunk
-  constexpr int64_t CPR = BV / CE;           // chunks per panel row (8)
-  const int64_t n = (ldE / BV) * Tn * CPR;
-  for (int64_t q = blockIdx.x * int64_t(256) + threadIdx.x; q < n;
-       q += int64_t(gridDim.x) * 256) {
-    const int64_t pn = q / (Tn * CPR);
-    const int64_t r = q - pn * (Tn * CPR);
-    const int64_t t = r / CPR, ch = r % CPR;
-    const int64_t v = pn * BV + ch * CE;
-    const int64_t yy = y[t];
-    const float g = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
-    const float m = cm[(v / kWaveRows) * Tn + t];
-    const float f = (g == 0.0f || m == kNegInf) ? 0.0f : g * __expf(m - lse[t]);
-    T* p = E + pn * pld * BV + t * BV + ch * CE;
-    T vals[CE];
-    *reinterpret_cast<u32x4*>(vals) = *reinterpret_cast<const u32x4*>(p);
+                                                        int64_t pn0, int64_t npanels) {
+  constexpr int BV = 128 / sizeof(T);   // panel width
+  constexpr int CE = 16 / sizeof(T);    // entries per chunk
+  const int64_t t = int64_t(blockIdx.x) * 32 + (threadIdx.x >> 3);
+  if (t >= Tn) return;
+  const int ch = threadIdx.x & 7;
+  const int64_t yy = y[t];
+  const float g = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
+  const float l = lse[t];
+  const int64_t p0 = pn0 + int64_t(blockIdx.y) * kCachePanels;
+  u32x4 raw[kCachePanels];
+  float f[kCachePanels];
 #pragma unroll
-    for (int e = 0; e < CE; ++e) vals[e] = T(float(vals[e]) * f);
-    *reinterpret_cast<u32x4*>(p) = *reinterpret_cast<const u32x4*>(vals);
+  for (int q = 0; q < kCachePanels; ++q) {
+    const int64_t pn = p0 + q;
+    if (pn < npanels) {
+      raw[q] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4*>(E + (pn * pld + t) * BV + ch * CE));
+      const float m = cm[((pn * BV + ch * CE) / kWaveRows) * Tn + t];
+      f[q] = (g == 0.0f || m == kNegInf) ? 0.0f : g * __expf(m - l);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kCachePanels; ++q) {
+    const int64_t pn = p0 + q;
+    if (pn < npanels) {
+      T vals[CE];
+      *reinterpret_cast<u32x4*>(vals) = raw[q];
+#pragma unroll
+      for (int e = 0; e < CE; ++e) vals[e] = T(float(vals[e]) * f[q]);
+      __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(vals),
+                                  reinterpret_cast<u32x4*>(E + (pn * pld + t) * BV + ch * CE));
+    }
   }
 }
 
@@ -772,10 +787,13 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
     const size_t p_bytes = size_t(pld) * ld * sizeof(T);
     if (cacheE) {
       ProfScope ps_(s, "logprob_bwd_cache_probs", 0.0, 2.0 * es * double(Tn) * ldc + 4.0 * Tn * 5);
-      const int64_t chunks = (ldc / (128 / int64_t(sizeof(T)))) * Tn * 8;
-      const int blocks = int(std::min<int64_t>(cdiv(chunks, 256), 256 * 64));
-      hipLaunchKernelGGL(k_cache_to_probs<T>, dim3(blocks), dim3(256), 0, s, P, cacheM, lse, dlogp,
-                         y, Tn, V, pld, ldc);
+      const int64_t panels = ldc / (128 / int64_t(sizeof(T)));
+      const int64_t groups = cdiv(panels, kCachePanels);
+      for (int64_t g0 = 0; g0 < groups; g0 += 65535) {   // grid y is at most 65535
+        const unsigned ng = unsigned(std::min<int64_t>(65535, groups - g0));
+        hipLaunchKernelGGL(k_cache_to_probs<T>, dim3(unsigned(cdiv(Tn, 32)), ng), dim3(256), 0, s,
+                           P, cacheM, lse, dlogp, y, Tn, V, pld, g0 * kCachePanels, panels);
+      }
     } else {
       // tile rows: chunk columns (up to the padded width ldc), tile columns: tokens
       Operand A{Wc, d, width, d}, B{H, d, Tn, d};
