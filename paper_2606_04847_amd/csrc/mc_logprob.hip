@@ -60,8 +60,10 @@ __device__ __forceinline__ int panel_stage_off(int v, int t) {
 }
 
 // Each panel's 256 token rows are 32 KiB of contiguous memory: 16-byte
-// stores, eight lanes per 128-byte row.  Rows t >= Tn and chunk columns
-// >= ld are skipped.  The caller has synchronised after staging.
+// stores, eight lanes per 128-byte row, non-temporal (the operand is far
+// larger than the caches and next read by another kernel).  Rows t >= Tn
+// and chunk columns >= ld are skipped.  The caller has synchronised after
+// staging.
 __device__ __forceinline__ void store_staged_panels(const char* lds, bf16_t* P, int64_t m0,
                                                     int64_t n0, int64_t Tn, int64_t ld,
                                                     int64_t pld) {
@@ -72,7 +74,8 @@ __device__ __forceinline__ void store_staged_panels(const char* lds, bf16_t* P, 
     if (t >= Tn || c >= ld) continue;
     const u32x4 val =
         *reinterpret_cast<const u32x4*>(lds + pn * 32768 + tl * 128 + ((ch ^ (tl & 7)) << 4));
-    *reinterpret_cast<u32x4*>(P + (c / kPanel) * pld * kPanel + t * kPanel + ch * 8) = val;
+    __builtin_nontemporal_store(
+        val, reinterpret_cast<u32x4*>(P + (c / kPanel) * pld * kPanel + t * kPanel + ch * 8));
   }
 }
 

@@ -685,6 +685,14 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     char* nxt = lds + ((kt + 1) & 1) * (2 * kStageBytes);
     read_frags<T, SA, SB>(a1, b1, cur, cur + kStageBytes, wm, wn, lane, 1);
     Mfma<T>::step(acc, a0, b0);
+    // issue order: one MFMA, one fragment read, ... so that the reads go out
+    // while the MFMA pipe is busy
+#pragma unroll
+    for (int r = 0; r < kTM + kTN; ++r) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kTM * kTN - (kTM + kTN), 0);
     // this wave: copies of stage kt+1 landed, reads of stage kt returned;
     // nothing is scheduled across the barrier
     __builtin_amdgcn_sched_barrier(0);
@@ -693,13 +701,28 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
-    if (kt + 2 < nk) {
-      ca.issue(kt + 2, cur);
-      cb.issue(kt + 2, cur + kStageBytes);
-    }
-    if (kt + 1 < nk) read_frags<T, SA, SB>(a0, b0, nxt, nxt + kStageBytes, wm, wn, lane, 0);
+    // stage kt+2 (past the end: every chunk out of K, zero-filled, harmless
+    // in a released buffer); the first fragments of stage kt+1 (past the
+    // end: unused)
+    ca.issue(kt + 2, cur);
+    cb.issue(kt + 2, cur + kStageBytes);
+    read_frags<T, SA, SB>(a0, b0, nxt, nxt + kStageBytes, wm, wn, lane, 0);
     Mfma<T>::step(acc, a1, b1);
+#pragma unroll
+    for (int r = 0; r < CA::NI + CB::NI; ++r) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // copy issue
+    }
+#pragma unroll
+    for (int r = 0; r < kTM + kTN; ++r) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kTM * kTN - (CA::NI + CB::NI) - (kTM + kTN), 0);
   }
+  // the zero-filling copies issued by the last two steps land before the
+  // LDS is reused
+  __builtin_amdgcn_s_waitcnt(0x0070);
   __syncthreads();
 }
 
