@@ -653,16 +653,31 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     // A transposing-read operand needs per-block fragment addresses; without
     // the spare registers for the cross-barrier prefetch, one barrier at the
     // top of each step: it publishes step k and releases step k-1's buffer.
+    constexpr int kReads = (SA == Stg::MN ? 2 : 1) * kTM + (SB == Stg::MN ? 2 : 1) * kTN;
     for (int64_t kt = 0; kt < nk; ++kt) {
       char* cur = lds + (kt & 1) * (2 * kStageBytes);
       char* nxt = lds + ((kt + 1) & 1) * (2 * kStageBytes);
       dma_wait_barrier();
-      if (kt + 1 < nk) {
-        ca.issue(kt + 1, nxt);
-        cb.issue(kt + 1, nxt + kStageBytes);
+      __builtin_amdgcn_sched_barrier(0);
+      // past the end: zero-filling copies into the released buffer
+      ca.issue(kt + 1, nxt);
+      cb.issue(kt + 1, nxt + kStageBytes);
+      u32x4 a0[kTM], b0[kTN], a1[kTM], b1[kTN];
+      read_frags<T, SA, SB>(a0, b0, cur, cur + kStageBytes, wm, wn, lane, 0);
+      Mfma<T>::step(acc, a0, b0);
+      read_frags<T, SA, SB>(a1, b1, cur, cur + kStageBytes, wm, wn, lane, 1);
+      Mfma<T>::step(acc, a1, b1);
+      // the step-1 reads go out one per MFMA of step 0
+      __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);   // step-0 reads
+#pragma unroll
+      for (int r = 0; r < kReads; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);     // step-1 read
       }
-      mfma_stage<T, SA, SB>(acc, cur, cur + kStageBytes, wm, wn, lane);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * kTM * kTN - kReads, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    __builtin_amdgcn_s_waitcnt(0x0070);
     __syncthreads();
     return;
   }
