@@ -33,10 +33,25 @@ METRIC = "fused logprob fwd+bwd tokens/s @ d=4096,V=151936; % bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2516.6     # 256 CUs x 4096 FLOP/clk x 2.4 GHz, dense bf16
 PEAK_FP32_TFLOPS = 157.3
 
-# HBM traffic of the dominant kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
-# passes, valid only for the kernel sources with this digest (else null).
-TRAFFIC = {"sources_sha256": "cd8fc555e1a934be6bf1add645b1c4a52f7af7689286082e62cacf261a1bae8a",
-           "kernel": "logprob_bwd_dweight", "bytes_per_launch": 3.826369e+10}
+# HBM traffic per launch of the step's kernels from rocprofv3 FETCH_SIZE /
+# WRITE_SIZE passes (scaled by the 1 GiB copy calibration), valid only for
+# the kernel sources with this digest (else null).
+TRAFFIC = {
+    "sources_sha256":
+        "b739e88bf9bae41e05fd7630f48e30c83a6618bf8530d600a66eb44fd008e732",
+    "bytes_per_launch": {
+        "logprob_fwd_gemm": 38159103966,
+        "logprob_fwd_merge": 78265908,
+        "rl_loss": 91896,
+        "logprob_bwd_bucket": 1436900,
+        "logprob_bwd_cache_probs": 10035310241,
+        "logprob_bwd_transpose": 1905338247,
+        "logprob_bwd_dhidden": 30224290064,
+        "logprob_bwd_dweight": 38750683180,
+        "logprob_bwd_onehot_dh": 674107502,
+        "logprob_bwd_onehot_dw": 650862578,
+    },
+}
 
 
 def sources_digest() -> str:
@@ -208,8 +223,8 @@ def main():
     dom_ms = dom["ms"] / dom["launches"]
     achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
     traffic = None
-    if (TRAFFIC["sources_sha256"] == sources_digest() and TRAFFIC["kernel"] == dom_name):
-        traffic = TRAFFIC["bytes_per_launch"]
+    if TRAFFIC["sources_sha256"] == sources_digest():
+        traffic = TRAFFIC["bytes_per_launch"].get(dom_name)
     roofline = {"bound": "mfma", "kernel": dom_name, "achieved": achieved,
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                 "traffic": traffic, "avg_launch_ms": dom_ms,
