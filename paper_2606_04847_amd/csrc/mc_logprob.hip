@@ -437,6 +437,57 @@ struct EpiProbs {
   }
 };
 
+// dH tile epilogue (rows: tokens, columns: hidden dimensions): stores (or
+// adds) the tile, plus the one-hot part of G W when W is set:
+//   dH[t, c] (+)= tile[t, c] + dlogp_t W[y_t - v_off, c]   (y_t in the shard)
+// in that order, all in fp32.
+template <typename T>
+struct EpiDH {
+  float* C;
+  int64_t ldc, rows, cols;
+  int accumulate;
+  const T* W;   // [Vs x ldc] weight shard, or null: no one-hot part here
+  const int64_t* y;
+  const float* dlogp;
+  int64_t v_off, Vs;
+  static constexpr int kLdsExtra = 16;
+
+  __device__ void prologue(int64_t, int64_t, char*) const {}
+  __device__ __forceinline__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char*,
+                                          char*) const {
+    const int lane = threadIdx.x & 63;
+    const int wm = wave_m(), wn = wave_n();
+#pragma unroll
+    for (int i = 0; i < kTM; ++i) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t r = m0 + acc_row(wm, i, e, lane);
+        if (r >= rows) continue;
+        float* crow = C + r * ldc;
+        const T* w = nullptr;
+        float g = 0.0f;
+        if (W != nullptr) {
+          const int64_t yy = y[r] - v_off;
+          if (yy >= 0 && yy < Vs) {
+            w = W + yy * ldc;
+            g = dlogp[r];
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < kTN; ++j) {
+          const int64_t c = n0 + acc_col(wn, j, lane);
+          if (c < cols) {
+            float v = acc[i][j][e];
+            if (accumulate) v += crow[c];
+            if (w != nullptr) v += g * float(w[c]);
+            crow[c] = v;
+          }
+        }
+      }
+    }
+  }
+};
+
 // Plain fp32 store (or accumulate) of the tile into C[rows x cols], ld = ldc.
 struct EpiStore {
   float* C;
@@ -469,23 +520,6 @@ struct EpiStore {
   }
 };
 
-// dH[t, :] += dlogp_t W[y_t, :]  (the one-hot part of G W, exact in fp32).
-template <typename T>
-__global__ __launch_bounds__(256) void k_onehot_dh(const T* __restrict__ W,
-                                                   const int64_t* __restrict__ y,
-                                                   const float* __restrict__ dlogp,
-                                                   int64_t d, int64_t v_off, int64_t V,
-                                                   float* __restrict__ dH) {
-  const int64_t t = blockIdx.x;
-  const int64_t yy = y[t] - v_off;
-  if (yy < 0 || yy >= V) return;
-  const float g = dlogp[t];
-  const T* w = W + yy * d;
-  float* o = dH + t * d;
-  for (int64_t k = threadIdx.x; k < d; k += blockDim.x) o[k] += g * float(w[k]);
-}
-
-// --- deterministic bucketing of tokens by target (for the one-hot part of dW)
 // out[c][r] = in[r][c] for r < rows, c < cols, and out[c][r] = 0 for
 // rows <= r < 64 ceil(rows / 64) (ld_out covers that padding; cols, ld_in and
 // ld_out are multiples of 8).  The zero padding matters: a K-contiguous
@@ -534,6 +568,7 @@ __global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ in, int
   }
 }
 
+// --- deterministic bucketing of tokens by target (for the one-hot part of dW)
 __global__ void k_fill_i32(int* __restrict__ p, int64_t n, int v) {
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i < n) p[i] = v;
@@ -547,30 +582,64 @@ __global__ void k_hist(const int64_t* __restrict__ y, int64_t T, int64_t v_off, 
   if (yy >= 0 && yy < V) atomicAdd(counts + yy, 1);
 }
 
-// Exclusive scan of counts[V] into offsets[V+1] by one block of 1024 threads,
-// each owning a contiguous segment.
-__global__ __launch_bounds__(1024) void k_scan(const int* __restrict__ counts, int64_t V,
-                                               int* __restrict__ offsets) {
-  __shared__ int part[1024];
-  const int tid = threadIdx.x;
-  const int64_t seg = (V + 1023) / 1024;
-  const int64_t b = imin(V, tid * seg), e = imin(V, b + seg);
-  int s = 0;
-  for (int64_t i = b; i < e; ++i) s += counts[i];
-  part[tid] = s;
+// Exclusive scan of counts[V] into offsets[V + 1] in two passes over blocks
+// of kScanBlock entries (256 threads x 4 consecutive entries, coalesced):
+// k_scan_sums writes each block's total, k_scan_apply adds the totals of the
+// blocks before its own to an in-block scan.  Integer sums: exact.
+constexpr int kScanBlock = 1024;
+
+__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(v, o, 64);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+__global__ __launch_bounds__(256) void k_scan_sums(const int* __restrict__ counts, int64_t V,
+                                                   int* __restrict__ sums) {
+  __shared__ int part[4];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int64_t i0 = int64_t(blockIdx.x) * kScanBlock + tid * 4;
+  int v = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (i0 + q < V) v += counts[i0 + q];
+  v = wave_incl_scan(v, lane);
+  if (lane == 63) part[tid >> 6] = v;
   __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int v = tid >= off ? part[tid - off] : 0;
-    __syncthreads();
-    part[tid] += v;
-    __syncthreads();
+  if (tid == 0) sums[blockIdx.x] = part[0] + part[1] + part[2] + part[3];
+}
+
+__global__ __launch_bounds__(256) void k_scan_apply(const int* __restrict__ counts, int64_t V,
+                                                    const int* __restrict__ sums,
+                                                    int* __restrict__ offsets) {
+  __shared__ int part[4];
+  __shared__ int base[4];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // total of the blocks before this one
+  int pre = 0;
+  for (int k = tid; k < int(blockIdx.x); k += 256) pre += sums[k];
+  pre = wave_incl_scan(pre, lane);
+  if (lane == 63) base[w] = pre;
+  // in-block exclusive scan
+  const int64_t i0 = int64_t(blockIdx.x) * kScanBlock + tid * 4;
+  int c[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) c[q] = i0 + q < V ? counts[i0 + q] : 0;
+  const int own = c[0] + c[1] + c[2] + c[3];
+  const int incl = wave_incl_scan(own, lane);
+  if (lane == 63) part[w] = incl;
+  __syncthreads();
+  int run = base[0] + base[1] + base[2] + base[3] + incl - own;
+  for (int k = 0; k < w; ++k) run += part[k];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (i0 + q < V) offsets[i0 + q] = run;
+    run += c[q];
   }
-  int run = part[tid] - s;
-  for (int64_t i = b; i < e; ++i) {
-    offsets[i] = run;
-    run += counts[i];
-  }
-  if (tid == 1023) offsets[V] = part[1023];
+  if (i0 < V && i0 + 4 >= V) offsets[V] = run;   // the thread holding entry V - 1
 }
 
 __global__ void k_bucket_fill(const int64_t* __restrict__ y, int64_t T, int64_t v_off,
@@ -599,6 +668,7 @@ __global__ void k_bucket_rank(const int64_t* __restrict__ y, int64_t T, int64_t 
 
 // dW[v, :] += sum over tokens t with y_t = v (ascending t) of dlogp_t h_t.
 // One block per bucketed position; only the first position of a bucket works.
+// Each thread owns 4 consecutive columns (d is a multiple of 8).
 template <typename T>
 __global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
                                                    const int64_t* __restrict__ y,
@@ -614,13 +684,18 @@ __global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
   const int b = offsets[v], e = offsets[v + 1];
   if (p != b) return;
   float* o = dW + v * d;
-  for (int64_t k = threadIdx.x; k < d; k += blockDim.x) {
-    float s = 0.0f;
+  for (int64_t k = int64_t(threadIdx.x) * 4; k < d; k += 4 * int64_t(blockDim.x)) {
+    f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int q = b; q < e; ++q) {
       const int t = sorted[q];
-      s += dlogp[t] * float(H[int64_t(t) * d + k]);
+      const float g = dlogp[t];
+      const T* h = H + int64_t(t) * d + k;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) s[c] += g * float(h[c]);
     }
-    o[k] += s;
+    f32x4 cur = *reinterpret_cast<const f32x4*>(o + k);
+    cur += s;
+    *reinterpret_cast<f32x4*>(o + k) = cur;
   }
 }
 
@@ -689,8 +764,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B,
 }
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand B, int64_t K,
-                                                             int nTm, int nTn, EpiStore epi) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiStore::kLdsExtra];
+                                                             int nTm, int nTn, EpiDH<T> epi) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiDH<T>::kLdsExtra];
   gemm_body<T, Lay::TileTK, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
 }
 template <typename T>
@@ -766,6 +841,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   int* offsets = cv.take<int>(Vs + 1);
   int* unsorted = cv.take<int>(Tn);
   int* sorted = cv.take<int>(Tn);
+  int* scan_sums = cv.take<int>(cdiv(Vs, kScanBlock));
   const int nTm = int(cdiv(Tn, kBM));
   const int nTd = int(cdiv(d, kBN));
 
@@ -776,7 +852,9 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
     hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, counts, Vs, 0);
     hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, cursor, Vs, 0);
     hipLaunchKernelGGL(k_hist, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, counts);
-    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, counts, Vs, offsets);
+    const int nsb = int(cdiv(Vs, kScanBlock));
+    hipLaunchKernelGGL(k_scan_sums, dim3(nsb), dim3(256), 0, s, counts, Vs, scan_sums);
+    hipLaunchKernelGGL(k_scan_apply, dim3(nsb), dim3(256), 0, s, counts, Vs, scan_sums, offsets);
     hipLaunchKernelGGL(k_bucket_fill, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, offsets,
                        cursor, unsorted);
     hipLaunchKernelGGL(k_bucket_rank, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, offsets,
@@ -823,10 +901,14 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
           !operand_in_bounds<T, Lay::KMajor>(B, size_t(d) * ldc * sizeof(T)) ||
           width > ldc || size_t(d) * ldc > size_t(d) * ld)
         return hipErrorInvalidValue;
-      EpiStore epi{dH, d, Tn, d, (v0 > 0 || (flags & MC_BWD_ACCUMULATE_DHIDDEN)) ? 1 : 0};
-      ProfScope ps_(s, "logprob_bwd_dhidden", 2.0 * Tn * d * width,
+      // the one-hot part goes into the last chunk's epilogue
+      const bool last = v0 + chunk >= Vs;
+      EpiDH<T> epi{dH,      d,     Tn,    d, (v0 > 0 || (flags & MC_BWD_ACCUMULATE_DHIDDEN)) ? 1 : 0,
+                   last ? W : nullptr, y, dlogp, v_off, Vs};
+      ProfScope ps_(s, "logprob_bwd_dhidden", 2.0 * Tn * d * (width + (last ? 1 : 0)),
                     es * (double(Tn) * width + double(width) * d) +
-                        4.0 * Tn * d * (epi.accumulate ? 2 : 1));
+                        4.0 * Tn * d * (epi.accumulate ? 2 : 1) +
+                        (last ? es * double(Tn) * d + 16.0 * Tn : 0.0));
       hipLaunchKernelGGL(k_bwd_dhidden<T>, dim3(nTm * nTd),
                          dim3(kThreads), 0, s, A, B, ldc, nTm, nTd, epi);
     }
@@ -850,11 +932,6 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       hipLaunchKernelGGL(k_bwd_dweight<T>, dim3(nTv * nTd),
                          dim3(kThreads), 0, s, A, B, Tn, nTv, nTd, epi);
     }
-  }
-  if (dH) {
-    ProfScope ps_(s, "logprob_bwd_onehot_dh", 2.0 * Tn * d, (es + 8.0) * Tn * d);
-    hipLaunchKernelGGL(k_onehot_dh<T>, dim3(Tn), dim3(256), 0, s, W, y, dlogp, d, v_off, Vs,
-                       dH);
   }
   if (dW) {
     ProfScope ps_(s, "logprob_bwd_onehot_dw", 2.0 * Tn * d, (es + 8.0) * Tn * d);
@@ -896,6 +973,7 @@ size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += 2 * align_up(size_t(V) * 4, kWsAlign);
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
+  n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
   return n;
 }
 
@@ -910,6 +988,7 @@ size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += 2 * align_up(size_t(V) * 4, kWsAlign);
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
+  n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
   return n;
 }
 
