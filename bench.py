@@ -38,18 +38,17 @@ PEAK_FP32_TFLOPS = 157.3
 # the kernel sources with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "b739e88bf9bae41e05fd7630f48e30c83a6618bf8530d600a66eb44fd008e732",
+        "f60e48940d05962acaf94e7d2cbb3afac4944f6315244ccdd3cdc10a67c9ae5b",
     "bytes_per_launch": {
-        "logprob_fwd_gemm": 38159103966,
-        "logprob_fwd_merge": 78265908,
+        "logprob_fwd_gemm": 38038229284,
+        "logprob_fwd_merge": 78265871,
         "rl_loss": 91896,
-        "logprob_bwd_bucket": 1436900,
-        "logprob_bwd_cache_probs": 10035310241,
-        "logprob_bwd_transpose": 1905338247,
-        "logprob_bwd_dhidden": 30224290064,
-        "logprob_bwd_dweight": 38750683180,
-        "logprob_bwd_onehot_dh": 674107502,
-        "logprob_bwd_onehot_dw": 650862578,
+        "logprob_bwd_bucket": 1326304,
+        "logprob_bwd_cache_probs": 10035307830,
+        "logprob_bwd_transpose": 1903662430,
+        "logprob_bwd_dhidden": 30277491461,
+        "logprob_bwd_dweight": 38238026882,
+        "logprob_bwd_onehot_dw": 650866485,
     },
 }
 
