@@ -1,7 +1,9 @@
 // Fused LM-head log-prob on gfx950: forward (GEMM + online log-sum-exp +
-// target gather in the epilogue), the partial merge, and the backward
-// (recomputed logits -> scaled softmax operand -> two contractions, plus the
-// exact one-hot terms in fp32).
+// target gather in the epilogue, optionally keeping a softmax cache), the
+// partial merge, and the backward: the scaled softmax operand (from the cache,
+// normalised in place, or from recomputed logits) -> two contractions, plus
+// the exact one-hot terms in fp32 (dH's in its contraction's epilogue, dW's
+// by a deterministic bucketed scatter).
 #include <hip/hip_runtime.h>
 
 #include "mc_internal.hpp"
