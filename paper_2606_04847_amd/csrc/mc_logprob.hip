@@ -490,6 +490,46 @@ struct EpiDH {
   }
 };
 
+// The same for a tile whose rows are C's columns and whose columns are C's
+// rows (C[c, r] = tile[r, c], C is [cols x ldc]): each lane's four
+// consecutive tile rows are 16 contiguous bytes of one row of C.
+struct EpiStoreT {
+  float* C;
+  int64_t ldc, rows, cols;
+  int accumulate;
+  static constexpr int kLdsExtra = 16;
+
+  __device__ void prologue(int64_t, int64_t, char*) const {}
+  __device__ __forceinline__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char*,
+                                          char*) const {
+    const int lane = threadIdx.x & 63;
+    const int wm = wave_m(), wn = wave_n();
+#pragma unroll
+    for (int j = 0; j < kTN; ++j) {
+      const int64_t c = n0 + acc_col(wn, j, lane);
+      if (c >= cols) continue;
+      float* crow = C + c * ldc;
+#pragma unroll
+      for (int i = 0; i < kTM; ++i) {
+        const int64_t r = m0 + acc_row(wm, i, 0, lane);   // rows r .. r + 3
+        if (r + 4 <= rows) {   // ldc and r are multiples of 4: 16-byte aligned
+          f32x4 v = acc[i][j];
+          if (accumulate) v += *reinterpret_cast<const f32x4*>(crow + r);
+          *reinterpret_cast<f32x4*>(crow + r) = v;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (r + e >= rows) continue;
+            float v = acc[i][j][e];
+            if (accumulate) v += crow[r + e];
+            crow[r + e] = v;
+          }
+        }
+      }
+    }
+  }
+};
+
 // Plain fp32 store (or accumulate) of the tile into C[rows x cols], ld = ldc.
 struct EpiStore {
   float* C;
@@ -770,11 +810,19 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand 
   __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiDH<T>::kLdsExtra];
   gemm_body<T, Lay::TileTK, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
 }
+// dW^T = H^T P~ : tile rows are hidden dimensions (A = H^T, along the
+// tokens), tile columns vocabulary entries (B = the operand panels read
+// across, with the transposing LDS read on the operand with fewer blocks per
+// wave), stored transposed into dW.
+// Tiles of 4 hidden-dimension rows walk the vocabulary together: the 32
+// workgroups of an XCD then share 4 H^T and 8 operand panels (measured best
+// of 1, 2, 4, 8 at the headline shape).
+constexpr int kGroupDW = 4;
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand B, int64_t K,
-                                                             int nTm, int nTn, EpiStore epi) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiStore::kLdsExtra];
-  gemm_body<T, Lay::TileVT, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
+                                                             int nTm, int nTn, EpiStoreT epi) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiStoreT::kLdsExtra];
+  gemm_body<T, Lay::KMajor, Lay::TileVT>(A, B, K, nTm, nTn, epi, lds, kGroupDW);
 }
 
 // Forward over a vocabulary shard [v_off, v_off + Vs) of a V-entry vocabulary
@@ -915,24 +963,24 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                          dim3(kThreads), 0, s, A, B, ldc, nTm, nTd, epi);
     }
     if (dW) {
-      // dW[chunk] (+)= P~^T H : M = chunk columns, N = d, K = T, with H^T
-      // [d x pld] (made once) so that the N operand runs along K
+      // dW[chunk]^T (+)= H^T P~ : M = d, N = chunk columns, K = T, with H^T
+      // [d x pld] (made once) so that the M operand runs along K
       if (v0 == 0) {
         ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(Tn) * d);
         hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(Tn, 64), cdiv(d, 64)), dim3(256), 0, s,
                            H, Tn, d, d, Ht, pld);
       }
-      Operand A{P, pld, ldc, Tn}, B{Ht, pld, d, Tn};   // pld = 64 ceil(Tn / 64)
-      if (!operand_in_bounds<T, Lay::TileVT>(A, p_bytes) ||
-          !operand_in_bounds<T, Lay::KMajor>(B, size_t(d) * pld * sizeof(T)))
+      Operand A{Ht, pld, d, Tn}, B{P, pld, ldc, Tn};   // pld = 64 ceil(Tn / 64)
+      if (!operand_in_bounds<T, Lay::KMajor>(A, size_t(d) * pld * sizeof(T)) ||
+          !operand_in_bounds<T, Lay::TileVT>(B, p_bytes))
         return hipErrorInvalidValue;
-      EpiStore epi{dW + v0 * d, d, width, d, (flags & MC_BWD_ACCUMULATE_DWEIGHT) ? 1 : 0};
+      EpiStoreT epi{dW + v0 * d, d, d, width, (flags & MC_BWD_ACCUMULATE_DWEIGHT) ? 1 : 0};
       const int nTv = int(cdiv(width, kBM));
       ProfScope ps_(s, "logprob_bwd_dweight", 2.0 * Tn * d * width,
                     es * (double(Tn) * width + double(Tn) * d) +
                         4.0 * width * d * (epi.accumulate ? 2 : 1));
-      hipLaunchKernelGGL(k_bwd_dweight<T>, dim3(nTv * nTd),
-                         dim3(kThreads), 0, s, A, B, Tn, nTv, nTd, epi);
+      hipLaunchKernelGGL(k_bwd_dweight<T>, dim3(nTd * nTv), dim3(kThreads), 0, s, A, B, Tn,
+                         nTd, nTv, epi);
     }
   }
   if (dW) {
