@@ -120,12 +120,13 @@ constexpr uint32_t kBufOut = 0x80000000u;     // an offset past the range: reads
 
 // Host-side check used before every launch: the last in-range chunk of the
 // operand (offsets grow with r and k in every layout) lies inside `bytes`,
-// and the per-thread 32-bit offsets of one tile cannot overflow.
+// the per-thread 32-bit offsets of one tile cannot overflow, and K fits the
+// copies' 32-bit K bounds.
 template <typename T, Lay L>
 inline bool operand_in_bounds(const Operand& op, size_t bytes) {
   using M = LayMath<T, L>;
   constexpr int64_t E = Elem<T>::kChunk;
-  if (op.rows < 1 || op.K < 1) return false;
+  if (op.rows < 1 || op.K < 1 || op.K > int64_t(0x7fffffff) - 2 * M::KT) return false;
   int64_t r = op.rows - 1, k = op.K - 1;
   if (KContig<L>::value) k = k / E * E; else r = r / E * E;
   const int64_t last = M::tile_base(op, r / 256 * 256) + (k / M::KT) * M::stage_step(op) +
@@ -514,19 +515,19 @@ template <typename T, Lay L, bool kAsm> struct DmaCopy {
   static constexpr int NI = kBM / 8 / kWaves;   // 1 KiB groups per wave
   static_assert(8 * kWaves % 32 == 0, "group stride must keep the row swizzle");
   const char* tb;
-  int64_t step, K;
+  int64_t step;
   uint32_t off0, istride;
-  int kc;
+  int klim;   // K - (this lane's chunk column): the chunk of step kt is in range iff kt KT < klim
   uint32_t rowok;
   int grp;
   __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
     tb = static_cast<const char*>(op.ptr) + M::tile_base(op, r0);
     step = M::stage_step(op);
-    K = op.K;
     const int lane = tid & 63;
     grp = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int row = 8 * grp + (lane >> 3);
-    kc = ((lane & 7) ^ swz(row)) * E;
+    const int kc = ((lane & 7) ^ swz(row)) * E;
+    klim = int(op.K) - kc;
     off0 = M::rel(op, row, kc);
     istride = M::rel(op, row + 8 * kWaves, kc) - off0;
     rowok = 0;
@@ -535,7 +536,7 @@ template <typename T, Lay L, bool kAsm> struct DmaCopy {
       if (r0 + row + 8 * kWaves * i < op.rows) rowok |= 1u << i;
   }
   __device__ __forceinline__ void issue(int64_t kt, char* lds) const {
-    const bool kok = kt * M::KT + kc < K;
+    const bool kok = int(kt) * int(M::KT) < klim;
     if constexpr (kAsm) {
       const i32x4 rs = dma_rsrc(tb + kt * step);
       const uint32_t m0 = lds_addr(lds) + grp * 1024;
@@ -567,18 +568,18 @@ template <Lay L> struct DmaCopyMN {
   static constexpr int NI = kStageBytes / 1024 / kWaves;   // 1 KiB groups per wave
   static_assert(2 * kWaves % 16 == 0, "group stride must keep the K-row swizzle");
   const char* tb;
-  int64_t step, K;
+  int64_t step;
   uint32_t off0, istride;
-  int k0;
+  int klim;   // K - (this lane's first K row): group i of step kt is in range iff kt KT + 2 kWaves i < klim
   bool mok;
   int grp;
   __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
     tb = static_cast<const char*>(op.ptr) + M::tile_base(op, r0);
     step = M::stage_step(op);
-    K = op.K;
     const int lane = tid & 63;
     grp = __builtin_amdgcn_readfirstlane(tid >> 6);
-    k0 = 2 * grp + (lane >> 5);
+    const int k0 = 2 * grp + (lane >> 5);
+    klim = int(op.K) - k0;
     const int c = (lane & 31) ^ mn_swz(k0);
     off0 = M::rel(op, 8 * c, k0);
     istride = M::rel(op, 8 * c, k0 + 2 * kWaves) - off0;
@@ -589,7 +590,7 @@ template <Lay L> struct DmaCopyMN {
     const uint32_t m0 = lds_addr(lds) + grp * 1024;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const bool ok = mok && (kt * M::KT + k0 + 2 * kWaves * i < K);
+      const bool ok = mok && (int(kt) * int(M::KT) + 2 * kWaves * i < klim);
       dma16(rs, ok ? off0 + i * istride : kBufOut, m0 + i * kWaves * 1024);
     }
   }
