@@ -15,8 +15,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-// Integer min / clamp (the device min/max overloads of int64 go through fp64).
-__device__ __forceinline__ int64_t imin(int64_t a, int64_t b) { return a < b ? a : b; }
+// Integer clamp (the device min/max overloads of int64 go through fp64).
 __device__ __forceinline__ int clamp_rows(int64_t n, int hi) {
   return n <= 0 ? 0 : (n >= hi ? hi : int(n));
 }
@@ -490,9 +489,9 @@ struct EpiDH {
   }
 };
 
-// The same for a tile whose rows are C's columns and whose columns are C's
-// rows (C[c, r] = tile[r, c], C is [cols x ldc]): each lane's four
-// consecutive tile rows are 16 contiguous bytes of one row of C.
+// fp32 store (or accumulate) of a tile whose rows are C's columns and whose
+// columns are C's rows (C[c, r] = tile[r, c], C is [cols x ldc]): each lane's
+// four consecutive tile rows are 16 contiguous bytes of one row of C.
 struct EpiStoreT {
   float* C;
   int64_t ldc, rows, cols;
@@ -523,38 +522,6 @@ struct EpiStoreT {
             float v = acc[i][j][e];
             if (accumulate) v += crow[r + e];
             crow[r + e] = v;
-          }
-        }
-      }
-    }
-  }
-};
-
-// Plain fp32 store (or accumulate) of the tile into C[rows x cols], ld = ldc.
-struct EpiStore {
-  float* C;
-  int64_t ldc, rows, cols;
-  int accumulate;
-  static constexpr int kLdsExtra = 16;
-
-  __device__ void prologue(int64_t, int64_t, char*) const {}
-  __device__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char*, char*) const {
-    const int lane = threadIdx.x & 63;
-    const int wm = wave_m(), wn = wave_n();
-#pragma unroll
-    for (int i = 0; i < kTM; ++i) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t r = m0 + acc_row(wm, i, e, lane);
-        if (r >= rows) continue;
-        float* crow = C + r * ldc;
-#pragma unroll
-        for (int j = 0; j < kTN; ++j) {
-          const int64_t c = n0 + acc_col(wn, j, lane);
-          if (c < cols) {
-            float v = acc[i][j][e];
-            if (accumulate) v += crow[c];
-            crow[c] = v;
           }
         }
       }
@@ -796,7 +763,7 @@ template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_fwd_logits_lse(Operand A, Operand B, int64_t K,
                                                                 int nTm, int nTn, EpiFwd<T> epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiFwd<T>::kLdsExtra];
-  gemm_body<T, Lay::KMajor, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
+  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiFwd<T>, 2>(A, B, K, nTm, nTn, epi, lds);
 }
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B, int64_t K,

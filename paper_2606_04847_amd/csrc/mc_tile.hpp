@@ -624,7 +624,10 @@ __device__ __forceinline__ void dma_wait_barrier() {
 //   stage k+1 | MFMAs of sub-step 1 of stage k
 // so the MFMAs after the barrier already have their fragments in registers
 // while the next stage's first reads are in flight.
-template <typename T, Lay LA, Lay LB>
+// kSpread: MFMAs between consecutive copy issues after the barrier of the
+// two-K-contiguous-operand loop (1 suits the backward's contractions, 2 the
+// forward's: measured).
+template <typename T, Lay LA, Lay LB, int kSpread = 1>
 __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operand& B, int64_t m0,
                                                   int64_t n0, int64_t K, char* lds, Acc& acc) {
   constexpr int KT = kRowBytes / sizeof(T);
@@ -724,17 +727,19 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     cb.issue(kt + 2, cur + kStageBytes);
     read_frags<T, SA, SB>(a0, b0, nxt, nxt + kStageBytes, wm, wn, lane, 0);
     Mfma<T>::step(acc, a1, b1);
+    static_assert(kSpread * (CA::NI + CB::NI) + kTM + kTN <= kTM * kTN, "issue slots");
 #pragma unroll
     for (int r = 0; r < CA::NI + CB::NI; ++r) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // copy issue
+      __builtin_amdgcn_sched_group_barrier(0x008, kSpread, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);         // copy issue
     }
 #pragma unroll
     for (int r = 0; r < kTM + kTN; ++r) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, kTM * kTN - (CA::NI + CB::NI) - (kTM + kTN), 0);
+    __builtin_amdgcn_sched_group_barrier(
+        0x008, kTM * kTN - kSpread * (CA::NI + CB::NI) - (kTM + kTN), 0);
   }
   // the zero-filling copies issued by the last two steps land before the
   // LDS is reused
@@ -790,11 +795,11 @@ __device__ __forceinline__ void gemm_mainloop_reg(const Operand& A, const Operan
 // Full K loop for the tile at (m0, n0).  `lds` holds kLdsGemm bytes.  bf16,
 // or fp32 with both operands K-contiguous: direct copies; otherwise (fp32
 // M/N-contiguous operands) register-staged copies.
-template <typename T, Lay LA, Lay LB>
+template <typename T, Lay LA, Lay LB, int kSpread = 1>
 __device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B, int64_t m0,
                                               int64_t n0, int64_t K, char* lds, Acc& acc) {
   if constexpr ((KContig<LA>::value && KContig<LB>::value) || sizeof(T) == 2)
-    gemm_mainloop_dma<T, LA, LB>(A, B, m0, n0, K, lds, acc);
+    gemm_mainloop_dma<T, LA, LB, kSpread>(A, B, m0, n0, K, lds, acc);
   else
     gemm_mainloop_reg<T, LA, LB>(A, B, m0, n0, K, lds, acc);
 }
@@ -814,7 +819,7 @@ __device__ __forceinline__ int acc_col(int wn, int j, int lane) {
 // extra) to stage per-row data into `extra` LDS before the loop and
 // epilogue(acc, tm, tn, m0, n0, lds, extra) after it.  Each use is wrapped in
 // a __global__ function of its own name (so profiles name the role).
-template <typename T, Lay LA, Lay LB, class Epi>
+template <typename T, Lay LA, Lay LB, class Epi, int kSpread = 1>
 __device__ __forceinline__ void gemm_body(const Operand& A, const Operand& B, int64_t K, int nTm,
                                           int nTn, const Epi& epi, char* lds,
                                           int group_m = kGroupM) {
@@ -824,7 +829,7 @@ __device__ __forceinline__ void gemm_body(const Operand& A, const Operand& B, in
   char* extra = lds + kLdsGemm;
   epi.prologue(m0, n0, extra);
   Acc acc;
-  gemm_mainloop<T, LA, LB>(A, B, m0, n0, K, lds, acc);
+  gemm_mainloop<T, LA, LB, kSpread>(A, B, m0, n0, K, lds, acc);
   epi.epilogue(acc, tm, tn, m0, n0, lds, extra);
 }
 
