@@ -785,11 +785,63 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand 
 // workgroups of an XCD then share 4 H^T and 8 operand panels (measured best
 // of 1, 2, 4, 8 at the headline shape).
 constexpr int kGroupDW = 4;
+// Workgroups past ts.full compute K slices of the last ts.rem tiles into
+// 256 x 256 fp32 slots (stored [column][row]) for k_tail_reduce.
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand B, int64_t K,
-                                                             int nTm, int nTn, EpiStoreT epi) {
+                                                             int nTm, int nTn, EpiStoreT epi,
+                                                             TailSplit ts, float* slots) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiStoreT::kLdsExtra];
-  gemm_body<T, Lay::KMajor, Lay::TileVT>(A, B, K, nTm, nTn, epi, lds, kGroupDW);
+  const int bid = blockIdx.x;
+  int tm, tn, j = -1;
+  Operand a = A, b = B;
+  int64_t k = K;
+  if (bid < ts.full) {
+    tile_of(bid, nTm, nTn, kGroupDW, tm, tn, ts.full);
+  } else {
+    j = bid - ts.full;
+    tile_of_logical(ts.full + j / ts.splits, nTm, nTn, kGroupDW, tm, tn);
+    const int64_t k0 = int64_t(j % ts.splits) * ts.ks;
+    k = K - k0 < ts.ks ? K - k0 : ts.ks;
+    a = k_slice<T, Lay::KMajor>(A, k0, k);
+    b = k_slice<T, Lay::TileVT>(B, k0, k);
+  }
+  const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
+  Acc acc;
+  gemm_mainloop<T, Lay::KMajor, Lay::TileVT>(a, b, m0, n0, k, lds, acc);
+  if (j < 0) {
+    epi.epilogue(acc, tm, tn, m0, n0, lds, nullptr);
+  } else {
+    const EpiStoreT slot{slots + int64_t(j) * (kBM * kBN), kBM, kBM, kBN, 0};
+    slot.epilogue(acc, tm, tn, 0, 0, lds, nullptr);
+  }
+}
+
+// dW[n0 + c, m0 + r] (+)= sum over the splits, in split order, of
+// slot[c][r] for each split tile (grid x: tiles, y: groups of 4 columns;
+// thread: 4 consecutive rows of one column).
+__global__ __launch_bounds__(256) void k_tail_reduce(const float* __restrict__ slots,
+                                                     TailSplit ts, int nTm, int nTn,
+                                                     float* __restrict__ C, int64_t ldc,
+                                                     int64_t rows, int64_t cols, int accumulate) {
+  int tm, tn;
+  tile_of_logical(ts.full + int(blockIdx.x), nTm, nTn, kGroupDW, tm, tn);
+  const int cl = int(blockIdx.y) * 4 + (threadIdx.x >> 6), rl = (threadIdx.x & 63) * 4;
+  const int64_t c = int64_t(tn) * kBN + cl, r = int64_t(tm) * kBM + rl;
+  if (c >= cols || r >= rows) return;   // rows, ldc and r are multiples of 4
+  const float* src = slots + int64_t(blockIdx.x) * ts.splits * (kBM * kBN) + cl * kBM + rl;
+  f32x4 v = *reinterpret_cast<const f32x4*>(src);
+  for (int q = 1; q < ts.splits; ++q) v += *reinterpret_cast<const f32x4*>(src + q * (kBM * kBN));
+  f32x4* o = reinterpret_cast<f32x4*>(C + c * ldc + r);
+  if (accumulate) v += *o;
+  *o = v;
+}
+
+// Slot floats the tail split of one dW launch over `width` vocabulary columns
+// can use: at most 8 splits of each of its tiles, and at most kTailSlots.
+size_t tail_slot_floats(int64_t d, int64_t width) {
+  const int64_t tiles = cdiv(d, int64_t(kBM)) * cdiv(width, int64_t(kBN));
+  return size_t(std::min<int64_t>(kTailSlots, 8 * tiles)) * kBM * kBN;
 }
 
 // Forward over a vocabulary shard [v_off, v_off + Vs) of a V-entry vocabulary
@@ -859,6 +911,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   int* unsorted = cv.take<int>(Tn);
   int* sorted = cv.take<int>(Tn);
   int* scan_sums = cv.take<int>(cdiv(Vs, kScanBlock));
+  float* slots = cv.take<float>(tail_slot_floats(d, min(chunk, Vs)));
+  int ncu = 0, dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    ncu = 0;   // no tail split
   const int nTm = int(cdiv(Tn, kBM));
   const int nTd = int(cdiv(d, kBN));
 
@@ -946,8 +1003,12 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       ProfScope ps_(s, "logprob_bwd_dweight", 2.0 * Tn * d * width,
                     es * (double(Tn) * width + double(Tn) * d) +
                         4.0 * width * d * (epi.accumulate ? 2 : 1));
-      hipLaunchKernelGGL(k_bwd_dweight<T>, dim3(nTd * nTv), dim3(kThreads), 0, s, A, B, Tn,
-                         nTd, nTv, epi);
+      const TailSplit ts = plan_tail(nTd * nTv, Tn, ncu);
+      hipLaunchKernelGGL(k_bwd_dweight<T>, dim3(ts.full + ts.rem * ts.splits), dim3(kThreads), 0,
+                         s, A, B, Tn, nTd, nTv, epi, ts, slots);
+      if (ts.rem > 0)
+        hipLaunchKernelGGL(k_tail_reduce, dim3(ts.rem, kBN / 4), dim3(256), 0, s, slots, ts, nTd,
+                           nTv, epi.C, epi.ldc, epi.rows, epi.cols, epi.accumulate);
     }
   }
   if (dW) {
@@ -991,6 +1052,7 @@ size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
   n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
+  n += align_up(tail_slot_floats(d, V) * 4, kWsAlign);
   return n;
 }
 
@@ -1006,6 +1068,7 @@ size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
   n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
+  n += align_up(tail_slot_floats(d, std::min(chunk, V)) * 4, kWsAlign);
   return n;
 }
 

@@ -20,6 +20,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 namespace mc {
 
 typedef __bf16 bf16_t;
@@ -146,12 +148,10 @@ __device__ __forceinline__ int lds_off(int r, int c) {
 // regrouped so that each XCD receives a contiguous run of logical tiles; the
 // logical order walks group_m tile rows before moving to the next tile column,
 // so the 32 workgroups resident on one XCD share a few operand panels in its L2.
-__device__ __forceinline__ void tile_of(int bid, int nTm, int nTn, int group_m, int& tm,
-                                        int& tn) {
-  const int total = nTm * nTn;
-  const int q = total / kXcds;
-  int L = bid;
-  if (bid < q * kXcds) L = (bid % kXcds) * q + bid / kXcds;
+// With `count` < nTm nTn only the first `count` logical tiles are regrouped
+// and handed out (the rest are covered by another launch shape).
+__device__ __forceinline__ void tile_of_logical(int L, int nTm, int nTn, int group_m, int& tm,
+                                                int& tn) {
   const int group = group_m * nTn;
   const int g = L / group;
   const int first = g * group_m;
@@ -159,6 +159,59 @@ __device__ __forceinline__ void tile_of(int bid, int nTm, int nTn, int group_m, 
   const int r = L - g * group;
   tm = first + r % gm;
   tn = r / gm;
+}
+__device__ __forceinline__ void tile_of(int bid, int nTm, int nTn, int group_m, int& tm, int& tn,
+                                        int count = -1) {
+  const int total = count < 0 ? nTm * nTn : count;
+  const int q = total / kXcds;
+  int L = bid;
+  if (bid < q * kXcds) L = (bid % kXcds) * q + bid / kXcds;
+  tile_of_logical(L, nTm, nTn, group_m, tm, tn);
+}
+
+// The operand restricted to K columns [k0, k0 + len): k0 is a multiple of the
+// stage depth, so the slice starts at a stage boundary of every layout.
+template <typename T, Lay L>
+__host__ __device__ inline Operand k_slice(const Operand& op, int64_t k0, int64_t len) {
+  using M = LayMath<T, L>;
+  Operand o = op;
+  o.ptr = static_cast<const char*>(op.ptr) + (k0 / M::KT) * M::stage_step(op);
+  o.K = len;
+  return o;
+}
+
+// Tail split: when the last round of tiles fills at most half of the CUs,
+// its `rem` tiles are each split into `splits` K ranges of `ks` columns
+// (whole stages), computed by rem * splits workgroups into fp32 slots and
+// summed in split order by a second kernel.  full = the tiles computed
+// whole.  At most kTailSlots slots.
+constexpr int kTailSlots = 256;
+struct TailSplit {
+  int full, rem, splits;
+  int64_t ks;
+};
+inline TailSplit plan_tail(int total, int64_t K, int ncu) {
+  constexpr int64_t kStage = 64;   // K columns of one bf16 stage (32 for fp32; a multiple works)
+  TailSplit t{total, 0, 1, K};
+  if (ncu <= 0) return t;
+  const int rem = total % ncu;
+  if (rem == 0 || 2 * rem > ncu) return t;
+  int splits = 1;
+  while (splits < 8 && rem * splits * 2 <= std::min(ncu, kTailSlots) &&
+         K >= int64_t(splits) * 2 * 4 * kStage)
+    splits *= 2;
+  const int64_t nst = (K + kStage - 1) / kStage;
+  int64_t ks = (nst + splits - 1) / splits * kStage;
+  while (splits > 1 && int64_t(splits - 1) * ks >= K) {   // every split non-empty
+    splits /= 2;
+    ks = (nst + splits - 1) / splits * kStage;
+  }
+  if (splits == 1) return t;
+  t.full = total - rem;
+  t.rem = rem;
+  t.splits = splits;
+  t.ks = ks;
+  return t;
 }
 
 // ---------------------------------------------------------------------------
