@@ -38,17 +38,17 @@ PEAK_FP32_TFLOPS = 157.3
 # the kernel sources with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "f60e48940d05962acaf94e7d2cbb3afac4944f6315244ccdd3cdc10a67c9ae5b",
+        "24e224c652a9905c853b3a8f0a190701065db4ffd7349b4c0ac98ec4f2225487",
     "bytes_per_launch": {
-        "logprob_fwd_gemm": 38038229284,
-        "logprob_fwd_merge": 78265871,
+        "logprob_fwd_gemm": 37542538879,
+        "logprob_fwd_merge": 78254620,
         "rl_loss": 91896,
-        "logprob_bwd_bucket": 1326304,
-        "logprob_bwd_cache_probs": 10035307830,
-        "logprob_bwd_transpose": 1903662430,
-        "logprob_bwd_dhidden": 30277491461,
-        "logprob_bwd_dweight": 38238026882,
-        "logprob_bwd_onehot_dw": 650866485,
+        "logprob_bwd_bucket": 1328755,
+        "logprob_bwd_cache_probs": 10035308762,
+        "logprob_bwd_transpose": 1911273197,
+        "logprob_bwd_dhidden": 30277024436,
+        "logprob_bwd_dweight": 32717267249,
+        "logprob_bwd_onehot_dw": 650840181,
     },
 }
 

@@ -706,10 +706,12 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
   cb.init(B, n0, tid);
   ca.issue(0, lds);
   cb.issue(0, lds + kStageBytes);
-  if constexpr (kAsm) {
-    // A transposing-read operand needs per-block fragment addresses; without
-    // the spare registers for the cross-barrier prefetch, one barrier at the
-    // top of each step: it publishes step k and releases step k-1's buffer.
+  if constexpr (SA == Stg::MN) {
+    // A transposing-read A operand needs per-block fragment addresses for its
+    // kTM blocks; without the spare registers for the cross-barrier
+    // prefetch, one barrier at the top of each step: it publishes step k and
+    // releases step k-1's buffer.  (With the transposing reads on B, kTN
+    // blocks, the cross-barrier loop below fits and is faster.)
     constexpr int kReads = (SA == Stg::MN ? 2 : 1) * kTM + (SB == Stg::MN ? 2 : 1) * kTN;
     for (int64_t kt = 0; kt < nk; ++kt) {
       char* cur = lds + (kt & 1) * (2 * kStageBytes);
