@@ -759,17 +759,21 @@ __global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
   }
 }
 
+// Vocabulary x token contractions (forward, softmax): tiles of 4 vocabulary
+// rows walk the tokens together (0.4 ms faster than 8 for the forward at the
+// headline shape; the backward's dH keeps 8).
+constexpr int kGroupVT = 4;
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_fwd_logits_lse(Operand A, Operand B, int64_t K,
                                                                 int nTm, int nTn, EpiFwd<T> epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiFwd<T>::kLdsExtra];
-  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiFwd<T>, 2>(A, B, K, nTm, nTn, epi, lds);
+  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiFwd<T>, 2>(A, B, K, nTm, nTn, epi, lds, kGroupVT);
 }
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B, int64_t K,
                                                            int nTm, int nTn, EpiProbs<T> epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiProbs<T>::kLdsExtra];
-  gemm_body<T, Lay::KMajor, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
+  gemm_body<T, Lay::KMajor, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds, kGroupVT);
 }
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand B, int64_t K,
