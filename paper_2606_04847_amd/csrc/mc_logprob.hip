@@ -106,20 +106,27 @@ struct EpiFwd {
   T* E;                   // softmax cache: panels [ldE / BV][pld][BV], or null
   float* cm;              // [2 nTv][Tn] block maxima (with E)
   int64_t pld, ldE;       // padded token count, padded vocabulary width
-  static constexpr int kLdsExtra = 256 * 4 + 3 * kWavesM * 256 * 4;
+  static constexpr int kLdsExtra = 3 * kWavesM * 256 * 4;
   static constexpr int64_t kPanel = 128 / sizeof(T);
 
-  __device__ void prologue(int64_t, int64_t n0, char* extra) const {
-    int* ys = reinterpret_cast<int*>(extra);
-    for (int i = threadIdx.x; i < kBN; i += kThreads) {
-      const int64_t t = n0 + i;
-      int v = -1;
+  // this lane's targets (shard-local, -1 outside the shard) of its kTN
+  // token columns
+  struct Pre {
+    int y[kTN];
+  };
+  __device__ __forceinline__ Pre prologue(int64_t, int64_t n0) const {
+    Pre p;
+    const int lane = threadIdx.x & 63, wn = wave_n();
+#pragma unroll
+    for (int j = 0; j < kTN; ++j) {
+      const int64_t t = n0 + wn * kWaveCols + j * 16 + (lane & 15);
+      p.y[j] = -1;
       if (t < Tn) {
         const int64_t yl = y[t] - v_off;
-        if (yl >= 0 && yl < Vs) v = int(yl);
+        if (yl >= 0 && yl < Vs) p.y[j] = int(yl);
       }
-      ys[i] = v;
     }
+    return p;
   }
 
   // max / sum exp / sum exp z of block column j over this lane's rows; kFull:
@@ -170,12 +177,11 @@ struct EpiFwd {
     if (with_u) u = quad_sum(u);
   }
 
-  __device__ void epilogue(Acc& acc, int tm, int, int64_t m0, int64_t n0, char* lds,
-                           char* extra) const {
+  __device__ __forceinline__ void epilogue(Acc& acc, int tm, int, int64_t m0, int64_t n0,
+                                          char* lds, char* extra, const Pre& pre) const {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wm = wave_m(), wn = wave_n();
-    const int* ys = reinterpret_cast<const int*>(extra);
-    float* red = reinterpret_cast<float*>(extra + 1024);   // [m|s|u][wm][token]
+    float* red = reinterpret_cast<float*>(extra);   // [m|s|u][wm][token]
     const int64_t rbase = m0 + wm * kWaveRows;              // first vocab row of this wave
     const int vlim = clamp_rows(Vs - rbase, kWaveRows);
     const bool with_u = part_u != nullptr;
@@ -197,7 +203,7 @@ struct EpiFwd {
           column<false, false>(acc, j, vlim, lane, with_u, mx, s, u, lds, wm, tl, m0, t);
       }
       // target logit: row yw of this wave, held by the lane of group (yw >> 2) & 3
-      const int yw = ys[tl] - int(rbase);
+      const int yw = pre.y[j] - int(rbase);
       if (yw >= 0 && yw < kWaveRows && ((yw >> 2) & 3) == (lane >> 4)) {
         const int ii = yw >> 4, ee = yw & 3;
         float z = 0.0f;
@@ -362,36 +368,42 @@ struct EpiProbs {
                                    // width; pld: padded token count
   T* P;                            // panel layout (see Lay::TileTK)
   static constexpr int64_t kPanel = 128 / sizeof(T);
-  static constexpr int kLdsExtra = 2 * 256 * 4;
+  static constexpr int kLdsExtra = 0;
 
-  __device__ void prologue(int64_t, int64_t n0, char* extra) const {
-    float* l2 = reinterpret_cast<float*>(extra);
-    float* g = l2 + 256;
-    for (int i = threadIdx.x; i < kBN; i += kThreads) {
-      const int64_t t = n0 + i;
-      float a = 0.0f, b = 0.0f;
+  // lse_t log2(e) and -dlogp_t (0 for ignored tokens) of this lane's kTN
+  // token columns
+  struct Pre {
+    float l2[kTN], g[kTN];
+  };
+  __device__ __forceinline__ Pre prologue(int64_t, int64_t n0) const {
+    Pre p;
+    const int lane = threadIdx.x & 63, wn = wave_n();
+#pragma unroll
+    for (int j = 0; j < kTN; ++j) {
+      const int64_t t = n0 + wn * kWaveCols + j * 16 + (lane & 15);
+      p.l2[j] = 0.0f;
+      p.g[j] = 0.0f;
       if (t < Tn) {
         const int64_t yy = y[t];
-        a = lse[t] * kLog2e;
-        b = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
+        p.l2[j] = lse[t] * kLog2e;
+        p.g[j] = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
       }
-      l2[i] = a;
-      g[i] = b;
     }
+    return p;
   }
 
   // P~ of this lane's elements.  vlim: valid rows (v < width) of the wave,
   // llim: rows below ld (a multiple of 4); kFull: all kWaveRows rows valid.
   template <bool kFull>
   __device__ __forceinline__ void values(const Acc& acc, char* lds, int lane, int wm, int wn,
-                                         const float* l2, const float* g, int vlim, int llim,
-                                         int64_t m0, int64_t n0) const {
+                                         const Pre& pre, int vlim, int llim, int64_t m0,
+                                         int64_t n0) const {
 #pragma unroll
     for (int j = 0; j < kTN; ++j) {
       const int tl = wn * kWaveCols + j * 16 + (lane & 15);
       const int64_t t = n0 + tl;
       if (t >= Tn) continue;
-      const float lb = l2[tl], gs = g[tl];
+      const float lb = pre.l2[j], gs = pre.g[j];
 #pragma unroll
       for (int i = 0; i < kTM; ++i) {
         {
@@ -418,19 +430,17 @@ struct EpiProbs {
     }
   }
 
-  __device__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char* lds,
-                           char* extra) const {
+  __device__ __forceinline__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0,
+                                          char* lds, char*, const Pre& pre) const {
     const int lane = threadIdx.x & 63;
     const int wm = wave_m(), wn = wave_n();
-    const float* l2 = reinterpret_cast<const float*>(extra);
-    const float* g = l2 + 256;
     const int64_t rb = m0 + wm * kWaveRows;
     const int vlim = clamp_rows(width - rb, kWaveRows);
     const int llim = clamp_rows(ld - rb, kWaveRows);
     if (vlim == kWaveRows)
-      values<true>(acc, lds, lane, wm, wn, l2, g, vlim, llim, m0, n0);
+      values<true>(acc, lds, lane, wm, wn, pre, vlim, llim, m0, n0);
     else
-      values<false>(acc, lds, lane, wm, wn, l2, g, vlim, llim, m0, n0);
+      values<false>(acc, lds, lane, wm, wn, pre, vlim, llim, m0, n0);
     if constexpr (sizeof(T) == 2) {
       __syncthreads();
       store_staged_panels(lds, P, m0, n0, Tn, ld, pld);
@@ -451,11 +461,12 @@ struct EpiDH {
   const int64_t* y;
   const float* dlogp;
   int64_t v_off, Vs;
-  static constexpr int kLdsExtra = 16;
+  static constexpr int kLdsExtra = 0;
 
-  __device__ void prologue(int64_t, int64_t, char*) const {}
+  struct Pre {};
+  __device__ __forceinline__ Pre prologue(int64_t, int64_t) const { return Pre{}; }
   __device__ __forceinline__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char*,
-                                          char*) const {
+                                          char*, const Pre& = Pre{}) const {
     const int lane = threadIdx.x & 63;
     const int wm = wave_m(), wn = wave_n();
 #pragma unroll
@@ -496,11 +507,12 @@ struct EpiStoreT {
   float* C;
   int64_t ldc, rows, cols;
   int accumulate;
-  static constexpr int kLdsExtra = 16;
+  static constexpr int kLdsExtra = 0;
 
-  __device__ void prologue(int64_t, int64_t, char*) const {}
+  struct Pre {};
+  __device__ __forceinline__ Pre prologue(int64_t, int64_t) const { return Pre{}; }
   __device__ __forceinline__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char*,
-                                          char*) const {
+                                          char*, const Pre& = Pre{}) const {
     const int lane = threadIdx.x & 63;
     const int wm = wave_m(), wn = wave_n();
 #pragma unroll
@@ -763,23 +775,30 @@ __global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
 // rows walk the tokens together (0.4 ms faster than 8 for the forward at the
 // headline shape; the backward's dH keeps 8).
 constexpr int kGroupVT = 4;
+// Which operand takes the 3-stage side of the loop's ring (measured).
+constexpr bool kDeepFwdA = true;    // forward / softmax: W (A) over H (B)
+constexpr bool kDeepDhA = true;     // dH: the operand panels (A) over W^T (B)
+constexpr bool kDeepDwA = false;    // dW^T: the operand panels (B) over H^T (A)
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_fwd_logits_lse(Operand A, Operand B, int64_t K,
                                                                 int nTm, int nTn, EpiFwd<T> epi) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiFwd<T>::kLdsExtra];
-  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiFwd<T>, 2>(A, B, K, nTm, nTn, epi, lds, kGroupVT);
+  static_assert(kLdsGemm + EpiFwd<T>::kLdsExtra <= kLdsRing, "epilogue LDS");
+  __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
+  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiFwd<T>, 2, kDeepFwdA>(A, B, K, nTm, nTn, epi, lds,
+                                                                  kGroupVT);
 }
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B, int64_t K,
                                                            int nTm, int nTn, EpiProbs<T> epi) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiProbs<T>::kLdsExtra];
-  gemm_body<T, Lay::KMajor, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds, kGroupVT);
+  __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
+  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiProbs<T>, 1, kDeepFwdA>(A, B, K, nTm, nTn, epi, lds,
+                                                                    kGroupVT);
 }
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand B, int64_t K,
                                                              int nTm, int nTn, EpiDH<T> epi) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiDH<T>::kLdsExtra];
-  gemm_body<T, Lay::TileTK, Lay::KMajor>(A, B, K, nTm, nTn, epi, lds);
+  __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
+  gemm_body<T, Lay::TileTK, Lay::KMajor, EpiDH<T>, 1, kDeepDhA>(A, B, K, nTm, nTn, epi, lds);
 }
 // dW^T = H^T P~ : tile rows are hidden dimensions (A = H^T, along the
 // tokens), tile columns vocabulary entries (B = the operand panels read
@@ -795,7 +814,7 @@ template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand B, int64_t K,
                                                              int nTm, int nTn, EpiStoreT epi,
                                                              TailSplit ts, float* slots) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsGemm + EpiStoreT::kLdsExtra];
+  __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
   const int bid = blockIdx.x;
   int tm, tn, j = -1;
   Operand a = A, b = B;
@@ -812,7 +831,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand 
   }
   const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
   Acc acc;
-  gemm_mainloop<T, Lay::KMajor, Lay::TileVT>(a, b, m0, n0, k, lds, acc);
+  gemm_mainloop<T, Lay::KMajor, Lay::TileVT, 1, kDeepDwA>(a, b, m0, n0, k, lds, acc);
   if (j < 0) {
     epi.epilogue(acc, tm, tn, m0, n0, lds, nullptr);
   } else {

@@ -50,6 +50,10 @@ constexpr int kTM = kWaveRows / 16;            // 16-row accumulator blocks per 
 constexpr int kTN = kWaveCols / 16;            // 16-column accumulator blocks per wave
 constexpr int kStageBytes = kBM * kRowBytes;   // 32 KiB per operand per stage
 constexpr int kLdsGemm = 4 * kStageBytes;      // 2 operands x 2 stages
+// The ring of the two-K-contiguous-operand loop: 3 stages of one operand and
+// 2 of the other, all of gfx950's 160 KiB.  Epilogues may use the bytes past
+// kLdsGemm once the loop is over.
+constexpr int kLdsRing = 5 * kStageBytes;
 constexpr int kGroupM = 8;                     // tile rows per scheduling group
 constexpr int kXcds = 8;                       // MI355X: 8 XCDs, workgroup i -> XCD i % 8
 
@@ -678,9 +682,9 @@ __device__ __forceinline__ void dma_wait_barrier() {
 // so the MFMAs after the barrier already have their fragments in registers
 // while the next stage's first reads are in flight.
 // kSpread: MFMAs between consecutive copy issues after the barrier of the
-// two-K-contiguous-operand loop (1 suits the backward's contractions, 2 the
-// forward's: measured).
-template <typename T, Lay LA, Lay LB, int kSpread = 1>
+// cross-barrier loop (1 suits dH, 2 the forward: measured).  kDeepA: operand
+// A gets the 3-stage side of the ring (else B).
+template <typename T, Lay LA, Lay LB, int kSpread = 1, bool kDeepA = true>
 __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operand& B, int64_t m0,
                                                   int64_t n0, int64_t K, char* lds, Acc& acc) {
   constexpr int KT = kRowBytes / sizeof(T);
@@ -704,9 +708,9 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
   CB cb;
   ca.init(A, m0, tid);
   cb.init(B, n0, tid);
-  ca.issue(0, lds);
-  cb.issue(0, lds + kStageBytes);
   if constexpr (SA == Stg::MN) {
+    ca.issue(0, lds);
+    cb.issue(0, lds + kStageBytes);
     // A transposing-read A operand needs per-block fragment addresses for its
     // kTM blocks; without the spare registers for the cross-barrier
     // prefetch, one barrier at the top of each step: it publishes step k and
@@ -740,24 +744,44 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     __syncthreads();
     return;
   }
-  if (nk > 1) {
-    ca.issue(1, lds + 2 * kStageBytes);
-    cb.issue(1, lds + 3 * kStageBytes);
-    // stage 0 landed; the CA::NI + CB::NI copies of stage 1 may be in flight
-    static_assert(CA::NI + CB::NI <= 15, "vmcnt field");
-    __builtin_amdgcn_s_waitcnt(0x3f70 | (CA::NI + CB::NI));
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
+  // Cross-barrier loop over a ring of kNA stages of A and kNB of B (one of
+  // them 3 deep): stage k of A lives in slot k % kNA at ldsA, of B in slot
+  // k % kNB at ldsB.  After the barrier of step k the slots of step k are
+  // free; the shallow operand's copy of step k + 2 is issued first, then the
+  // deep operand's of step k + 3, so the wait for step k + 1 before the next
+  // barrier may leave exactly the deep operand's newest copies in flight.
+  constexpr int kNA = kDeepA ? 3 : 2, kNB = kDeepA ? 2 : 3;
+  static_assert((kNA + kNB) * kStageBytes <= kLdsRing, "ring");
+  constexpr int kNID = kDeepA ? CA::NI : CB::NI;                // deep copies per step
+  constexpr int kNIS = kDeepA ? CB::NI : CA::NI;                // shallow copies per step
+  static_assert(kNIS + 2 * kNID <= 15, "vmcnt field");
+  char* const ldsA = lds;
+  char* const ldsB = lds + kNA * kStageBytes;
+  // prologue: steps 0 and 1 of both, step 2 of the deep operand (past the
+  // end: zero-filled); wait for step 0
+  ca.issue(0, ldsA);
+  cb.issue(0, ldsB);
+  if constexpr (kDeepA) {
+    cb.issue(1, ldsB + kStageBytes);
+    ca.issue(1, ldsA + kStageBytes);
+    ca.issue(2, ldsA + 2 * kStageBytes);
   } else {
-    dma_wait_barrier();
+    ca.issue(1, ldsA + kStageBytes);
+    cb.issue(1, ldsB + kStageBytes);
+    cb.issue(2, ldsB + 2 * kStageBytes);
   }
+  __builtin_amdgcn_s_waitcnt(0x3f70 | (kNIS + 2 * kNID));
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
   u32x4 a0[kTM], b0[kTN], a1[kTM], b1[kTN];
-  read_frags<T, SA, SB>(a0, b0, lds, lds + kStageBytes, wm, wn, lane, 0);
+  read_frags<T, SA, SB>(a0, b0, ldsA, ldsB, wm, wn, lane, 0);
+  int sa = 0, sb = 0;   // slots of step kt
   for (int64_t kt = 0; kt < nk; ++kt) {
-    char* cur = lds + (kt & 1) * (2 * kStageBytes);
-    char* nxt = lds + ((kt + 1) & 1) * (2 * kStageBytes);
-    read_frags<T, SA, SB>(a1, b1, cur, cur + kStageBytes, wm, wn, lane, 1);
+    char* const curA = ldsA + sa * kStageBytes;
+    char* const curB = ldsB + sb * kStageBytes;
+    const int na = sa + 1 == kNA ? 0 : sa + 1, nb = sb + 1 == kNB ? 0 : sb + 1;
+    read_frags<T, SA, SB>(a1, b1, curA, curB, wm, wn, lane, 1);
     Mfma<T>::step(acc, a0, b0);
     // issue order: one MFMA, one fragment read, ... so that the reads go out
     // while the MFMA pipe is busy
@@ -767,20 +791,27 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
     }
     __builtin_amdgcn_sched_group_barrier(0x008, kTM * kTN - (kTM + kTN), 0);
-    // this wave: copies of stage kt+1 landed, reads of stage kt returned;
-    // nothing is scheduled across the barrier
+    // this wave: step kt+1 landed (only the deep operand's step kt+2 may be
+    // in flight), reads of step kt returned; nothing is scheduled across the
+    // barrier
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
+    __builtin_amdgcn_s_waitcnt(0x0070 | kNID);   // vmcnt(kNID) lgkmcnt(0)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
-    // stage kt+2 (past the end: every chunk out of K, zero-filled, harmless
-    // in a released buffer); the first fragments of stage kt+1 (past the
-    // end: unused)
-    ca.issue(kt + 2, cur);
-    cb.issue(kt + 2, cur + kStageBytes);
-    read_frags<T, SA, SB>(a0, b0, nxt, nxt + kStageBytes, wm, wn, lane, 0);
+    // the freed slots: shallow step kt+2, deep step kt+3 (past the end: every
+    // chunk out of K, zero-filled, harmless in a free slot); the first
+    // fragments of step kt+1 (past the end: unused)
+    if constexpr (kDeepA) {
+      cb.issue(kt + 2, curB);
+      ca.issue(kt + 3, curA);
+    } else {
+      ca.issue(kt + 2, curA);
+      cb.issue(kt + 3, curB);
+    }
+    read_frags<T, SA, SB>(a0, b0, ldsA + na * kStageBytes, ldsB + nb * kStageBytes, wm, wn,
+                          lane, 0);
     Mfma<T>::step(acc, a1, b1);
     static_assert(kSpread * (CA::NI + CB::NI) + kTM + kTN <= kTM * kTN, "issue slots");
 #pragma unroll
@@ -795,9 +826,11 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     }
     __builtin_amdgcn_sched_group_barrier(
         0x008, kTM * kTN - kSpread * (CA::NI + CB::NI) - (kTM + kTN), 0);
+    sa = na;
+    sb = nb;
   }
-  // the zero-filling copies issued by the last two steps land before the
-  // LDS is reused
+  // the zero-filling copies issued by the last steps land before the LDS is
+  // reused
   __builtin_amdgcn_s_waitcnt(0x0070);
   __syncthreads();
 }
@@ -850,11 +883,11 @@ __device__ __forceinline__ void gemm_mainloop_reg(const Operand& A, const Operan
 // Full K loop for the tile at (m0, n0).  `lds` holds kLdsGemm bytes.  bf16,
 // or fp32 with both operands K-contiguous: direct copies; otherwise (fp32
 // M/N-contiguous operands) register-staged copies.
-template <typename T, Lay LA, Lay LB, int kSpread = 1>
+template <typename T, Lay LA, Lay LB, int kSpread = 1, bool kDeepA = true>
 __device__ __forceinline__ void gemm_mainloop(const Operand& A, const Operand& B, int64_t m0,
                                               int64_t n0, int64_t K, char* lds, Acc& acc) {
   if constexpr ((KContig<LA>::value && KContig<LB>::value) || sizeof(T) == 2)
-    gemm_mainloop_dma<T, LA, LB, kSpread>(A, B, m0, n0, K, lds, acc);
+    gemm_mainloop_dma<T, LA, LB, kSpread, kDeepA>(A, B, m0, n0, K, lds, acc);
   else
     gemm_mainloop_reg<T, LA, LB>(A, B, m0, n0, K, lds, acc);
 }
@@ -870,22 +903,24 @@ __device__ __forceinline__ int acc_col(int wn, int j, int lane) {
   return wn * kWaveCols + j * 16 + (lane & 15);
 }
 
-// Body of every tiled contraction kernel: Epi provides prologue(m0, n0,
-// extra) to stage per-row data into `extra` LDS before the loop and
-// epilogue(acc, tm, tn, m0, n0, lds, extra) after it.  Each use is wrapped in
-// a __global__ function of its own name (so profiles name the role).
-template <typename T, Lay LA, Lay LB, class Epi, int kSpread = 1>
+// Body of every tiled contraction kernel.  Epi provides prologue(m0, n0),
+// which loads the few per-lane values its epilogue needs into registers
+// before the loop (the loop owns all of the LDS), and epilogue(acc, tm, tn,
+// m0, n0, lds, extra, pre), which may use the LDS once the loop is over:
+// the stage buffers from `lds` and kLdsRing - kLdsGemm bytes from `extra`.
+// Each use is wrapped in a __global__ function of its own name (so profiles
+// name the role), whose LDS array is kLdsRing bytes.
+template <typename T, Lay LA, Lay LB, class Epi, int kSpread = 1, bool kDeepA = true>
 __device__ __forceinline__ void gemm_body(const Operand& A, const Operand& B, int64_t K, int nTm,
                                           int nTn, const Epi& epi, char* lds,
                                           int group_m = kGroupM) {
   int tm, tn;
   tile_of(blockIdx.x, nTm, nTn, group_m, tm, tn);
   const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
-  char* extra = lds + kLdsGemm;
-  epi.prologue(m0, n0, extra);
+  const auto pre = epi.prologue(m0, n0);
   Acc acc;
-  gemm_mainloop<T, LA, LB, kSpread>(A, B, m0, n0, K, lds, acc);
-  epi.epilogue(acc, tm, tn, m0, n0, lds, extra);
+  gemm_mainloop<T, LA, LB, kSpread, kDeepA>(A, B, m0, n0, K, lds, acc);
+  epi.epilogue(acc, tm, tn, m0, n0, lds, lds + kLdsGemm, pre);
 }
 
 }  // namespace mc
