@@ -394,6 +394,23 @@ template <Lay L> struct StageCopy<float, L, false> {
 // supplies row (l & 31) of each 32-row block and K-chunk (l >> 5) of each
 // 32-byte K slice; A and B use the same lane -> k assignment.
 // ---------------------------------------------------------------------------
+// Compile-time loop: f(integral_constant<int, i>) for i = b .. e-1.
+template <int V> struct IntC {
+  static constexpr int value = V;
+};
+template <int b, int e, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (b < e) {
+    f(IntC<b>{});
+    static_for<b + 1, e>(f);
+  }
+}
+
+template <bool c, class X, class Y>
+__device__ __forceinline__ auto& pick(X& x, Y& y) {
+  if constexpr (c) return x; else return y;
+}
+
 template <typename T> struct Mfma;
 
 template <> struct Mfma<bf16_t> {
@@ -405,6 +422,16 @@ template <> struct Mfma<bf16_t> {
       for (int j = 0; j < kTN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             __builtin_bit_cast(bf16x8, a[i]), __builtin_bit_cast(bf16x8, b[j]), acc[i][j], 0, 0, 0);
+  }
+  // the MFMAs r0 .. r1-1 of step()'s order (r = i kTN + j)
+  template <int r0, int r1>
+  __device__ __forceinline__ static void range(Acc& acc, const u32x4 (&a)[kTM],
+                                               const u32x4 (&b)[kTN]) {
+#pragma unroll
+    for (int r = r0; r < r1; ++r)
+      acc[r / kTN][r % kTN] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          __builtin_bit_cast(bf16x8, a[r / kTN]), __builtin_bit_cast(bf16x8, b[r % kTN]),
+          acc[r / kTN][r % kTN], 0, 0, 0);
   }
 };
 
@@ -592,6 +619,20 @@ template <typename T, Lay L, bool kAsm> struct DmaCopy {
     for (int i = 0; i < NI; ++i)
       if (r0 + row + 8 * kWaves * i < op.rows) rowok |= 1u << i;
   }
+  // one copy at a time (inline-asm path): prep() once per step, then one(i)
+  struct Step {
+    i32x4 rs;
+    uint32_t m0;
+    bool kok;
+  };
+  __device__ __forceinline__ Step prep(int64_t kt, char* lds) const {
+    return Step{dma_rsrc(tb + kt * step), lds_addr(lds) + grp * 1024,
+                int(kt) * int(M::KT) < klim};
+  }
+  __device__ __forceinline__ void one(const Step& h, int i) const {
+    const bool ok = h.kok && ((rowok >> i) & 1u);
+    dma16(h.rs, ok ? off0 + i * istride : kBufOut, h.m0 + i * kWaves * 1024);
+  }
   __device__ __forceinline__ void issue(int64_t kt, char* lds) const {
     const bool kok = int(kt) * int(M::KT) < klim;
     if constexpr (kAsm) {
@@ -642,14 +683,22 @@ template <Lay L> struct DmaCopyMN {
     istride = M::rel(op, 8 * c, k0 + 2 * kWaves) - off0;
     mok = r0 + 8 * c < op.rows;
   }
+  struct Step {
+    i32x4 rs;
+    uint32_t m0;
+    int kk;
+  };
+  __device__ __forceinline__ Step prep(int64_t kt, char* lds) const {
+    return Step{dma_rsrc(tb + kt * step), lds_addr(lds) + grp * 1024, int(kt) * int(M::KT)};
+  }
+  __device__ __forceinline__ void one(const Step& h, int i) const {
+    const bool ok = mok && (h.kk + 2 * kWaves * i < klim);
+    dma16(h.rs, ok ? off0 + i * istride : kBufOut, h.m0 + i * kWaves * 1024);
+  }
   __device__ __forceinline__ void issue(int64_t kt, char* lds) const {
-    const i32x4 rs = dma_rsrc(tb + kt * step);
-    const uint32_t m0 = lds_addr(lds) + grp * 1024;
+    const Step h = prep(kt, lds);
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const bool ok = mok && (int(kt) * int(M::KT) + 2 * kWaves * i < klim);
-      dma16(rs, ok ? off0 + i * istride : kBufOut, m0 + i * kWaves * 1024);
-    }
+    for (int i = 0; i < NI; ++i) one(h, i);
   }
 };
 
@@ -751,6 +800,9 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
   // deep operand's of step k + 3, so the wait for step k + 1 before the next
   // barrier may leave exactly the deep operand's newest copies in flight.
   constexpr int kNA = kDeepA ? 3 : 2, kNB = kDeepA ? 2 : 3;
+  // LDS reads per sub-step: one per block, two per transposed block
+  constexpr int kRd = (SA == Stg::MN ? 2 : 1) * kTM + (SB == Stg::MN ? 2 : 1) * kTN;
+  static_assert(kRd <= kTM * kTN, "read slots");
   static_assert((kNA + kNB) * kStageBytes <= kLdsRing, "ring");
   constexpr int kNID = kDeepA ? CA::NI : CB::NI;                // deep copies per step
   constexpr int kNIS = kDeepA ? CB::NI : CA::NI;                // shallow copies per step
@@ -786,11 +838,11 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     // issue order: one MFMA, one fragment read, ... so that the reads go out
     // while the MFMA pipe is busy
 #pragma unroll
-    for (int r = 0; r < kTM + kTN; ++r) {
+    for (int r = 0; r < kRd; ++r) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, kTM * kTN - (kTM + kTN), 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, kTM * kTN - kRd, 0);
     // this wave: step kt+1 landed (only the deep operand's step kt+2 may be
     // in flight), reads of step kt returned; nothing is scheduled across the
     // barrier
@@ -803,6 +855,36 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     // the freed slots: shallow step kt+2, deep step kt+3 (past the end: every
     // chunk out of K, zero-filled, harmless in a free slot); the first
     // fragments of step kt+1 (past the end: unused)
+    if constexpr (kAsm) {
+      // the scheduler does not see inline-asm copies: one copy, then kCopyGap
+      // MFMAs, in program order, each pair fenced
+      constexpr int kCopyGap = 2;
+      static_assert(kCopyGap * (CA::NI + CB::NI) + kRd <= kTM * kTN, "issue slots");
+      const auto& cs = pick<kDeepA>(cb, ca);   // shallow
+      const auto& cd = pick<kDeepA>(ca, cb);   // deep
+      const auto hs = cs.prep(kt + 2, kDeepA ? curB : curA);
+      const auto hd = cd.prep(kt + 3, kDeepA ? curA : curB);
+      static_for<0, CA::NI + CB::NI>([&](auto c) {
+        constexpr int r = decltype(c)::value;
+        if constexpr (r < kNIS)
+          cs.one(hs, r);
+        else
+          cd.one(hd, r - kNIS);
+        Mfma<T>::template range<kCopyGap * r, kCopyGap * (r + 1)>(acc, a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      read_frags<T, SA, SB>(a0, b0, ldsA + na * kStageBytes, ldsB + nb * kStageBytes, wm, wn,
+                            lane, 0);
+      Mfma<T>::template range<kCopyGap * (CA::NI + CB::NI), kTM * kTN>(acc, a1, b1);
+#pragma unroll
+      for (int r = 0; r < kRd; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+      }
+      sa = na;
+      sb = nb;
+      continue;
+    }
     if constexpr (kDeepA) {
       cb.issue(kt + 2, curB);
       ca.issue(kt + 3, curA);
@@ -813,19 +895,19 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     read_frags<T, SA, SB>(a0, b0, ldsA + na * kStageBytes, ldsB + nb * kStageBytes, wm, wn,
                           lane, 0);
     Mfma<T>::step(acc, a1, b1);
-    static_assert(kSpread * (CA::NI + CB::NI) + kTM + kTN <= kTM * kTN, "issue slots");
+    static_assert(kSpread * (CA::NI + CB::NI) + kRd <= kTM * kTN, "issue slots");
 #pragma unroll
     for (int r = 0; r < CA::NI + CB::NI; ++r) {
       __builtin_amdgcn_sched_group_barrier(0x008, kSpread, 0);   // MFMA
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);         // copy issue
     }
 #pragma unroll
-    for (int r = 0; r < kTM + kTN; ++r) {
+    for (int r = 0; r < kRd; ++r) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
     }
     __builtin_amdgcn_sched_group_barrier(
-        0x008, kTM * kTN - kSpread * (CA::NI + CB::NI) - (kTM + kTN), 0);
+        0x008, kTM * kTN - kSpread * (CA::NI + CB::NI) - kRd, 0);
     sa = na;
     sb = nb;
   }
