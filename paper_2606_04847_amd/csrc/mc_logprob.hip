@@ -798,7 +798,7 @@ template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand B, int64_t K,
                                                              int nTm, int nTn, EpiDH<T> epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
-  gemm_body<T, Lay::TileTK, Lay::KMajor, EpiDH<T>, 1, kDeepDhA>(A, B, K, nTm, nTn, epi, lds);
+  gemm_body<T, Lay::TileTK, Lay::KMajor, EpiDH<T>, 2, kDeepDhA>(A, B, K, nTm, nTn, epi, lds);
 }
 // dW^T = H^T P~ : tile rows are hidden dimensions (A = H^T, along the
 // tokens), tile columns vocabulary entries (B = the operand panels read

@@ -731,7 +731,7 @@ __device__ __forceinline__ void dma_wait_barrier() {
 // so the MFMAs after the barrier already have their fragments in registers
 // while the next stage's first reads are in flight.
 // kSpread: MFMAs between consecutive copy issues after the barrier of the
-// cross-barrier loop (1 suits dH, 2 the forward: measured).  kDeepA: operand
+// cross-barrier loop (2 for the forward and dH: measured).  kDeepA: operand
 // A gets the 3-stage side of the ring (else B).
 template <typename T, Lay LA, Lay LB, int kSpread = 1, bool kDeepA = true>
 __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operand& B, int64_t m0,
