@@ -161,6 +161,35 @@ def test_accumulate_flags_and_partial_outputs():
     assert torch.equal(only_h, dH) and torch.equal(only_w, dW)
 
 
+def test_dweight_split_tail_accumulate():
+    # 12 tiles of dW (d = 256, V = 3000): the whole launch is one partial
+    # round, computed as K slices (T = 1500: 4 slices of 384 tokens) summed
+    # by the tail reduction; accumulate adds the stored dW after the sum
+    cfg = scaled_config(4, T=1500, n_groups=2, group_size=8, d=256, V=3000, hi=200, seed=16,
+                        drift=_drift(16))
+    case = small_case(cfg)
+    mc = _mc()
+    H, W, y = device_tensors(case)
+    logp, lse = mc.logprob_fwd(H, W, y)
+    dl = torch.randn(len(case["y"]), device="cuda") * 1e-3
+    _, dW = mc.logprob_bwd(H, W, y, lse, dl)
+    dW2 = torch.full_like(dW, 0.5)
+    mc.logprob_bwd(H, W, y, lse, dl, dweight=dW2, accumulate_dweight=True, need_dhidden=False)
+    cache = mc.softmax_cache(H, W)
+    _, lse_c = mc.logprob_fwd_cached(H, W, y, cache)
+    dW3 = torch.full_like(dW, -0.25)
+    mc.logprob_bwd_cached(H, W, y, lse_c, dl, cache, dweight=dW3, accumulate_dweight=True,
+                          need_dhidden=False)
+    torch.cuda.synchronize()
+    assert torch.allclose(dW2, dW + 0.5, atol=1e-6, rtol=0)
+    Wd = W.double().cpu().numpy()
+    lo, so = oracle.logprob_fwd(H.float().cpu().numpy().astype(np.float64), Wd, y.cpu().numpy())
+    _, dW_o = oracle.logprob_bwd(H.float().cpu().numpy().astype(np.float64), Wd, y.cpu().numpy(),
+                                 so, dl.double().cpu().numpy())
+    assert rel_fro((dW3 + 0.25).cpu().numpy(), dW_o) <= GRAD_RTOL
+    assert rel_fro(dW.cpu().numpy(), dW_o) <= GRAD_RTOL
+
+
 def test_determinism_bit_identical():
     cfg = scaled_config(4, T=1200, n_groups=4, group_size=8, d=256, V=1500, hi=300, seed=15,
                         drift=_drift(32))
