@@ -791,7 +791,7 @@ template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B, int64_t K,
                                                            int nTm, int nTn, EpiProbs<T> epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
-  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiProbs<T>, 1, kDeepFwdA>(A, B, K, nTm, nTn, epi, lds,
+  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiProbs<T>, 2, kDeepFwdA>(A, B, K, nTm, nTn, epi, lds,
                                                                     kGroupVT);
 }
 template <typename T>
