@@ -368,7 +368,6 @@ struct EpiProbs {
                                    // width; pld: padded token count
   T* P;                            // panel layout (see Lay::TileTK)
   static constexpr int64_t kPanel = 128 / sizeof(T);
-  static constexpr int kLdsExtra = 0;
 
   // lse_t log2(e) and -dlogp_t (0 for ignored tokens) of this lane's kTN
   // token columns
@@ -461,7 +460,6 @@ struct EpiDH {
   const int64_t* y;
   const float* dlogp;
   int64_t v_off, Vs;
-  static constexpr int kLdsExtra = 0;
 
   struct Pre {};
   __device__ __forceinline__ Pre prologue(int64_t, int64_t) const { return Pre{}; }
@@ -507,7 +505,6 @@ struct EpiStoreT {
   float* C;
   int64_t ldc, rows, cols;
   int accumulate;
-  static constexpr int kLdsExtra = 0;
 
   struct Pre {};
   __device__ __forceinline__ Pre prologue(int64_t, int64_t) const { return Pre{}; }
@@ -545,46 +542,44 @@ struct EpiStoreT {
 // rows <= r < 64 ceil(rows / 64) (ld_out covers that padding; cols, ld_in and
 // ld_out are multiples of 8).  The zero padding matters: a K-contiguous
 // operand is copied in 16-byte chunks, so up to the next multiple of 8 (bf16)
-// past K is read.  64 x 64 tiles through LDS (grid x over row tiles, y over
-// column tiles); 16-byte global accesses along both rows.  Gives the
-// backward's contractions over the vocabulary and over tokens operands that
-// run along K.
+// past K is read.  One wave per 64 x 64 tile (grid x over row tiles, y over
+// groups of 4 column tiles), no LDS: lane (a, b) loads rows 8a .. 8a+7 of
+// column chunk b (CE elements per 16 bytes), transposes the CE x CE block in
+// registers and stores it as rows 8b .. of output chunk a; every 8 lanes
+// cover one whole 128-byte row in each access.  Gives the backward's
+// contractions over the vocabulary and over tokens operands that run along K.
 template <typename T>
 __global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ in, int64_t rows,
                                                    int64_t cols, int64_t ld_in,
                                                    T* __restrict__ out, int64_t ld_out) {
-  constexpr int V = 16 / sizeof(T);   // elements per 16-byte access
-  constexpr int P = 64 + V;           // padded LDS row (elements)
-  __shared__ __attribute__((aligned(16))) T tile[64 * P];
-  const int64_t r0 = int64_t(blockIdx.x) * 64, c0 = int64_t(blockIdx.y) * 64;
-  const int t = threadIdx.x;
-  // load 64 rows x 64 columns (zeros outside): each thread 16 consecutive
-  // columns of one row
-  {
-    const int rr = t >> 2, cc = (t & 3) * 16;
-    const int64_t r = r0 + rr;
+  constexpr int CE = 16 / sizeof(T);   // elements per 16-byte access
+  constexpr int S = 64 / CE;           // lanes per 64-element row: 8 (bf16) or 16 (fp32)
+  const int lane = threadIdx.x & 63;
+  const int64_t r0 = int64_t(blockIdx.x) * 64;
+  const int64_t c0 = (int64_t(blockIdx.y) * 4 + (threadIdx.x >> 6)) * 64;
+  if (c0 >= cols) return;
+  constexpr int kPasses = (64 / CE) * (64 / CE) / 64;   // bf16: 1, fp32: 4
 #pragma unroll
-    for (int h = 0; h < 16 / V; ++h) {
-      const int64_t c = c0 + cc + h * V;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (r < rows && c < cols) v = *reinterpret_cast<const u32x4*>(in + r * ld_in + c);
-      *reinterpret_cast<u32x4*>(&tile[rr * P + cc + h * V]) = v;
+  for (int pass = 0; pass < kPasses; ++pass) {
+    const int blk = pass * 64 + lane;          // CE x CE block index within the tile
+    const int a = blk / S, b = blk % S;        // row block, column chunk
+    const int64_t c = c0 + int64_t(b) * CE;    // first input column of the chunk
+    T v[CE][CE];
+#pragma unroll
+    for (int j = 0; j < CE; ++j) {
+      const int64_t r = r0 + int64_t(a) * CE + j;
+      u32x4 raw = {0u, 0u, 0u, 0u};
+      if (r < rows && c < cols) raw = *reinterpret_cast<const u32x4*>(in + r * ld_in + c);
+      *reinterpret_cast<u32x4*>(v[j]) = raw;
     }
-  }
-  __syncthreads();
-  // store 64 output rows (input columns) x 64 output columns (input rows,
-  // the padding included)
-  {
-    const int oc = t >> 2, orr = (t & 3) * 16;
-    const int64_t c = c0 + oc;
-    if (c >= cols) return;
-    T* o = out + c * ld_out + r0 + orr;
+    if (c >= cols) continue;
 #pragma unroll
-    for (int h = 0; h < 16 / V; ++h) {
-      T v[V];
+    for (int i = 0; i < CE; ++i) {
+      T o[CE];
 #pragma unroll
-      for (int e = 0; e < V; ++e) v[e] = tile[(orr + h * V + e) * P + oc];
-      *reinterpret_cast<u32x4*>(o + h * V) = __builtin_bit_cast(u32x4, v);
+      for (int j = 0; j < CE; ++j) o[j] = v[j][i];
+      *reinterpret_cast<u32x4*>(out + (c + i) * ld_out + r0 + int64_t(a) * CE) =
+          *reinterpret_cast<const u32x4*>(o);
     }
   }
 }
@@ -990,7 +985,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       // so that both operands run along K
       {
         ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(width) * d);
-        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(width, 64), cdiv(d, 64)), dim3(256), 0, s,
+        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(width, 64), cdiv(d, 256)), dim3(256), 0, s,
                            Wc, width, d, d, Wt, ldc);
       }
       Operand A{P, pld, Tn, ldc}, B{Wt, ldc, d, width};   // ldc = 64 ceil(width / 64)
@@ -1014,7 +1009,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       // [d x pld] (made once) so that the M operand runs along K
       if (v0 == 0) {
         ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(Tn) * d);
-        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(Tn, 64), cdiv(d, 64)), dim3(256), 0, s,
+        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(Tn, 64), cdiv(d, 256)), dim3(256), 0, s,
                            H, Tn, d, d, Ht, pld);
       }
       Operand A{Ht, pld, d, Tn}, B{P, pld, ldc, Tn};   // pld = 64 ceil(Tn / 64)
