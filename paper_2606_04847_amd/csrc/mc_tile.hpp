@@ -12,9 +12,11 @@
 // global->LDS copy and the 16-byte fragment reads of the MFMA loop avoid bank
 // conflicts.  An operand that is contiguous along M/N in memory is transposed
 // in registers on its way to LDS (fp32), or copied as is and read back with
-// the transposing LDS read (bf16).  Two LDS stages.  Direct global->LDS
-// copies keep step k+1 in flight while step k is multiplied; the
-// register-staged copies (fp32 M/N-contiguous operands) keep step k+2.
+// the transposing LDS read (bf16).  Direct global->LDS copies fill a ring of
+// 3 + 2 operand stages (all 160 KiB of LDS), keeping one operand's copies two
+// steps and the other's one step ahead of the MFMAs; the register-staged
+// copies (fp32 M/N-contiguous operands) use two stages and keep step k+2 in
+// registers.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -279,62 +281,6 @@ template <typename T, Lay L> struct StageCopy<T, L, true> {
 #pragma unroll
     for (int i = 0; i < NL; ++i)
       *reinterpret_cast<u32x4*>(lds + lds_off((tid >> 3) + kPass * i, c)) = r[i];
-  }
-};
-
-// M/N-contiguous bf16: thread owns an 8(mn) x KB(k) block, mn-block tid & 31,
-// k-block tid >> 5 (KB = 8 with 256 threads, 4 with 512); transposed with
-// byte permutes, written as KB*2-byte pieces of the K-contiguous rows.
-template <Lay L> struct StageCopy<bf16_t, L, false> {
-  using M = LayMath<bf16_t, L>;
-  static constexpr int KB = 8 * 256 / kThreads;
-  u32x4 r[KB];
-  const char* tb;
-  int64_t step, K;
-  uint32_t off0, dk_bytes;
-  int kb;
-  bool mnok;
-  __device__ __forceinline__ void init(const Operand& op, int64_t r0, int tid) {
-    tb = static_cast<const char*>(op.ptr) + M::tile_base(op, r0);
-    step = M::stage_step(op);
-    K = op.K;
-    kb = (tid >> 5) * KB;
-    off0 = M::rel(op, (tid & 31) * 8, kb);
-    dk_bytes = M::rel(op, (tid & 31) * 8, kb + 1) - off0;
-    mnok = r0 + (tid & 31) * 8 < op.rows;
-  }
-  __device__ __forceinline__ void load(int64_t kt) {
-    const __amdgpu_buffer_rsrc_t rs = stage_rsrc(tb + kt * step);
-    const int64_t k0 = kt * M::KT + kb;
-#pragma unroll
-    for (int i = 0; i < KB; ++i) {
-      const bool ok = mnok && (k0 + i < K);
-      r[i] = buf_load16(rs, ok ? off0 + i * dk_bytes : kBufOut);
-    }
-  }
-  __device__ __forceinline__ void store(char* lds, int tid) const {
-    const int row0 = (tid & 31) * 8;
-    const int kq = tid >> 5;   // k-block index; KB k values = KB*2 bytes
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      // word q packs (k = 2q, k = 2q+1) of column j: low halves for even j,
-      // high halves for odd j.
-      const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-      const int row = row0 + j;
-      if constexpr (KB == 8) {
-        u32x4 out;
-        out[0] = __builtin_amdgcn_perm(r[1][j >> 1], r[0][j >> 1], sel);
-        out[1] = __builtin_amdgcn_perm(r[3][j >> 1], r[2][j >> 1], sel);
-        out[2] = __builtin_amdgcn_perm(r[5][j >> 1], r[4][j >> 1], sel);
-        out[3] = __builtin_amdgcn_perm(r[7][j >> 1], r[6][j >> 1], sel);
-        *reinterpret_cast<u32x4*>(lds + lds_off(row, kq)) = out;
-      } else {
-        u32x2 out;
-        out[0] = __builtin_amdgcn_perm(r[1][j >> 1], r[0][j >> 1], sel);
-        out[1] = __builtin_amdgcn_perm(r[3][j >> 1], r[2][j >> 1], sel);
-        *reinterpret_cast<u32x2*>(lds + lds_off(row, kq >> 1) + (kq & 1) * 8) = out;
-      }
-    }
   }
 };
 
