@@ -38,17 +38,17 @@ PEAK_FP32_TFLOPS = 157.3
 # the kernel sources with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "959548176f3476a7ce85b980286e80f3ffd24347f6098573117e3011896bf044",
+        "0d3cc488f65eea678c9c24125adf5747b79b3d7f7158d2e6b9eb2422beca9b63",
     "bytes_per_launch": {
-        "logprob_fwd_gemm": 36309334407,
+        "logprob_fwd_gemm": 36261471545,
         "logprob_fwd_merge": 78254645,
         "rl_loss": 91896,
-        "logprob_bwd_bucket": 1328755,
-        "logprob_bwd_cache_probs": 10035312033,
-        "logprob_bwd_transpose": 1903639181,
-        "logprob_bwd_dhidden": 30296551332,
-        "logprob_bwd_dweight": 32661685640,
-        "logprob_bwd_onehot_dw": 650844274,
+        "logprob_bwd_bucket": 1328787,
+        "logprob_bwd_cache_probs": 10035311777,
+        "logprob_bwd_transpose": 1378944395,
+        "logprob_bwd_dhidden": 30289034033,
+        "logprob_bwd_dweight": 32661881776,
+        "logprob_bwd_onehot_dw": 650846322,
     },
 }
 
