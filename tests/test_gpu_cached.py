@@ -106,6 +106,47 @@ def test_cached_peaked_softmax_pterm():
     assert rel_fro(g["dW"] - Wg, o["dW"] - Wo) <= PTERM_RTOL
 
 
+def test_large_logits_both_paths():
+    # W std 10: logits of std ~80, every softmax effectively one-hot and the
+    # per-block maxima hundreds of nats apart (the cache's exp(c_b - lse)
+    # underflows to 0 for most blocks); targets uniform so that the gradient
+    # (dlogp (onehot_y - onehot_argmax)) is far from zero
+    cfg = scaled_config(4, d=64, V=2000, seed=77, w_std=10.0)
+    T = 300
+    H, W, hb, wb = make_tensors_numpy(cfg, T)
+    rng = np.random.default_rng(78)
+    y = rng.integers(0, 2000, size=T)
+    case = dict(H=H, W=W, hb=hb, wb=wb, y=y)
+    logp_o, lse_o = oracle.logprob_fwd(H, W, y)
+    dlogp = rng.standard_normal(T) * 1e-2
+    dH_o, dW_o = oracle.logprob_bwd(H, W, y, lse_o, dlogp)
+    mc = _mc()
+    Hd, Wd, yd = device_tensors(case)
+    dl = torch.from_numpy(dlogp.astype(np.float32)).cuda()
+    logp_p, lse_p = mc.logprob_fwd(Hd, Wd, yd)
+    dH_p, dW_p = mc.logprob_bwd(Hd, Wd, yd, lse_p, dl)
+    cache = mc.softmax_cache(Hd, Wd)
+    logp_c, lse_c = mc.logprob_fwd_cached(Hd, Wd, yd, cache)
+    dH_c, dW_c = mc.logprob_bwd_cached(Hd, Wd, yd, lse_c, dl, cache)
+    torch.cuda.synchronize()
+    assert np.abs(lse_o).max() > 100.0
+    # here the softmax part carries about half of the gradient, and its bf16
+    # operand bounds it at 2^-8 relative (not the near-uniform 1e-3 bar): the
+    # one-hot part is exact, so the whole gradient is held to that bound too
+    Wf, Hf = W.astype(np.float64), H.astype(np.float64)
+    onehot_dH = dlogp[:, None] * Wf[y]
+    onehot_dW = np.zeros_like(dW_o)
+    np.add.at(onehot_dW, y, dlogp[:, None] * Hf)
+    for logp, lse, dH, dW in ((logp_p, lse_p, dH_p, dW_p), (logp_c, lse_c, dH_c, dW_c)):
+        assert np.max(np.abs(logp.cpu().numpy() - logp_o)) <= LOGP_ATOL
+        assert np.max(np.abs(lse.cpu().numpy() - lse_o)) <= LOGP_ATOL
+        g_dH, g_dW = dH.cpu().numpy().astype(np.float64), dW.cpu().numpy().astype(np.float64)
+        assert np.isfinite(g_dH).all() and np.isfinite(g_dW).all()
+        assert rel_fro(g_dH - onehot_dH, dH_o - onehot_dH) <= PTERM_RTOL
+        assert rel_fro(g_dW - onehot_dW, dW_o - onehot_dW) <= PTERM_RTOL
+        assert rel_fro(g_dH, dH_o) <= PTERM_RTOL and rel_fro(g_dW, dW_o) <= PTERM_RTOL
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("T,d,V", [(1, 8, 1), (1, 64, 7), (300, 136, 257), (257, 8, 513),
                                    (513, 64, 256)])
