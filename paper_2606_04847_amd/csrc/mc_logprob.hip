@@ -721,7 +721,11 @@ __global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
 // Grid: x over blocks of 32 tokens, y over groups of kCachePanels panels
 // from panel pn0; thread = one 16-byte chunk of one row of each of those
 // panels (8 lanes per 128-byte row).  The stream is touched once:
-// non-temporal loads and stores.
+// non-temporal loads and stores.  Where the factor is exactly zero (a
+// token whose dlogp is zero: outside the loss mask, in a filtered sequence
+// or clipped; an ignored target; a block past the vocabulary) the chunk is
+// written as zeros without reading it: the cached values are finite, so
+// the product would be zeros of the same sign.
 constexpr int kCachePanels = 4;
 template <typename T>
 __global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
@@ -745,11 +749,14 @@ __global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
 #pragma unroll
   for (int q = 0; q < kCachePanels; ++q) {
     const int64_t pn = p0 + q;
-    if (pn < npanels) {
-      raw[q] = __builtin_nontemporal_load(
-          reinterpret_cast<const u32x4*>(E + (pn * pld + t) * BV + ch * CE));
+    raw[q] = u32x4{0u, 0u, 0u, 0u};
+    f[q] = 0.0f;
+    if (pn < npanels && g != 0.0f) {
       const float m = cm[((pn * BV + ch * CE) / kWaveRows) * Tn + t];
-      f[q] = (g == 0.0f || m == kNegInf) ? 0.0f : g * __expf(m - l);
+      if (m != kNegInf) f[q] = g * __expf(m - l);
+      if (f[q] != 0.0f)
+        raw[q] = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>(E + (pn * pld + t) * BV + ch * CE));
     }
   }
 #pragma unroll
