@@ -38,17 +38,17 @@ PEAK_FP32_TFLOPS = 157.3
 # the kernel sources with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "0d3cc488f65eea678c9c24125adf5747b79b3d7f7158d2e6b9eb2422beca9b63",
+        "74e5a1e293242bd192fe065f659f4dc1966a022b308839751610be3fa18433df",
     "bytes_per_launch": {
-        "logprob_fwd_gemm": 36261471545,
-        "logprob_fwd_merge": 78254645,
+        "logprob_fwd_gemm": 36163264967,
+        "logprob_fwd_merge": 78254626,
         "rl_loss": 91896,
-        "logprob_bwd_bucket": 1328787,
-        "logprob_bwd_cache_probs": 10035311777,
-        "logprob_bwd_transpose": 1378944395,
-        "logprob_bwd_dhidden": 30289034033,
-        "logprob_bwd_dweight": 32661881776,
-        "logprob_bwd_onehot_dw": 650846322,
+        "logprob_bwd_bucket": 1328778,
+        "logprob_bwd_cache_probs": 6305141870,
+        "logprob_bwd_transpose": 1378943527,
+        "logprob_bwd_dhidden": 30287986008,
+        "logprob_bwd_dweight": 32660759534,
+        "logprob_bwd_onehot_dw": 650837012,
     },
 }
 
