@@ -38,17 +38,17 @@ PEAK_FP32_TFLOPS = 157.3
 # the kernel sources with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "74e5a1e293242bd192fe065f659f4dc1966a022b308839751610be3fa18433df",
+        "29dd98661d1e482f5b17067a87a62d1fc21f1748bc67acf07f750732df1d2817",
     "bytes_per_launch": {
-        "logprob_fwd_gemm": 36163264967,
-        "logprob_fwd_merge": 78254626,
+        "logprob_fwd_gemm": 35755479170,
+        "logprob_fwd_merge": 78254642,
         "rl_loss": 91896,
-        "logprob_bwd_bucket": 1328778,
-        "logprob_bwd_cache_probs": 6305141870,
-        "logprob_bwd_transpose": 1378943527,
-        "logprob_bwd_dhidden": 30287986008,
-        "logprob_bwd_dweight": 32660759534,
-        "logprob_bwd_onehot_dw": 650837012,
+        "logprob_bwd_bucket": 1328782,
+        "logprob_bwd_cache_probs": 6307992511,
+        "logprob_bwd_transpose": 1378948912,
+        "logprob_bwd_dhidden": 30353646505,
+        "logprob_bwd_dweight": 32665598863,
+        "logprob_bwd_onehot_dw": 650831715,
     },
 }
 
