@@ -542,8 +542,9 @@ struct EpiStoreT {
 // rows <= r < 64 ceil(rows / 64) (ld_out covers that padding; cols, ld_in and
 // ld_out are multiples of 8).  The zero padding matters: a K-contiguous
 // operand is copied in 16-byte chunks, so up to the next multiple of 8 (bf16)
-// past K is read.  One wave per 64 x 64 tile (grid x over row tiles, y over
-// groups of 4 column tiles), no LDS: lane (a, b) loads rows 8a .. 8a+7 of
+// past K is read.  One wave per 64 x 64 tile (grid x over groups of 4
+// column tiles, y over row tiles: consecutive workgroups read whole input
+// rows; 6% faster than row tiles first), no LDS: lane (a, b) loads rows 8a .. 8a+7 of
 // column chunk b (CE elements per 16 bytes), transposes the CE x CE block in
 // registers and stores it as rows 8b .. of output chunk a; every 8 lanes
 // cover one whole 128-byte row in each access.  Gives the backward's
@@ -555,8 +556,8 @@ __global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ in, int
   constexpr int CE = 16 / sizeof(T);   // elements per 16-byte access
   constexpr int S = 64 / CE;           // lanes per 64-element row: 8 (bf16) or 16 (fp32)
   const int lane = threadIdx.x & 63;
-  const int64_t r0 = int64_t(blockIdx.x) * 64;
-  const int64_t c0 = (int64_t(blockIdx.y) * 4 + (threadIdx.x >> 6)) * 64;
+  const int64_t r0 = int64_t(blockIdx.y) * 64;
+  const int64_t c0 = (int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6)) * 64;
   if (c0 >= cols) return;
   constexpr int kPasses = (64 / CE) * (64 / CE) / 64;   // bf16: 1, fp32: 4
 #pragma unroll
@@ -998,7 +999,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       // so that both operands run along K
       {
         ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(width) * d);
-        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(width, 64), cdiv(d, 256)), dim3(256), 0, s,
+        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(d, 256), cdiv(width, 64)), dim3(256), 0, s,
                            Wc, width, d, d, Wt, ldc);
       }
       Operand A{P, pld, Tn, ldc}, B{Wt, ldc, d, width};   // ldc = 64 ceil(width / 64)
@@ -1022,7 +1023,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       // [d x pld] (made once) so that the M operand runs along K
       if (v0 == 0) {
         ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(Tn) * d);
-        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(Tn, 64), cdiv(d, 256)), dim3(256), 0, s,
+        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(d, 256), cdiv(Tn, 64)), dim3(256), 0, s,
                            H, Tn, d, d, Ht, pld);
       }
       Operand A{Ht, pld, d, Tn}, B{P, pld, ldc, Tn};   // pld = 64 ceil(Tn / 64)
