@@ -700,12 +700,19 @@ __global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
   const int64_t v = y[t0] - v_off;
   const int b = offsets[v], e = offsets[v + 1];
   if (p != b) return;
+  // tokens with a zero dlogp (outside the loss mask, filtered, clipped) add
+  // nothing: a bucket of only such tokens leaves its row as it is, and the
+  // others skip their rows of H
+  bool live = false;
+  for (int q = b; q < e && !live; ++q) live = dlogp[sorted[q]] != 0.0f;
+  if (!live) return;
   float* o = dW + v * d;
   for (int64_t k = int64_t(threadIdx.x) * 4; k < d; k += 4 * int64_t(blockDim.x)) {
     f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int q = b; q < e; ++q) {
       const int t = sorted[q];
       const float g = dlogp[t];
+      if (g == 0.0f) continue;
       const T* h = H + int64_t(t) * d + k;
 #pragma unroll
       for (int c = 0; c < 4; ++c) s[c] += g * float(h[c]);
