@@ -38,17 +38,17 @@ PEAK_FP32_TFLOPS = 157.3
 # the kernel sources with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "29dd98661d1e482f5b17067a87a62d1fc21f1748bc67acf07f750732df1d2817",
+        "9937044a41dad17887a6066040e7be2f7cca451983fb4ca35a27fa645b671120",
     "bytes_per_launch": {
-        "logprob_fwd_gemm": 35755479170,
+        "logprob_fwd_gemm": 36241498914,
         "logprob_fwd_merge": 78254642,
         "rl_loss": 91896,
-        "logprob_bwd_bucket": 1328782,
-        "logprob_bwd_cache_probs": 6307992511,
-        "logprob_bwd_transpose": 1378948912,
-        "logprob_bwd_dhidden": 30353646505,
-        "logprob_bwd_dweight": 32665598863,
-        "logprob_bwd_onehot_dw": 650831715,
+        "logprob_bwd_bucket": 1328801,
+        "logprob_bwd_cache_probs": 6307885119,
+        "logprob_bwd_transpose": 1378909745,
+        "logprob_bwd_dhidden": 30289453692,
+        "logprob_bwd_dweight": 32658435884,
+        "logprob_bwd_onehot_dw": 176647409,
     },
 }
 
