@@ -508,32 +508,47 @@ struct EpiStoreT {
 
   struct Pre {};
   __device__ __forceinline__ Pre prologue(int64_t, int64_t) const { return Pre{}; }
-  __device__ __forceinline__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char*,
+  // The tile goes out through the LDS in two halves of 128 columns (128 KiB
+  // of fp32 each): the waves holding a half write their blocks to it, a
+  // 16-byte chunk per row of 4, chunk index XOR-ed with the column so the 16
+  // columns of a write hit distinct banks; then every wave stores whole
+  // 1 KiB row segments of C (0.67 ms of dW's epilogue went to stores of
+  // 64 bytes into 16 rows each before).
+  __device__ __forceinline__ void epilogue(Acc& acc, int, int, int64_t m0, int64_t n0, char* lds,
                                           char*, const Pre& = Pre{}) const {
-    const int lane = threadIdx.x & 63;
+    const int tid = threadIdx.x, lane = tid & 63;
     const int wm = wave_m(), wn = wave_n();
+    constexpr int kHalf = kBN / 2;                 // columns per pass
+    constexpr int kRowChunks = kBM / 4;            // 16-byte chunks per staged column
+    static_assert(kHalf * kRowChunks * 16 <= kLdsGemm, "staging");
+    static_assert(kWavesN % 2 == 0, "a half of the columns per pair of wave columns");
 #pragma unroll
-    for (int j = 0; j < kTN; ++j) {
-      const int64_t c = n0 + acc_col(wn, j, lane);
-      if (c >= cols) continue;
-      float* crow = C + c * ldc;
+    for (int h = 0; h < 2; ++h) {
+      if (wn / (kWavesN / 2) == h) {
 #pragma unroll
-      for (int i = 0; i < kTM; ++i) {
-        const int64_t r = m0 + acc_row(wm, i, 0, lane);   // rows r .. r + 3
-        if (r + 4 <= rows) {   // ldc and r are multiples of 4: 16-byte aligned
-          f32x4 v = acc[i][j];
-          if (accumulate) v += *reinterpret_cast<const f32x4*>(crow + r);
-          *reinterpret_cast<f32x4*>(crow + r) = v;
-        } else {
+        for (int j = 0; j < kTN; ++j) {
+          const int cl = (wn % (kWavesN / 2)) * kWaveCols + j * 16 + (lane & 15);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (r + e >= rows) continue;
-            float v = acc[i][j][e];
-            if (accumulate) v += crow[r + e];
-            crow[r + e] = v;
+          for (int i = 0; i < kTM; ++i) {
+            const int ch = (wm * kWaveRows + i * 16 + 4 * (lane >> 4)) >> 2;
+            *reinterpret_cast<f32x4*>(lds + cl * (kRowChunks * 16) + ((ch ^ (cl & 15)) << 4)) =
+                acc[i][j];
           }
         }
       }
+      __syncthreads();
+      for (int q = tid; q < kHalf * kRowChunks; q += kThreads) {
+        const int cl = q / kRowChunks, ch = q % kRowChunks;
+        const int64_t c = n0 + h * kHalf + cl, r = m0 + 4 * ch;
+        if (c < cols && r < rows) {   // rows, ldc and r are multiples of 4
+          f32x4 v = *reinterpret_cast<const f32x4*>(lds + cl * (kRowChunks * 16) +
+                                                    ((ch ^ (cl & 15)) << 4));
+          f32x4* o = reinterpret_cast<f32x4*>(C + c * ldc + r);
+          if (accumulate) v += *o;
+          *o = v;
+        }
+      }
+      if (h == 0) __syncthreads();   // the second half reuses the staging
     }
   }
 };
