@@ -38,17 +38,17 @@ PEAK_FP32_TFLOPS = 157.3
 # the kernel sources with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "9937044a41dad17887a6066040e7be2f7cca451983fb4ca35a27fa645b671120",
+        "89ad65df62fb23cf00c5428c95b78f287ce26a37e30086ab9ae8d1ee8371718a",
     "bytes_per_launch": {
-        "logprob_fwd_gemm": 36241498914,
-        "logprob_fwd_merge": 78254642,
+        "logprob_fwd_gemm": 35776496589,
+        "logprob_fwd_merge": 78254638,
         "rl_loss": 91896,
-        "logprob_bwd_bucket": 1328801,
-        "logprob_bwd_cache_probs": 6307885119,
-        "logprob_bwd_transpose": 1378909745,
-        "logprob_bwd_dhidden": 30289453692,
-        "logprob_bwd_dweight": 32658435884,
-        "logprob_bwd_onehot_dw": 176647409,
+        "logprob_bwd_bucket": 1328759,
+        "logprob_bwd_cache_probs": 6307905290,
+        "logprob_bwd_transpose": 1378909526,
+        "logprob_bwd_dhidden": 30298377440,
+        "logprob_bwd_dweight": 32539418634,
+        "logprob_bwd_onehot_dw": 176661100,
     },
 }
 
