@@ -64,19 +64,32 @@ __device__ __forceinline__ int panel_stage_off(int v, int t) {
 // stores, eight lanes per 128-byte row, non-temporal (the operand is far
 // larger than the caches and next read by another kernel).  Rows t >= Tn
 // and chunk columns >= ld are skipped.  The caller has synchronised after
-// staging.
+// staging.  A thread's chunks are all read from the LDS first and then
+// stored, from one base address per thread: as a loop of read, wait, store
+// (with 64-bit address arithmetic in each step) this took most of the
+// cache's cost in the forward.
 __device__ __forceinline__ void store_staged_panels(const char* lds, bf16_t* P, int64_t m0,
                                                     int64_t n0, int64_t Tn, int64_t ld,
                                                     int64_t pld) {
   constexpr int64_t kPanel = 64;
-  for (int k = threadIdx.x; k < 4 * 256 * 8; k += kThreads) {
-    const int pn = k >> 11, tl = (k >> 3) & 255, ch = k & 7;
-    const int64_t t = n0 + tl, c = m0 + pn * 64;
-    if (t >= Tn || c >= ld) continue;
-    const u32x4 val =
-        *reinterpret_cast<const u32x4*>(lds + pn * 32768 + tl * 128 + ((ch ^ (tl & 7)) << 4));
-    __builtin_nontemporal_store(
-        val, reinterpret_cast<u32x4*>(P + (c / kPanel) * pld * kPanel + t * kPanel + ch * 8));
+  constexpr int kRows = kThreads / 8;            // token rows per round
+  constexpr int kRounds = 256 / kRows;           // rounds per panel
+  constexpr int kIters = 4 * kRounds;
+  const int ch = threadIdx.x & 7, r0 = threadIdx.x >> 3;
+  const int sw = (ch ^ (r0 & 7)) << 4;           // kRows is a multiple of 8
+  u32x4 v[kIters];
+#pragma unroll
+  for (int it = 0; it < kIters; ++it)
+    v[it] = *reinterpret_cast<const u32x4*>(lds + (it / kRounds) * 32768 +
+                                            ((it % kRounds) * kRows + r0) * 128 + sw);
+  bf16_t* const base = P + (m0 / kPanel) * pld * kPanel + (n0 + r0) * kPanel + ch * 8;
+#pragma unroll
+  for (int it = 0; it < kIters; ++it) {
+    const int pn = it / kRounds, tl = (it % kRounds) * kRows + r0;
+    if (n0 + tl < Tn && m0 + pn * kPanel < ld)
+      __builtin_nontemporal_store(
+          v[it], reinterpret_cast<u32x4*>(base + pn * pld * kPanel +
+                                          int64_t((it % kRounds) * kRows) * kPanel));
   }
 }
 
