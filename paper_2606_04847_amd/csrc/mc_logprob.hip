@@ -285,11 +285,26 @@ __device__ __forceinline__ Lse3 fold_tiles(const float* __restrict__ pm,
                                            int64_t t, float (*sh)[8][64]) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   Lse3 acc;
-  if (t < T)
-    for (int j = w; j < nT; j += 8) {
+  if (t < T) {
+    // four tiles' partials are loaded before they are folded (same order)
+    int j = w;
+    for (; j + 24 < nT; j += 32) {
+      float m4[4], s4[4], u4[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t o = int64_t(j + 8 * q) * T + t;
+        m4[q] = pm[o];
+        s4[q] = ps[o];
+        u4[q] = pu ? pu[o] : 0.0f;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc.add(m4[q], s4[q], u4[q]);
+    }
+    for (; j < nT; j += 8) {
       const int64_t o = int64_t(j) * T + t;
       acc.add(pm[o], ps[o], pu ? pu[o] : 0.0f);
     }
+  }
   sh[0][w][lane] = acc.m;
   sh[1][w][lane] = acc.s;
   sh[2][w][lane] = acc.u;
