@@ -38,17 +38,17 @@ PEAK_FP32_TFLOPS = 157.3
 # the kernel sources with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "89ad65df62fb23cf00c5428c95b78f287ce26a37e30086ab9ae8d1ee8371718a",
+        "4ea36eac2f2bade72a846fdbfaea22c9dbbfabf1de7686558141baea982c02b0",
     "bytes_per_launch": {
-        "logprob_fwd_gemm": 35776496589,
-        "logprob_fwd_merge": 78254638,
-        "rl_loss": 91896,
-        "logprob_bwd_bucket": 1328759,
-        "logprob_bwd_cache_probs": 6307905290,
-        "logprob_bwd_transpose": 1378909526,
-        "logprob_bwd_dhidden": 30298377440,
-        "logprob_bwd_dweight": 32539418634,
-        "logprob_bwd_onehot_dw": 176661100,
+        "logprob_fwd_gemm": 36081671967,
+        "logprob_fwd_merge": 78294396,
+        "rl_loss": 91895,
+        "logprob_bwd_bucket": 1330709,
+        "logprob_bwd_cache_probs": 6307923785,
+        "logprob_bwd_transpose": 1378914300,
+        "logprob_bwd_dhidden": 30280244998,
+        "logprob_bwd_dweight": 32537844447,
+        "logprob_bwd_onehot_dw": 176637559,
     },
 }
 
