@@ -267,3 +267,52 @@ def test_cached_fullsize_sampled(cid):
     assert rel_fro(dW[torch.from_numpy(vrows).cuda()].cpu().numpy(), dW_o) <= GRAD_RTOL
     del dH, dW, cache
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("path", ["cached", "recompute"])
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_zero_dlogp_rows_and_shared_targets(path, accumulate):
+    # Tokens outside the loss mask reach the backward with dlogp exactly 0:
+    # their softmax rows are written as zeros without being read, they are
+    # skipped in dW's one-hot scatter, and a target whose tokens all have
+    # zero dlogp leaves its dW row to the contraction alone.  Few distinct
+    # targets so that buckets mix zero and nonzero tokens and some hold
+    # only zero ones.
+    cfg = scaled_config(4, T=700, n_groups=2, group_size=8, d=136, V=300, hi=100, seed=23,
+                        drift=_drift(16))
+    case = small_case(cfg)
+    T = len(case["y"])
+    rng = np.random.default_rng(7)
+    y = rng.integers(0, 40, T).astype(np.int64)
+    dl = rng.normal(0.0, 1e-3, T).astype(np.float32)
+    dl[rng.random(T) < 0.6] = 0.0
+    dl[y < 8] = 0.0                                  # buckets of only zero-dlogp tokens
+    assert (dl == 0).any() and (dl != 0).any()
+    _, lse_o = oracle.logprob_fwd(case["H"], case["W"], y)
+    dH_o, dW_o = oracle.logprob_bwd(case["H"], case["W"], y, lse_o, dl.astype(np.float64))
+
+    mc = _mc()
+    H, W, _ = device_tensors(case)
+    yd = torch.from_numpy(y).cuda()
+    dld = torch.from_numpy(dl).cuda()
+    base_h = torch.full((T, H.shape[1]), 0.5, device="cuda") if accumulate else None
+    base_w = torch.full((W.shape[0], W.shape[1]), -0.25, device="cuda") if accumulate else None
+    kw = dict(dhidden=base_h, dweight=base_w, accumulate_dhidden=accumulate,
+              accumulate_dweight=accumulate)
+    if path == "cached":
+        cache = mc.softmax_cache(H, W)
+        _, lse = mc.logprob_fwd_cached(H, W, yd, cache)
+        dH, dW = mc.logprob_bwd_cached(H, W, yd, lse, dld, cache, **kw)
+    else:
+        _, lse = mc.logprob_fwd(H, W, yd)
+        dH, dW = mc.logprob_bwd(H, W, yd, lse, dld, **kw)
+    torch.cuda.synchronize()
+    dH, dW = dH.cpu().numpy().astype(np.float64), dW.cpu().numpy().astype(np.float64)
+    if accumulate:
+        dH -= 0.5
+        dW += 0.25
+    assert np.isfinite(dH).all() and np.isfinite(dW).all()
+    assert rel_fro(dH, dH_o) <= GRAD_RTOL
+    assert rel_fro(dW, dW_o) <= GRAD_RTOL
+    # a token with zero dlogp has a zero gradient row exactly
+    assert (dH[dl == 0] == 0).all()
