@@ -634,12 +634,23 @@ __global__ void k_fill_i32(int* __restrict__ p, int64_t n, int v) {
   if (i < n) p[i] = v;
 }
 
-__global__ void k_hist(const int64_t* __restrict__ y, int64_t T, int64_t v_off, int64_t V,
-                       int* __restrict__ counts) {
+// Also counts into counts[V] the tokens whose gradient row is live (a
+// target in range and a nonzero dlogp): one atomic per workgroup of 256.
+__global__ __launch_bounds__(256) void k_hist(const int64_t* __restrict__ y,
+                                              const float* __restrict__ dlogp, int64_t T,
+                                              int64_t v_off, int64_t V, int* __restrict__ counts) {
+  __shared__ int wave_live[4];
   const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (t >= T) return;
-  const int64_t yy = y[t] - v_off;
-  if (yy >= 0 && yy < V) atomicAdd(counts + yy, 1);
+  const int64_t yy = t < T ? y[t] - v_off : -1;
+  const bool in = yy >= 0 && yy < V;
+  const uint64_t live = __ballot(in && dlogp[t] != 0.0f);
+  if ((threadIdx.x & 63) == 0) wave_live[threadIdx.x >> 6] = int(__popcll(live));
+  if (in) atomicAdd(counts + yy, 1);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int n = wave_live[0] + wave_live[1] + wave_live[2] + wave_live[3];
+    if (n) atomicAdd(counts + V, n);
+  }
 }
 
 // Exclusive scan of counts[V] into offsets[V + 1] in two passes over blocks
@@ -769,14 +780,18 @@ __global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
 // Named kernels, one per role of the shared tile core.
 // Softmax cache -> backward operand, in place: P~[t, v] = -dlogp_t
 // exp(cm[v / kWaveRows][t] - lse_t) E[t, v] (0 for ignored tokens).
-// Grid: x over groups of kCachePanels consecutive panels, y over blocks of
-// 32 tokens from block tb0; thread = one 16-byte chunk of one row of each
-// of those panels (8 lanes per 128-byte row).  Consecutive workgroups walk
-// the panels of one token block, so the writes in flight at any time are
-// 4 KiB pieces spread over many panels (2 MiB apart at the headline shape):
-// 1.36 ms against 1.51 with the tokens walked first, and 4 panels per
-// thread against 1.45-2.6 ms for 1, 2, 3, 6 or 8 (measured).  The stream is
-// touched once: non-temporal loads and stores.  Where the factor is exactly zero (a
+// Workgroup = one group of kCachePanels consecutive panels x one block of
+// 32 tokens; thread = one 16-byte chunk of one row of each of those panels
+// (8 lanes per 128-byte row).  The order of the workgroups follows the
+// number of live tokens (nonzero factor), counted by the bucketing pass:
+// with few of them the pass is mostly writes, and walking the panels of one
+// token block first spreads the 4 KiB pieces in flight over many panels
+// (headline workload, 27% live: 1.36 ms against 1.50); with most tokens live
+// it streams reads and writes in place, and walking the tokens of one panel
+// group first is faster (all live: 1.68 against 1.86 ms at the headline
+// shape, 11.35 against 12.19 ms at T = 65536, V = 248320).  4 panels per
+// thread: 1, 2, 3, 6 or 8 measured 1.45-2.6 ms.  The stream is touched
+// once: non-temporal loads and stores.  Where the factor is exactly zero (a
 // token whose dlogp is zero: outside the loss mask, in a filtered sequence
 // or clipped; an ignored target; a block past the vocabulary) the chunk is
 // written as zeros without reading it: the cached values are finite, so
@@ -789,16 +804,21 @@ __global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
                                                         const float* __restrict__ dlogp,
                                                         const int64_t* __restrict__ y,
                                                         int64_t Tn, int64_t V, int64_t pld,
-                                                        int64_t tb0, int64_t npanels) {
+                                                        int64_t npanels, uint32_t ngroups,
+                                                        const int* __restrict__ live) {
   constexpr int BV = 128 / sizeof(T);   // panel width
   constexpr int CE = 16 / sizeof(T);    // entries per chunk
-  const int64_t t = (tb0 + int64_t(blockIdx.y)) * 32 + (threadIdx.x >> 3);
+  const uint32_t nblocks = uint32_t((Tn + 31) / 32);
+  const bool sparse = live != nullptr && 2 * int64_t(*live) < Tn;
+  const uint32_t gi = sparse ? blockIdx.x % ngroups : blockIdx.x / nblocks;
+  const uint32_t tb = sparse ? blockIdx.x / ngroups : blockIdx.x % nblocks;
+  const int64_t t = int64_t(tb) * 32 + (threadIdx.x >> 3);
   if (t >= Tn) return;
   const int ch = threadIdx.x & 7;
   const int64_t yy = y[t];
   const float g = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
   const float l = lse[t];
-  const int64_t p0 = int64_t(blockIdx.x) * kCachePanels;
+  const int64_t p0 = int64_t(gi) * kCachePanels;
   u32x4 raw[kCachePanels];
   float f[kCachePanels];
 #pragma unroll
@@ -985,7 +1005,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   T* P = cacheE ? cacheE : cv.take<T>(size_t(pld) * ld);
   T* Wt = cv.take<T>(size_t(d) * ld);    // [d x chunk] transpose of W's chunk rows
   T* Ht = cv.take<T>(size_t(d) * pld);   // [d x T] transpose of H
-  int* counts = cv.take<int>(Vs);
+  int* counts = cv.take<int>(Vs + 1);   // counts[Vs]: live tokens
   int* cursor = cv.take<int>(Vs);
   int* offsets = cv.take<int>(Vs + 1);
   int* unsorted = cv.take<int>(Tn);
@@ -1003,9 +1023,9 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   if (dW) {
     ProfScope ps_(s, "logprob_bwd_bucket", 0.0, 32.0 * Tn + 16.0 * Vs);
     const int nb = int(cdiv(Vs, 256)), tb = int(cdiv(Tn, 256));
-    hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, counts, Vs, 0);
+    hipLaunchKernelGGL(k_fill_i32, dim3(nb + 1), dim3(256), 0, s, counts, Vs + 1, 0);
     hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, cursor, Vs, 0);
-    hipLaunchKernelGGL(k_hist, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, counts);
+    hipLaunchKernelGGL(k_hist, dim3(tb), dim3(256), 0, s, y, dlogp, Tn, v_off, Vs, counts);
     const int nsb = int(cdiv(Vs, kScanBlock));
     hipLaunchKernelGGL(k_scan_sums, dim3(nsb), dim3(256), 0, s, counts, Vs, scan_sums);
     hipLaunchKernelGGL(k_scan_apply, dim3(nsb), dim3(256), 0, s, counts, Vs, scan_sums, offsets);
@@ -1026,11 +1046,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       ProfScope ps_(s, "logprob_bwd_cache_probs", 0.0, es * double(Tn) * ldc + 4.0 * Tn * 5);
       const int64_t panels = ldc / (128 / int64_t(sizeof(T)));
       const int64_t groups = cdiv(panels, kCachePanels), blocks = cdiv(Tn, 32);
-      for (int64_t b0 = 0; b0 < blocks; b0 += 65535) {   // grid y is at most 65535
-        const unsigned nb = unsigned(std::min<int64_t>(65535, blocks - b0));
-        hipLaunchKernelGGL(k_cache_to_probs<T>, dim3(unsigned(groups), nb), dim3(256), 0, s, P,
-                           cacheM, lse, dlogp, y, Tn, V, pld, b0, panels);
-      }
+      if (groups * blocks > int64_t(0x7fffffff)) return hipErrorInvalidValue;
+      // the live-token count comes with the bucketing (run when dW is wanted)
+      hipLaunchKernelGGL(k_cache_to_probs<T>, dim3(unsigned(groups * blocks)), dim3(256), 0, s,
+                         P, cacheM, lse, dlogp, y, Tn, V, pld, panels, uint32_t(groups),
+                         dW ? counts + Vs : nullptr);
     } else {
       // tile rows: chunk columns (up to the padded width ldc), tile columns: tokens
       Operand A{Wc, d, width, d}, B{H, d, Tn, d};
@@ -1130,7 +1150,7 @@ size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   const size_t pld = size_t(cdiv(T, 64)) * 64;
   size_t n = align_up(size_t(d) * ld * es, kWsAlign);
   n += align_up(size_t(d) * pld * es, kWsAlign);
-  n += 2 * align_up(size_t(V) * 4, kWsAlign);
+  n += align_up(size_t(V + 1) * 4, kWsAlign) + align_up(size_t(V) * 4, kWsAlign);
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
   n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
@@ -1146,7 +1166,7 @@ size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   size_t n = align_up(pld * ld * es, kWsAlign);
   n += align_up(size_t(d) * ld * es, kWsAlign);
   n += align_up(size_t(d) * pld * es, kWsAlign);
-  n += 2 * align_up(size_t(V) * 4, kWsAlign);
+  n += align_up(size_t(V + 1) * 4, kWsAlign) + align_up(size_t(V) * 4, kWsAlign);
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
   n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
