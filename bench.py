@@ -38,17 +38,17 @@ PEAK_FP32_TFLOPS = 157.3
 # the kernel sources with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "4ea36eac2f2bade72a846fdbfaea22c9dbbfabf1de7686558141baea982c02b0",
+        "1594188e4715e5fcee36035359920661c238767c4ed47d3fae05d3022f09f279",
     "bytes_per_launch": {
-        "logprob_fwd_gemm": 36081671967,
-        "logprob_fwd_merge": 78294396,
-        "rl_loss": 91895,
-        "logprob_bwd_bucket": 1330709,
-        "logprob_bwd_cache_probs": 6307923785,
-        "logprob_bwd_transpose": 1378914300,
-        "logprob_bwd_dhidden": 30280244998,
-        "logprob_bwd_dweight": 32537844447,
-        "logprob_bwd_onehot_dw": 176637559,
+        "logprob_fwd_gemm": 36390683079,
+        "logprob_fwd_merge": 78294570,
+        "rl_loss": 91896,
+        "logprob_bwd_bucket": 1339054,
+        "logprob_bwd_cache_probs": 6307788885,
+        "logprob_bwd_transpose": 1378915322,
+        "logprob_bwd_dhidden": 30539571966,
+        "logprob_bwd_dweight": 32541790369,
+        "logprob_bwd_onehot_dw": 176637033,
     },
 }
 
