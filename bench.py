@@ -38,17 +38,17 @@ PEAK_FP32_TFLOPS = 157.3
 # the kernel sources with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "1594188e4715e5fcee36035359920661c238767c4ed47d3fae05d3022f09f279",
+        "4fd5ae0e70ff241c11156f6c4cd0eff374332b9ecf5b799e931b940bfc0eb1ae",
     "bytes_per_launch": {
-        "logprob_fwd_gemm": 36390683079,
-        "logprob_fwd_merge": 78294570,
+        "logprob_fwd_gemm": 35759080788,
+        "logprob_fwd_merge": 78294580,
         "rl_loss": 91896,
-        "logprob_bwd_bucket": 1339054,
-        "logprob_bwd_cache_probs": 6307788885,
-        "logprob_bwd_transpose": 1378915322,
-        "logprob_bwd_dhidden": 30539571966,
-        "logprob_bwd_dweight": 32541790369,
-        "logprob_bwd_onehot_dw": 176637033,
+        "logprob_bwd_bucket": 1338976,
+        "logprob_bwd_cache_probs": 6307710964,
+        "logprob_bwd_transpose": 1378916044,
+        "logprob_bwd_dhidden": 30274365503,
+        "logprob_bwd_dweight": 32536170929,
+        "logprob_bwd_onehot_dw": 176654837,
     },
 }
 
