@@ -45,6 +45,23 @@ a convention; the paper prints no number that pins them):
       gradient is d k3 / d logp = 1 - exp(r).  Parity of this estimator with
       the paper is unpinned (the paper prints none); its arithmetic is pinned
       by closed forms and finite differences.
+  R12 token-level truncation of the importance ratio (TIS, named in Sec. 4.5.2
+      as an alternative to sequence masking, defined there by no formula):
+      the policy-gradient weight rho_t A_i of a retained token is truncated
+      at a cap C, i.e. its term of Eq. 17 is multiplied by the stop-gradient
+      factor w_t = min(1, C / rho_t) = exp(min(0, ln C - ell_t)), so its
+      gradient with respect to ell_t is min(rho_t, C) A_i on the unclipped
+      branch.  C is a parameter (default 2); parity of this definition with
+      the paper is unpinned.
+  R13 token-level hard filtering of the importance ratio (IcePop, named in
+      Sec. 4.5.2, defined there by no formula): a retained token whose ratio
+      lies outside [alpha, beta] (decided in log space, ln alpha <= ell_t <=
+      ln beta kept) contributes neither to the surrogate sum nor to the
+      gradient; it still counts in N, in L_i and in the statistics of Eq. 18-21.
+      alpha, beta are parameters (defaults 0.5, 2); parity of this definition
+      with the paper is unpinned.
+      Either mode combines with any sequence filter; `token_frac` reports the
+      share of the N tokens it truncated (TIS) or dropped (IcePop).
 """
 from __future__ import annotations
 
@@ -54,6 +71,7 @@ import math
 import numpy as np
 
 FILTERS = ("none", "vanilla", "mirrorpop")
+TOKEN_MODES = ("none", "tis", "icepop")
 
 
 @dataclasses.dataclass
@@ -65,6 +83,10 @@ class RLParams:
     std_ddof: int = 0
     filter: str = "mirrorpop"
     kl_beta: float = 0.0
+    token_mode: str = "none"      # R12 / R13
+    tis_cap: float = 2.0          # C of R12
+    icepop_lo: float = 0.5        # alpha of R13
+    icepop_hi: float = 2.0        # beta of R13
 
 
 def _advantages(rewards, cu_groups, p: RLParams) -> np.ndarray:
@@ -90,6 +112,8 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
     p = params or RLParams()
     if p.filter not in FILTERS:
         raise ValueError(p.filter)
+    if p.token_mode not in TOKEN_MODES:
+        raise ValueError(p.token_mode)
     logp = np.asarray(logp, dtype=np.float64)
     logp_rollout = np.asarray(logp_rollout, dtype=np.float64)
     T = len(logp)
@@ -126,10 +150,15 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
     N = int((seq_len * keep).sum())
 
     lo, hi = 1.0 - p.eps_low, 1.0 + p.eps_high
+    # R12 / R13 bounds in log space (float parameters widened to fp64)
+    log_cap = math.log(float(np.float32(p.tis_cap)))
+    log_alo = math.log(float(np.float32(p.icepop_lo)))
+    log_ahi = math.log(float(np.float32(p.icepop_hi)))
     dlogp = np.zeros(T, dtype=np.float64)
     total = 0.0
     kl_total = 0.0
     n_clipped = 0
+    n_token = 0
     use_kl = logp_ref is not None and p.kl_beta != 0.0
     if use_kl:
         logp_ref = np.asarray(logp_ref, dtype=np.float64)
@@ -140,13 +169,22 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
         for t in range(s, e):
             if not mask[t]:
                 continue
-            unclipped = rho[t] * A[i]
-            clipped = min(max(rho[t], lo), hi) * A[i]
-            total += min(unclipped, clipped)
-            if unclipped <= clipped:                      # R9
-                dlogp[t] = unclipped                      # d(rho A)/d ell = rho A
-            else:
-                n_clipped += 1
+            weight = 1.0
+            dropped = False
+            if p.token_mode == "tis" and ell[t] > log_cap:          # R12
+                weight = math.exp(log_cap - ell[t])
+                n_token += 1
+            elif p.token_mode == "icepop" and not (log_alo <= ell[t] <= log_ahi):   # R13
+                dropped = True
+                n_token += 1
+            if not dropped:
+                unclipped = rho[t] * A[i]
+                clipped = min(max(rho[t], lo), hi) * A[i]
+                total += weight * min(unclipped, clipped)
+                if unclipped <= clipped:                      # R9
+                    dlogp[t] = weight * unclipped             # d(rho A)/d ell = rho A
+                else:
+                    n_clipped += 1
             if use_kl:                                    # R11
                 r = logp_ref[t] - logp[t]
                 kl_total += math.exp(r) - r - 1.0
@@ -157,10 +195,12 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
         loss = -total / N + (p.kl_beta * kl_total / N if use_kl else 0.0)
         dlogp *= -1.0 / N
         clip_frac = n_clipped / N
+        token_frac = n_token / N
         kl = kl_total / N
     else:                                                 # R8
-        loss, clip_frac, kl = 0.0, 0.0, 0.0
+        loss, clip_frac, token_frac, kl = 0.0, 0.0, 0.0, 0.0
         dlogp[:] = 0.0
     return dict(loss=loss, dlogp=dlogp, seq_mask=keep.astype(np.uint8),
                 seq_len=seq_len.astype(np.int32), n_valid=N, adv=A,
-                stat_abs=stat_abs, stat_signed=stat_signed, clip_frac=clip_frac, kl=kl)
+                stat_abs=stat_abs, stat_signed=stat_signed, clip_frac=clip_frac,
+                token_frac=token_frac, kl=kl)

@@ -184,3 +184,97 @@ def test_dlogp_matches_central_differences(seed):
             continue   # the filter decision itself moved: no derivative
         fd = (fp["loss"] - fm["loss"]) / (2 * h)
         assert abs(fd - out["dlogp"][t]) < 1e-7
+
+
+# ---------------------------------------------------------------------------
+# Token-level modes (readings R12 / R13 of the oracle)
+# ---------------------------------------------------------------------------
+def _token_params(g, mode):
+    kw = dict(g["params"])
+    return RLParams(token_mode=mode, **kw)
+
+
+@pytest.mark.parametrize("mode", ["none", "tis", "icepop"])
+def test_hand_derived_token_modes(mode):
+    g = _load("token_modes.json")
+    ell = np.log(np.array(g["rho"]))
+    out = rl_loss(ell, np.zeros_like(ell), None, np.array(g["cu_seqlens"]),
+                  np.array(g["cu_groups"]), np.array(g["rewards"]), _token_params(g, mode))
+    want = g["modes"][mode]
+    np.testing.assert_allclose(out["adv"], g["adv"], rtol=0, atol=1e-15)
+    assert out["n_valid"] == g["n_valid"]
+    assert abs(out["loss"] - want["loss"]) < 1e-14
+    np.testing.assert_allclose(out["dlogp"], want["dlogp"], rtol=0, atol=1e-14)
+    assert abs(out["clip_frac"] - want["clip_frac"]) < 1e-15
+    assert abs(out["token_frac"] - want["token_frac"]) < 1e-15
+
+
+@pytest.mark.parametrize("mode", ["tis", "icepop"])
+def test_token_modes_without_tokens_outside_bounds_equal_the_base_loss(mode):
+    # every ratio inside [0.5, 2] (and below the cap 2): nothing to truncate or
+    # drop, so the objective and its gradient are those of Eq. 17 unchanged
+    cu, groups, mask, rewards, logp, rng = _batch(21)
+    lr = logp + rng.normal(0, 0.1, size=len(logp))
+    assert np.all(np.abs(logp - lr) < math.log(2.0) - 1e-3)
+    base = rl_loss(logp, lr, mask, cu, groups, rewards, RLParams(delta=0.3))
+    out = rl_loss(logp, lr, mask, cu, groups, rewards, RLParams(delta=0.3, token_mode=mode))
+    assert out["loss"] == base["loss"] and np.array_equal(out["dlogp"], base["dlogp"])
+    assert out["token_frac"] == 0.0 and out["clip_frac"] == base["clip_frac"]
+
+
+def test_token_modes_reduce_to_the_base_loss_in_their_limits():
+    # an unbounded cap / interval touches no token
+    cu, groups, mask, rewards, logp, rng = _batch(22)
+    lr = logp + rng.normal(0, 1.0, size=len(logp))
+    p = dict(delta=10.0, filter="none")
+    base = rl_loss(logp, lr, mask, cu, groups, rewards, RLParams(**p))
+    tis = rl_loss(logp, lr, mask, cu, groups, rewards,
+                  RLParams(token_mode="tis", tis_cap=1e30, **p))
+    ice = rl_loss(logp, lr, mask, cu, groups, rewards,
+                  RLParams(token_mode="icepop", icepop_lo=1e-30, icepop_hi=1e30, **p))
+    for o in (tis, ice):
+        assert o["loss"] == base["loss"] and np.array_equal(o["dlogp"], base["dlogp"])
+
+
+def test_tis_truncated_tokens_keep_a_bounded_gradient():
+    # a negative-advantage token far above the clip range: on the unclipped
+    # branch of Eq. 5 its gradient grows with rho; truncated it stays at C A
+    cu = np.array([0, 1, 2], np.int32)
+    groups = np.array([0, 2], np.int32)
+    rewards = np.array([1.0, 0.0])                  # A = (+1, -1) with eps 0
+    for rho in (3.0, 30.0, 3000.0):
+        ell = np.array([0.0, math.log(rho)])
+        p = RLParams(filter="none", adv_eps=0.0, token_mode="tis", tis_cap=2.0)
+        out = rl_loss(ell, np.zeros(2), None, cu, groups, rewards, p)
+        assert abs(out["dlogp"][1] - 2.0 / 2) < 1e-15          # -(1/N) C A, N = 2
+        base = rl_loss(ell, np.zeros(2), None, cu, groups, rewards,
+                       RLParams(filter="none", adv_eps=0.0))
+        assert abs(base["dlogp"][1] - rho / 2) < 1e-12 * rho
+
+
+@pytest.mark.parametrize("seed", [23, 24])
+def test_icepop_dlogp_matches_central_differences(seed):
+    # the IcePop mask is piecewise constant in logp, so away from its bounds
+    # (and from the clip kinks) the gradient is the derivative of the loss
+    cu, groups, mask, rewards, logp, rng = _batch(seed)
+    lr = logp + rng.normal(0, 0.6, size=len(logp))
+    p = RLParams(delta=10.0, token_mode="icepop", icepop_lo=0.7, icepop_hi=1.6)
+    out = rl_loss(logp, lr, mask, cu, groups, rewards, p)
+    assert 0.0 < out["token_frac"] < 1.0
+    h = 1e-7
+    edges = [math.log(1 - p.eps_low), math.log(1 + p.eps_high),
+             math.log(float(np.float32(0.7))), math.log(float(np.float32(1.6)))]
+    checked = 0
+    for t in range(len(logp)):
+        ell = logp[t] - lr[t]
+        if min(abs(ell - e) for e in edges) < 1e-4:
+            continue
+        lp, lm = logp.copy(), logp.copy()
+        lp[t] += h
+        lm[t] -= h
+        fp = rl_loss(lp, lr, mask, cu, groups, rewards, p)
+        fm = rl_loss(lm, lr, mask, cu, groups, rewards, p)
+        fd = (fp["loss"] - fm["loss"]) / (2 * h)
+        assert abs(fd - out["dlogp"][t]) < 1e-7
+        checked += 1
+    assert checked > len(logp) // 2
