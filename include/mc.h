@@ -6,14 +6,22 @@
  *   - the trainer-side per-token log-probability log pi_theta(o_t | x, o_<t)
  *     over the full vocabulary (the numerator of the importance ratio of
  *     Eq. 4): logits z = hidden . weight^T are reduced in the GEMM epilogue by
- *     an online log-sum-exp and a gather of the target logit, and are never
- *     written to memory;
+ *     an online log-sum-exp and a gather of the target logit.  In the plain
+ *     pair (mc_logprob_fwd / mc_logprob_bwd) the logits are never written to
+ *     memory: the forward keeps only per-row partials and the backward
+ *     recomputes the logits, writing their gradient (a bf16 transient per
+ *     vocabulary chunk) as the operand of its two contractions.  The cached
+ *     pair (mc_logprob_fwd_cached / mc_logprob_bwd_cached) trades memory for
+ *     that recomputation: its forward writes a [T, V] softmax cache;
  *   - its backward (chain rule through the log-softmax);
  *   - the RL objective on top of it: log importance ratios (Eq. 4), the
  *     MirrorPop sequence statistic and mask (Eq. 19-21) or the signed one
- *     (Eq. 18), group-normalised advantages (Eq. 3 / Eq. 12) and the
- *     sequence-masked clipped surrogate (Eq. 17 with the KL weight beta = 0),
- *     with its gradient with respect to the per-token log-probs.
+ *     (Eq. 18), optional token-level truncation or dropping of the ratio
+ *     (Sec. 4.5.2), group-normalised advantages (Eq. 3 / Eq. 12), the
+ *     sequence-masked clipped surrogate and the KL term beta D_KL of Eq. 17
+ *     (beta a parameter, 0 unless a reference policy's log-probs are passed;
+ *     the paper names no estimator, this library uses k3), with its gradient
+ *     with respect to the per-token log-probs.
  *
  * Conventions shared by every entry point
  *   Memory      Every array argument is caller-owned DEVICE memory unless a
@@ -65,6 +73,20 @@ typedef enum {
   MC_FILTER_MIRRORPOP = 2   /* (1/L_i) sum_t |log rho_t| <= delta (Eq. 21) */
 } mc_filter_t;
 
+/* Token-level treatment of the importance ratio, the alternatives to
+ * sequence masking that Sec. 4.5.2 names (truncated importance sampling and
+ * IcePop) without giving formulas; the definitions below are this library's
+ * readings.  Both combine with any mc_filter_t and act on retained tokens
+ * (loss mask set, M_i = 1) only. */
+typedef enum {
+  MC_TOKEN_NONE = 0,        /* plain Eq. 17 */
+  MC_TOKEN_TIS = 1,         /* a token with rho_t > tis_cap has its term scaled by the
+                               stop-gradient factor tis_cap / rho_t: its gradient
+                               weight rho_t A_i is truncated to tis_cap A_i */
+  MC_TOKEN_ICEPOP = 2       /* a token with rho_t outside [icepop_lo, icepop_hi] adds
+                               nothing to the loss or the gradient (it still counts in N) */
+} mc_token_mode_t;
+
 /* Parameters of the objective (host struct). */
 typedef struct {
   float eps_low;            /* lower clip width of Eq. 5/17; ratio >= 1-eps_low, 0 <= eps_low < 1 */
@@ -75,6 +97,10 @@ typedef struct {
   int32_t filter;           /* an mc_filter_t */
   float kl_beta;            /* weight beta of the KL term of Eq. 5/17 (>= 0); used only
                                when a reference log-prob array is passed */
+  int32_t token_mode;       /* an mc_token_mode_t */
+  float tis_cap;            /* MC_TOKEN_TIS: cap C > 0 of the ratio (default 2) */
+  float icepop_lo;          /* MC_TOKEN_ICEPOP: 0 < icepop_lo <= icepop_hi (defaults 0.5, 2); */
+  float icepop_hi;          /*   ratios are compared in log space, bounds inclusive */
 } mc_rl_params_t;
 
 /* Outputs of mc_rl_loss (host struct holding device pointers).  `loss` and
@@ -91,6 +117,8 @@ typedef struct {
   float* clip_frac;         /* [1]  share of the N tokens on the clipped branch */
   int32_t* error_flag;      /* [1]  set to 1 when cu_seqlens/cu_groups are inconsistent */
   float* kl;                /* [1]  (1/N) sum_i M_i sum_t k3_t (0 without a reference) */
+  float* token_frac;        /* [1]  share of the N tokens the token mode truncated (TIS)
+                                    or dropped (IcePop); 0 for MC_TOKEN_NONE */
 } mc_rl_outputs_t;
 
 /* Flags of mc_logprob_bwd. */

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(PKG, "libmc.so")
 MC_OK, MC_ERR_INVALID_ARG, MC_ERR_UNSUPPORTED, MC_ERR_WORKSPACE, MC_ERR_HIP = range(5)
 MC_F32, MC_BF16 = 0, 1
 MC_FILTER = {"none": 0, "vanilla": 1, "mirrorpop": 2}
+MC_TOKEN = {"none": 0, "tis": 1, "icepop": 2}
 MC_BWD_ACCUMULATE_DHIDDEN = 1
 MC_BWD_ACCUMULATE_DWEIGHT = 2
 
@@ -27,11 +28,13 @@ class RLParamsC(ctypes.Structure):
     _fields_ = [("eps_low", ctypes.c_float), ("eps_high", ctypes.c_float),
                 ("delta", ctypes.c_float), ("adv_eps", ctypes.c_float),
                 ("std_ddof", ctypes.c_int32), ("filter", ctypes.c_int32),
-                ("kl_beta", ctypes.c_float)]
+                ("kl_beta", ctypes.c_float), ("token_mode", ctypes.c_int32),
+                ("tis_cap", ctypes.c_float), ("icepop_lo", ctypes.c_float),
+                ("icepop_hi", ctypes.c_float)]
 
 
 _OUT_FIELDS = ("loss", "dlogp", "seq_mask", "seq_len", "n_valid", "adv", "stat_abs",
-               "stat_signed", "clip_frac", "error_flag", "kl")
+               "stat_signed", "clip_frac", "error_flag", "kl", "token_frac")
 
 
 class RLOutputsC(ctypes.Structure):
@@ -53,10 +56,16 @@ class RLParams:
     std_ddof: int = 0
     filter: str = "mirrorpop"
     kl_beta: float = 0.0
+    token_mode: str = "none"
+    tis_cap: float = 2.0
+    icepop_lo: float = 0.5
+    icepop_hi: float = 2.0
 
     def to_c(self) -> RLParamsC:
         return RLParamsC(self.eps_low, self.eps_high, self.delta, self.adv_eps,
-                         int(self.std_ddof), MC_FILTER[self.filter], self.kl_beta)
+                         int(self.std_ddof), MC_FILTER[self.filter], self.kl_beta,
+                         MC_TOKEN[self.token_mode], self.tis_cap, self.icepop_lo,
+                         self.icepop_hi)
 
 
 class MCError(RuntimeError):
@@ -170,14 +179,36 @@ def _check(status, what):
         raise MCError(status, what)
 
 
-def _workspace(nbytes, device, workspace=None):
+def _workspace(nbytes, device, workspace=None, owned=None):
+    """The caller's workspace when it is large enough, else a new one (added
+    to `owned`, the list of tensors this wrapper allocated)."""
     torch = _torch()
     if nbytes == 0:
         return None, 0
     if workspace is not None and workspace.numel() >= nbytes:
         return workspace, workspace.numel()
     ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    if owned is not None:
+        owned.append(ws)
     return ws, nbytes
+
+
+def _new(owned, *shape, dtype, device):
+    """An uninitialised device tensor allocated by a wrapper (kept in `owned`)."""
+    t = _torch().empty(*shape, dtype=dtype, device=device)
+    owned.append(t)
+    return t
+
+
+def _keep_alive(stream, *tensors):
+    """Memory a wrapper allocated on the current stream but handed to kernels
+    enqueued on another stream: record that stream on it, so the caching
+    allocator does not reuse it before that stream's work is done."""
+    if stream is None:
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(stream)
 
 
 def _need(cond, msg):
@@ -204,15 +235,18 @@ def logprob_fwd(hidden, weight, targets, *, logp=None, lse=None, entropy=None,
     _need(weight.shape[1] == d and targets.shape == (T,), "shape mismatch")
     dt = _dtype_code(hidden)
     dev = hidden.device
-    logp = torch.empty(T, dtype=torch.float32, device=dev) if logp is None else logp
-    lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
+    owned = []
+    f32 = torch.float32
+    logp = _new(owned, T, dtype=f32, device=dev) if logp is None else logp
+    lse = _new(owned, T, dtype=f32, device=dev) if lse is None else lse
     if with_entropy and entropy is None:
-        entropy = torch.empty(T, dtype=torch.float32, device=dev)
+        entropy = _new(owned, T, dtype=f32, device=dev)
     need = lib.mc_logprob_fwd_workspace_size(T, d, V, dt)
-    ws, nbytes = _workspace(need, dev, workspace)
+    ws, nbytes = _workspace(need, dev, workspace, owned)
     _check(lib.mc_logprob_fwd(_ptr(hidden), _ptr(weight), _ptr(targets), T, d, V, dt,
                               _ptr(logp), _ptr(lse), _ptr(entropy), _ptr(ws), nbytes,
                               _stream(stream)), "mc_logprob_fwd")
+    _keep_alive(stream, *owned)
     return (logp, lse, entropy) if entropy is not None else (logp, lse)
 
 
@@ -229,12 +263,15 @@ def logprob_fwd_shard(hidden, weight_shard, targets, v_offset, V_total, *, parti
         _need(t.is_cuda and t.is_contiguous(), "contiguous GPU tensors")
     dt = _dtype_code(hidden)
     dev = hidden.device
-    partial = torch.empty(4, T, dtype=torch.float32, device=dev) if partial is None else partial
+    owned = []
+    if partial is None:
+        partial = _new(owned, 4, T, dtype=torch.float32, device=dev)
     need = lib.mc_logprob_fwd_workspace_size(T, d, Vs, dt)
-    ws, nbytes = _workspace(need, dev, workspace)
+    ws, nbytes = _workspace(need, dev, workspace, owned)
     _check(lib.mc_logprob_fwd_shard(_ptr(hidden), _ptr(weight_shard), _ptr(targets), T, d, Vs,
                                     int(v_offset), int(V_total), dt, _ptr(partial), _ptr(ws),
                                     nbytes, _stream(stream)), "mc_logprob_fwd_shard")
+    _keep_alive(stream, *owned)
     return partial
 
 
@@ -246,12 +283,14 @@ def logprob_merge_shards(partials, targets, V_total, *, with_entropy=True, strea
     _need(four == 4 and partials.dtype == torch.float32 and partials.is_contiguous(),
           "partials [S, 4, T] fp32")
     dev = partials.device
-    logp = torch.empty(T, dtype=torch.float32, device=dev)
-    lse = torch.empty(T, dtype=torch.float32, device=dev)
-    ent = torch.empty(T, dtype=torch.float32, device=dev) if with_entropy else None
+    owned = []
+    logp = _new(owned, T, dtype=torch.float32, device=dev)
+    lse = _new(owned, T, dtype=torch.float32, device=dev)
+    ent = _new(owned, T, dtype=torch.float32, device=dev) if with_entropy else None
     _check(lib.mc_logprob_merge_shards(_ptr(partials), S, _ptr(targets), T, int(V_total),
                                        _ptr(logp), _ptr(lse), _ptr(ent), _stream(stream)),
            "mc_logprob_merge_shards")
+    _keep_alive(stream, *owned)
     return logp, lse, ent
 
 
@@ -266,17 +305,19 @@ def logprob_bwd_shard(hidden, weight_shard, targets, lse, dlogp, v_offset, V_tot
     Vs = weight_shard.shape[0]
     dt = _dtype_code(hidden)
     dev = hidden.device
+    owned = []
     if need_dhidden and dhidden is None:
-        dhidden = torch.empty(T, d, dtype=torch.float32, device=dev)
+        dhidden = _new(owned, T, d, dtype=torch.float32, device=dev)
     if need_dweight and dweight is None:
-        dweight = torch.empty(Vs, d, dtype=torch.float32, device=dev)
+        dweight = _new(owned, Vs, d, dtype=torch.float32, device=dev)
     need = lib.mc_logprob_bwd_workspace_size(T, d, Vs, dt)
-    ws, nbytes = _workspace(need, dev, workspace)
+    ws, nbytes = _workspace(need, dev, workspace, owned)
     _check(lib.mc_logprob_bwd_shard(_ptr(hidden), _ptr(weight_shard), _ptr(targets), _ptr(lse),
                                     _ptr(dlogp), T, d, Vs, int(v_offset), int(V_total), dt,
                                     _ptr(dhidden if need_dhidden else None),
                                     _ptr(dweight if need_dweight else None), 0, _ptr(ws),
                                     nbytes, _stream(stream)), "mc_logprob_bwd_shard")
+    _keep_alive(stream, *owned)
     return (dhidden if need_dhidden else None), (dweight if need_dweight else None)
 
 
@@ -293,10 +334,12 @@ def primeecho_rewards(scores, success=None, n_turns=None, *, alpha=0.75, beta1=0
           "success uint8 [B, Kmax]")
     _need(n_turns is None or (n_turns.dtype == torch.int32 and n_turns.shape == (B,)),
           "n_turns int32 [B]")
-    out = torch.empty(B, dtype=torch.float32, device=scores.device)
+    owned = []
+    out = _new(owned, B, dtype=torch.float32, device=scores.device)
     _check(lib.mc_primeecho_rewards(_ptr(scores), _ptr(success), _ptr(n_turns), B, K,
                                     float(alpha), float(beta1), float(beta2), _ptr(out),
                                     _stream(stream)), "mc_primeecho_rewards")
+    _keep_alive(stream, *owned)
     return out
 
 
@@ -317,10 +360,11 @@ def logprob_bwd(hidden, weight, targets, lse, dlogp, *, dhidden=None, dweight=No
     _need(lse.shape == (T,) and dlogp.shape == (T,) and targets.shape == (T,), "shape mismatch")
     dt = _dtype_code(hidden)
     dev = hidden.device
+    owned = []
     if need_dhidden and dhidden is None:
-        dhidden = torch.empty(T, d, dtype=torch.float32, device=dev)
+        dhidden = _new(owned, T, d, dtype=torch.float32, device=dev)
     if need_dweight and dweight is None:
-        dweight = torch.empty(V, d, dtype=torch.float32, device=dev)
+        dweight = _new(owned, V, d, dtype=torch.float32, device=dev)
     if not need_dhidden:
         dhidden = None
     if not need_dweight:
@@ -328,10 +372,11 @@ def logprob_bwd(hidden, weight, targets, lse, dlogp, *, dhidden=None, dweight=No
     flags = ((MC_BWD_ACCUMULATE_DHIDDEN if accumulate_dhidden else 0)
              | (MC_BWD_ACCUMULATE_DWEIGHT if accumulate_dweight else 0))
     need = lib.mc_logprob_bwd_workspace_size(T, d, V, dt)
-    ws, nbytes = _workspace(need, dev, workspace)
+    ws, nbytes = _workspace(need, dev, workspace, owned)
     _check(lib.mc_logprob_bwd(_ptr(hidden), _ptr(weight), _ptr(targets), _ptr(lse), _ptr(dlogp),
                               T, d, V, dt, _ptr(dhidden), _ptr(dweight), flags, _ptr(ws),
                               nbytes, _stream(stream)), "mc_logprob_bwd")
+    _keep_alive(stream, *owned)
     return dhidden, dweight
 
 
@@ -362,16 +407,19 @@ def logprob_fwd_cached(hidden, weight, targets, cache, *, logp=None, lse=None, e
     _need(weight.shape[1] == d and targets.shape == (T,), "shape mismatch")
     dt = _dtype_code(hidden)
     dev = hidden.device
-    logp = torch.empty(T, dtype=torch.float32, device=dev) if logp is None else logp
-    lse = torch.empty(T, dtype=torch.float32, device=dev) if lse is None else lse
+    owned = []
+    f32 = torch.float32
+    logp = _new(owned, T, dtype=f32, device=dev) if logp is None else logp
+    lse = _new(owned, T, dtype=f32, device=dev) if lse is None else lse
     if with_entropy and entropy is None:
-        entropy = torch.empty(T, dtype=torch.float32, device=dev)
+        entropy = _new(owned, T, dtype=f32, device=dev)
     need = lib.mc_logprob_fwd_workspace_size(T, d, V, dt)
-    ws, nbytes = _workspace(need, dev, workspace)
+    ws, nbytes = _workspace(need, dev, workspace, owned)
     _check(lib.mc_logprob_fwd_cached(_ptr(hidden), _ptr(weight), _ptr(targets), T, d, V, dt,
                                      _ptr(logp), _ptr(lse), _ptr(entropy), _ptr(cache),
                                      cache.numel(), _ptr(ws), nbytes, _stream(stream)),
            "mc_logprob_fwd_cached")
+    _keep_alive(stream, *owned)
     return (logp, lse, entropy) if entropy is not None else (logp, lse)
 
 
@@ -393,10 +441,11 @@ def logprob_bwd_cached(hidden, weight, targets, lse, dlogp, cache, *, dhidden=No
     _need(lse.shape == (T,) and dlogp.shape == (T,) and targets.shape == (T,), "shape mismatch")
     dt = _dtype_code(hidden)
     dev = hidden.device
+    owned = []
     if need_dhidden and dhidden is None:
-        dhidden = torch.empty(T, d, dtype=torch.float32, device=dev)
+        dhidden = _new(owned, T, d, dtype=torch.float32, device=dev)
     if need_dweight and dweight is None:
-        dweight = torch.empty(V, d, dtype=torch.float32, device=dev)
+        dweight = _new(owned, V, d, dtype=torch.float32, device=dev)
     if not need_dhidden:
         dhidden = None
     if not need_dweight:
@@ -404,19 +453,22 @@ def logprob_bwd_cached(hidden, weight, targets, lse, dlogp, cache, *, dhidden=No
     flags = ((MC_BWD_ACCUMULATE_DHIDDEN if accumulate_dhidden else 0)
              | (MC_BWD_ACCUMULATE_DWEIGHT if accumulate_dweight else 0))
     need = lib.mc_logprob_bwd_cached_workspace_size(T, d, V, dt)
-    ws, nbytes = _workspace(need, dev, workspace)
+    ws, nbytes = _workspace(need, dev, workspace, owned)
     _check(lib.mc_logprob_bwd_cached(_ptr(hidden), _ptr(weight), _ptr(targets), _ptr(lse),
                                      _ptr(dlogp), T, d, V, dt, _ptr(cache), cache.numel(),
                                      _ptr(dhidden), _ptr(dweight), flags, _ptr(ws), nbytes,
                                      _stream(stream)), "mc_logprob_bwd_cached")
+    _keep_alive(stream, *owned)
     return dhidden, dweight
 
 
 def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
-            params: RLParams | None = None, *, logp_ref=None, workspace=None, stream=None):
+            params: RLParams | None = None, *, logp_ref=None, workspace=None, stream=None,
+            out=None):
     """RL objective over a packed batch (see mc_rl_loss).  Returns a dict of
     device tensors: loss, dlogp, seq_mask, seq_len, n_valid, adv, stat_abs,
-    stat_signed, clip_frac, error_flag, kl."""
+    stat_signed, clip_frac, error_flag, kl, token_frac (`out` may supply
+    them)."""
     torch = _torch()
     lib = load_library()
     p = params or RLParams()
@@ -433,6 +485,7 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
     for t in (logp, logp_rollout, logp_ref, cu_seqlens, cu_groups, rewards, loss_mask):
         _need(t is None or (t.is_cuda and t.is_contiguous()), "contiguous GPU tensors")
     dev = logp.device
+    given = out
     out = dict(
         loss=torch.empty(1, dtype=torch.float32, device=dev),
         dlogp=torch.empty(T, dtype=torch.float32, device=dev),
@@ -445,15 +498,19 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
         clip_frac=torch.empty(1, dtype=torch.float32, device=dev),
         error_flag=torch.empty(1, dtype=torch.int32, device=dev),
         kl=torch.empty(1, dtype=torch.float32, device=dev),
-    )
-    oc = RLOutputsC(*[out[k].data_ptr() if out[k].numel() else None for k in _OUT_FIELDS])
+        token_frac=torch.empty(1, dtype=torch.float32, device=dev),
+    ) if given is None else given
+    oc = RLOutputsC(*[out[k].data_ptr() if out.get(k) is not None and out[k].numel() else None
+                      for k in _OUT_FIELDS])
     pc = p.to_c()
+    owned = [] if given is not None else list(out.values())
     need = lib.mc_rl_loss_workspace_size(T, B, NG)
-    ws, nbytes = _workspace(need, dev, workspace)
+    ws, nbytes = _workspace(need, dev, workspace, owned)
     _check(lib.mc_rl_loss(_ptr(logp), _ptr(logp_rollout), _ptr(logp_ref), _ptr(loss_mask),
                           _ptr(cu_seqlens),
                           _ptr(cu_groups), _ptr(rewards), T, B, NG, ctypes.byref(pc),
                           ctypes.byref(oc), _ptr(ws), nbytes, _stream(stream)), "mc_rl_loss")
+    _keep_alive(stream, *owned)
     return out
 
 

@@ -228,11 +228,11 @@ size_t mc_rl_loss_workspace_size(int64_t T, int32_t B, int32_t NG) {
   return mc::loss_workspace(T, B, NG);
 }
 
-mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const float* logp_ref,
-                       const uint8_t* loss_mask, const int32_t* cu_seqlens,
-                       const int32_t* cu_groups, const float* rewards, int64_t T, int32_t B,
-                       int32_t NG, const mc_rl_params_t* params, const mc_rl_outputs_t* out,
-                       void* ws, size_t ws_bytes, void* stream) {
+// Argument checks of mc_rl_loss.
+static mc_status_t check_loss_args(const float* logp, const float* logp_rollout,
+                                   const int32_t* cu_seqlens, const int32_t* cu_groups,
+                                   const float* rewards, int64_t T, int32_t B, int32_t NG,
+                                   const mc_rl_params_t* params, const mc_rl_outputs_t* out) {
   if (T < 0 || B < 0 || NG < 0 || T > kMaxDim) return MC_ERR_INVALID_ARG;
   if (!params || !out || !out->loss) return MC_ERR_INVALID_ARG;
   if (B == 0 && T > 0) return MC_ERR_INVALID_ARG;   // tokens outside every sequence
@@ -248,15 +248,35 @@ mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const float
   if (p.filter != MC_FILTER_NONE && p.filter != MC_FILTER_VANILLA &&
       p.filter != MC_FILTER_MIRRORPOP)
     return MC_ERR_INVALID_ARG;
+  if (p.token_mode != MC_TOKEN_NONE && p.token_mode != MC_TOKEN_TIS &&
+      p.token_mode != MC_TOKEN_ICEPOP)
+    return MC_ERR_INVALID_ARG;
+  if (p.token_mode == MC_TOKEN_TIS && !(finite(p.tis_cap) && p.tis_cap > 0.0f))
+    return MC_ERR_INVALID_ARG;
+  if (p.token_mode == MC_TOKEN_ICEPOP &&
+      !(finite(p.icepop_lo) && finite(p.icepop_hi) && p.icepop_lo > 0.0f &&
+        p.icepop_lo <= p.icepop_hi))
+    return MC_ERR_INVALID_ARG;
   if (!cu_seqlens || !cu_groups || (B > 0 && !rewards)) return MC_ERR_INVALID_ARG;
   if (T > 0 && (!logp || !logp_rollout || !out->dlogp)) return MC_ERR_INVALID_ARG;
   if (!aligned(cu_seqlens, 4) || !aligned(cu_groups, 4) || !aligned(out->loss, 4) ||
       (out->n_valid && !aligned(out->n_valid, 8)))
     return MC_ERR_INVALID_ARG;
-  mc_status_t st = check_ws(ws, ws_bytes, mc::loss_workspace(T, B, NG));
+  return MC_OK;
+}
+
+mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const float* logp_ref,
+                       const uint8_t* loss_mask, const int32_t* cu_seqlens,
+                       const int32_t* cu_groups, const float* rewards, int64_t T, int32_t B,
+                       int32_t NG, const mc_rl_params_t* params, const mc_rl_outputs_t* out,
+                       void* ws, size_t ws_bytes, void* stream) {
+  mc_status_t st = check_loss_args(logp, logp_rollout, cu_seqlens, cu_groups, rewards, T, B, NG,
+                                   params, out);
+  if (st != MC_OK) return st;
+  st = check_ws(ws, ws_bytes, mc::loss_workspace(T, B, NG));
   if (st != MC_OK) return st;
   return from_hip(mc::launch_loss(logp, logp_rollout, logp_ref, loss_mask, cu_seqlens, cu_groups,
-                                  rewards, T, B, NG, p, *out, ws,
+                                  rewards, T, B, NG, *params, *out, ws,
                                   static_cast<hipStream_t>(stream)));
 }
 

@@ -33,7 +33,8 @@ struct Carve {
 constexpr size_t kBwdChunkBytes = size_t(8) << 30;
 int64_t bwd_chunk_cols(int64_t T, int64_t V, size_t esize);
 
-// RAII timing scope around one or more launches on `s` (see mc_profiler_*).
+// RAII timing scope around one or more launches on `s` (see mc_profiler_*);
+// a null name records nothing.
 class ProfScope {
  public:
   ProfScope(hipStream_t s, const char* name, double flops, double bytes);
@@ -83,6 +84,6 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
                        const int32_t* cu_seqlens, const int32_t* cu_groups,
                        const float* rewards, int64_t T, int32_t B, int32_t NG,
                        const mc_rl_params_t& p, const mc_rl_outputs_t& out, void* ws,
-                       hipStream_t s);
+                       hipStream_t s, bool profile = true);
 
 }  // namespace mc

@@ -1,7 +1,8 @@
 // RL objective over a packed ragged batch: per-sequence log-ratio statistics
 // and filter masks (Eq. 18-21), group-normalised advantages (Eq. 3 / 12), the
-// sequence-masked clipped surrogate (Eq. 17, beta = 0) and its gradient with
-// respect to the per-token log-probs.  One workgroup per group, one wave per
+// sequence-masked clipped surrogate (Eq. 17) with an optional token-level
+// truncation or drop of the ratio (Sec. 4.5.2) and an optional KL term, and
+// its gradient with respect to the per-token log-probs.  One workgroup per group, one wave per
 // sequence, wave-level reductions; all sums in fp64 and in a fixed order.
 #include <hip/hip_runtime.h>
 
@@ -158,14 +159,18 @@ __global__ __launch_bounds__(256) void k_count(const long long* __restrict__ gro
 
 // Phase 3: per-token surrogate and gradient (Eq. 17); per-sequence sums.
 // With a reference policy, the KL term beta * k3 (k3 = e^r - r - 1,
-// r = logp_ref - logp) joins the same token mean.
+// r = logp_ref - logp) joins the same token mean.  The token mode acts on
+// the log-ratio ell: TIS scales the term of a token with ell > ln C by the
+// constant C / rho (its gradient weight becomes C A), IcePop drops a token
+// with ell outside [ln lo, ln hi] from the surrogate (it stays in N).
 __global__ __launch_bounds__(kLossThreads) void k_surrogate(
     const float* __restrict__ logp, const float* __restrict__ lr,
     const float* __restrict__ lref, const uint8_t* __restrict__ mask,
     const int32_t* __restrict__ cu, const int32_t* __restrict__ cg, int64_t T, int B, int NG,
     mc_rl_params_t p, const uint8_t* __restrict__ seq_mask, const double* __restrict__ adv_d,
     const long long* __restrict__ n_valid, float* __restrict__ dlogp,
-    double* __restrict__ seq_sum, int* __restrict__ seq_clip, double* __restrict__ seq_kl) {
+    double* __restrict__ seq_sum, int* __restrict__ seq_clip, double* __restrict__ seq_kl,
+    int* __restrict__ seq_tok) {
   const int g = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   bool bad = false;
@@ -174,6 +179,10 @@ __global__ __launch_bounds__(kLossThreads) void k_surrogate(
   const long long N = *n_valid;
   const double invN = N > 0 ? 1.0 / double(N) : 0.0;
   const double lo = 1.0 - double(p.eps_low), hi = 1.0 + double(p.eps_high);
+  const int mode = p.token_mode;
+  const double log_cap = mode == MC_TOKEN_TIS ? log(double(p.tis_cap)) : 0.0;
+  const double log_alo = mode == MC_TOKEN_ICEPOP ? log(double(p.icepop_lo)) : 0.0;
+  const double log_ahi = mode == MC_TOKEN_ICEPOP ? log(double(p.icepop_hi)) : 0.0;
   for (int i = a + w; i < b; i += kLossWaves) {
     int64_t s, e;
     seq_bounds(cu, i, B, T, s, e, bad);
@@ -182,19 +191,31 @@ __global__ __launch_bounds__(kLossThreads) void k_surrogate(
     const double beta = double(p.kl_beta);
     const bool with_kl = lref != nullptr && beta != 0.0;
     double sum = 0.0, kl = 0.0;
-    int nclip = 0;
+    int nclip = 0, ntok = 0;
     for (int64_t t = s + lane; t < e; t += 64) {
       float out = 0.0f;
       const bool valid = mask ? mask[t] != 0 : true;
       if (keep && valid) {
         const double lp = double(logp[t]);
-        const double rho = exp(lp - double(lr[t]));
-        const double un = rho * A;
-        const double cl = fmin(fmax(rho, lo), hi) * A;
-        sum += fmin(un, cl);
+        const double ell = lp - double(lr[t]);
+        double wgt = 1.0;
+        bool dropped = false;
+        if (mode == MC_TOKEN_TIS && ell > log_cap) {
+          wgt = exp(log_cap - ell);
+          ntok += 1;
+        } else if (mode == MC_TOKEN_ICEPOP && !(ell >= log_alo && ell <= log_ahi)) {
+          dropped = true;
+          ntok += 1;
+        }
         double g = 0.0;
-        if (un <= cl) g = -un;
-        else nclip += 1;
+        if (!dropped) {
+          const double rho = exp(ell);
+          const double un = rho * A;
+          const double cl = fmin(fmax(rho, lo), hi) * A;
+          sum += wgt * fmin(un, cl);
+          if (un <= cl) g = -wgt * un;
+          else nclip += 1;
+        }
         if (with_kl) {
           const double r = double(lref[t]) - lp;
           const double er = exp(r);
@@ -208,41 +229,48 @@ __global__ __launch_bounds__(kLossThreads) void k_surrogate(
     sum = wave_sum(sum);
     kl = wave_sum(kl);
     nclip = wave_sum(nclip);
+    ntok = wave_sum(ntok);
     if (lane == 0) {
       seq_sum[i] = sum;
       seq_clip[i] = nclip;
       seq_kl[i] = kl;
+      seq_tok[i] = ntok;
     }
   }
 }
 
-// Phase 4: loss = -(1/N) sum_i seq_sum_i (+ beta * KL), the clip fraction and
-// the mean KL estimate.
+// Phase 4: loss = -(1/N) sum_i seq_sum_i (+ beta * KL), the clip fraction,
+// the token-mode fraction and the mean KL estimate.
 __global__ __launch_bounds__(256) void k_finish(const double* __restrict__ seq_sum,
                                                 const int* __restrict__ seq_clip,
-                                                const double* __restrict__ seq_kl, int B,
+                                                const double* __restrict__ seq_kl,
+                                                const int* __restrict__ seq_tok, int B,
                                                 float beta, const long long* __restrict__ n_valid,
                                                 float* __restrict__ loss,
                                                 float* __restrict__ clip_frac,
-                                                float* __restrict__ kl_out) {
+                                                float* __restrict__ kl_out,
+                                                float* __restrict__ tok_frac) {
   __shared__ double ps[256], pk[256];
-  __shared__ long long pc[256];
+  __shared__ long long pc[256], pt[256];
   double s = 0.0, k = 0.0;
-  long long c = 0;
+  long long c = 0, n = 0;
   for (int i = threadIdx.x; i < B; i += 256) {
     s += seq_sum[i];
     k += seq_kl[i];
     c += seq_clip[i];
+    n += seq_tok[i];
   }
   ps[threadIdx.x] = s;
   pk[threadIdx.x] = k;
   pc[threadIdx.x] = c;
+  pt[threadIdx.x] = n;
   __syncthreads();
   for (int off = 128; off > 0; off >>= 1) {
     if (threadIdx.x < off) {
       ps[threadIdx.x] += ps[threadIdx.x + off];
       pk[threadIdx.x] += pk[threadIdx.x + off];
       pc[threadIdx.x] += pc[threadIdx.x + off];
+      pt[threadIdx.x] += pt[threadIdx.x + off];
     }
     __syncthreads();
   }
@@ -252,6 +280,7 @@ __global__ __launch_bounds__(256) void k_finish(const double* __restrict__ seq_s
     *loss = N > 0 ? float(-ps[0] / double(N) + double(beta) * kl) : 0.0f;
     if (clip_frac) *clip_frac = N > 0 ? float(double(pc[0]) / double(N)) : 0.0f;
     if (kl_out) *kl_out = float(kl);
+    if (tok_frac) *tok_frac = N > 0 ? float(double(pt[0]) / double(N)) : 0.0f;
   }
 }
 
@@ -293,6 +322,7 @@ size_t loss_workspace(int64_t T, int32_t B, int32_t NG) {
   n += align_up(b * 8, kWsAlign);                 // seq_sum
   n += align_up(b * 4, kWsAlign);                 // seq_clip
   n += align_up(b * 8, kWsAlign);                 // seq_kl
+  n += align_up(b * 4, kWsAlign);                 // seq_tok
   n += align_up(g * 8, kWsAlign);                 // group_n
   n += align_up(8, kWsAlign);                     // n_valid
   n += align_up(4, kWsAlign);                     // err
@@ -313,7 +343,7 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
                        const int32_t* cu_seqlens, const int32_t* cu_groups,
                        const float* rewards, int64_t T, int32_t B, int32_t NG,
                        const mc_rl_params_t& p, const mc_rl_outputs_t& out, void* ws,
-                       hipStream_t s) {
+                       hipStream_t s, bool profile) {
   const size_t b = size_t(B > 0 ? B : 1), g = size_t(NG > 0 ? NG : 1);
   Carve cv(ws);
   uint8_t* w_mask = cv.take<uint8_t>(b);
@@ -325,6 +355,7 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
   double* seq_sum = cv.take<double>(b);
   int* seq_clip = cv.take<int>(b);
   double* seq_kl = cv.take<double>(b);
+  int* seq_tok = cv.take<int>(b);
   long long* group_n = cv.take<long long>(g);
   long long* w_n = cv.take<long long>(1);
   int32_t* w_err = cv.take<int32_t>(1);
@@ -339,7 +370,9 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
            out.error_flag ? out.error_flag : w_err};
   long long* n_valid = out.n_valid ? reinterpret_cast<long long*>(out.n_valid) : w_n;
 
-  ProfScope ps_(s, "rl_loss", 0.0, double(T) * (4 + 4 + (mask ? 1 : 0) + 4) + 16.0 * b);
+  // (the profiler's events are created only when it is enabled and profile is set)
+  ProfScope ps_(s, profile ? "rl_loss" : nullptr, 0.0,
+                double(T) * (4 + 4 + (mask ? 1 : 0) + 4) + 16.0 * b);
   hipLaunchKernelGGL(k_loss_init, dim3(1), dim3(64), 0, s, o.err);
   if (NG > 0)
     hipLaunchKernelGGL(k_seq_stats, dim3(NG), dim3(kLossThreads), 0, s, logp, logp_rollout,
@@ -348,9 +381,9 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
   if (NG > 0)
     hipLaunchKernelGGL(k_surrogate, dim3(NG), dim3(kLossThreads), 0, s, logp, logp_rollout,
                        logp_ref, mask, cu_seqlens, cu_groups, T, B, NG, p, o.seq_mask, adv_d,
-                       n_valid, out.dlogp, seq_sum, seq_clip, seq_kl);
-  hipLaunchKernelGGL(k_finish, dim3(1), dim3(256), 0, s, seq_sum, seq_clip, seq_kl, B,
-                     p.kl_beta, n_valid, out.loss, out.clip_frac, out.kl);
+                       n_valid, out.dlogp, seq_sum, seq_clip, seq_kl, seq_tok);
+  hipLaunchKernelGGL(k_finish, dim3(1), dim3(256), 0, s, seq_sum, seq_clip, seq_kl, seq_tok, B,
+                     p.kl_beta, n_valid, out.loss, out.clip_frac, out.kl, out.token_frac);
   return hipGetLastError();
 }
 

@@ -61,7 +61,7 @@ void fold_locked() {
 
 ProfScope::ProfScope(hipStream_t s, const char* name, double flops, double bytes)
     : stream_(s), name_(name), flops_(flops), bytes_(bytes) {
-  if (!g_on.load(std::memory_order_relaxed)) return;
+  if (name_ == nullptr || !g_on.load(std::memory_order_relaxed)) return;
   if (hipEventCreate(&start_) != hipSuccess) return;
   if (hipEventCreate(&stop_) != hipSuccess) {
     (void)hipEventDestroy(start_);

@@ -19,7 +19,8 @@ PTERM_RTOL = 2.0 ** -8
 
 def to_params(p: oracle.RLParams):
     from paper_2606_04847_amd import RLParams
-    return RLParams(p.eps_low, p.eps_high, p.delta, p.adv_eps, p.std_ddof, p.filter, p.kl_beta)
+    return RLParams(p.eps_low, p.eps_high, p.delta, p.adv_eps, p.std_ddof, p.filter, p.kl_beta,
+                    p.token_mode, p.tis_cap, p.icepop_lo, p.icepop_hi)
 
 
 def small_case(cfg, seed=None):

@@ -108,7 +108,7 @@ def test_bwd_argument_checks(lib):
 
 def loss(lib, T=10, B=2, NG=1, params=None, out=None, ws=FAKE_WS, nbytes=None, **ptrs):
     p = params or binding.RLParams().to_c()
-    o = out or binding.RLOutputsC(FAKE, FAKE, *([None] * 9))
+    o = out or binding.RLOutputsC(FAKE, FAKE, *([None] * (len(binding._OUT_FIELDS) - 2)))
     need = lib.mc_rl_loss_workspace_size(T, B, NG)
     args = dict(logp=FAKE, lr=FAKE, mask=None, cu=FAKE, cg=FAKE, rw=FAKE)
     args.update(ptrs)
@@ -120,12 +120,27 @@ def loss(lib, T=10, B=2, NG=1, params=None, out=None, ws=FAKE_WS, nbytes=None, *
 @pytest.mark.parametrize("field,value", [
     ("eps_low", 1.0), ("eps_low", -0.1), ("eps_high", -0.5), ("delta", -1.0),
     ("delta", float("nan")), ("adv_eps", float("inf")), ("std_ddof", 2), ("filter", 3),
-    ("kl_beta", -0.1), ("kl_beta", float("nan")),
+    ("kl_beta", -0.1), ("kl_beta", float("nan")), ("token_mode", 3), ("token_mode", -1),
 ])
 def test_loss_parameter_checks(lib, field, value):
     p = binding.RLParams().to_c()
     setattr(p, field, value)
     assert loss(lib, params=p) == INVALID
+
+
+@pytest.mark.parametrize("mode,field,value,ok", [
+    ("tis", "tis_cap", 0.0, False), ("tis", "tis_cap", -1.0, False),
+    ("tis", "tis_cap", float("inf"), False), ("tis", "tis_cap", 0.5, True),
+    ("icepop", "icepop_lo", 0.0, False), ("icepop", "icepop_hi", 0.4, False),
+    ("icepop", "icepop_hi", float("nan"), False), ("icepop", "icepop_lo", 1.0, True),
+    ("none", "tis_cap", -1.0, True),          # parameters of an unused mode are not read
+])
+def test_token_mode_parameter_checks(lib, mode, field, value, ok):
+    # a valid parameter set passes the parameter checks and stops at the
+    # (deliberately short) workspace check, before any launch
+    p = binding.RLParams(token_mode=mode).to_c()
+    setattr(p, field, value)
+    assert loss(lib, params=p, nbytes=1) == (WS if ok else INVALID)
 
 
 def test_loss_argument_checks(lib):
@@ -135,9 +150,9 @@ def test_loss_argument_checks(lib):
     assert loss(lib, logp=None) == INVALID
     assert loss(lib, cu=None) == INVALID
     assert loss(lib, rw=None) == INVALID
-    o = binding.RLOutputsC(None, FAKE, *([None] * 9))
+    o = binding.RLOutputsC(None, FAKE, *([None] * (len(binding._OUT_FIELDS) - 2)))
     assert loss(lib, out=o) == INVALID                # loss output is required
-    o = binding.RLOutputsC(FAKE, None, *([None] * 9))
+    o = binding.RLOutputsC(FAKE, None, *([None] * (len(binding._OUT_FIELDS) - 2)))
     assert loss(lib, out=o) == INVALID                # dlogp output is required
     assert loss(lib, nbytes=1) == WS
 
@@ -195,4 +210,5 @@ def test_cached_argument_checks(lib):
     assert bwd(FAKE_WS, 0) == WS
     assert bwd(FAKE_WS, need_c, flags=8) == INVALID
     assert bwd(FAKE_WS, need_c, dh=FAKE + 4) == INVALID
+
 

@@ -146,3 +146,121 @@ def test_primeecho_rewards_match_oracle_and_feed_the_loss():
     torch.cuda.synchronize()
     o = oracle.rl_loss(logp, logp, None, cu, cg, r.cpu().numpy())
     np.testing.assert_allclose(g["adv"].cpu().numpy(), o["adv"], rtol=1e-6, atol=1e-6)
+
+
+# ---------------------------------------------------------------------------
+# Token-level modes of the objective (TIS / IcePop readings)
+# ---------------------------------------------------------------------------
+def _wide_offsets(T, rng, edges, sigma=0.4, margin=5e-3):
+    """Per-token log-ratio offsets spread wide enough that many tokens fall
+    outside the token-mode bounds, kept `margin` away from every decision
+    edge (clip edges and the mode's bounds), so every decision is unique."""
+    x = rng.normal(0.0, sigma, size=T)
+    for _ in range(1000):
+        bad = np.zeros(T, bool)
+        for e in edges:
+            bad |= np.abs(-x - e) < margin
+        if not bad.any():
+            return x
+        x[bad] = rng.normal(0.0, sigma, size=int(bad.sum()))
+    raise RuntimeError("margin not reachable")
+
+
+_TOKEN_MODES = [("tis", dict(tis_cap=1.5)), ("icepop", dict(icepop_lo=0.75, icepop_hi=1.3))]
+
+
+def _edges(p):
+    return [math.log(1 - p.eps_low), math.log(1 + p.eps_high),
+            math.log(float(np.float32(p.tis_cap))), math.log(float(np.float32(p.icepop_lo))),
+            math.log(float(np.float32(p.icepop_hi)))]
+
+
+@pytest.mark.parametrize("cid", [3, 4, 5])
+@pytest.mark.parametrize("mode,kw", _TOKEN_MODES)
+def test_token_mode_loss_full_size(cid, mode, kw):
+    from workloads import make_structure
+    mc = _mc()
+    s = make_structure(cid)
+    p = oracle.RLParams(filter="none", token_mode=mode, **kw)
+    rng = np.random.default_rng(200 + cid)
+    logp = (-rng.uniform(0.5, 12.0, size=s.T)).astype(np.float32)
+    x = _wide_offsets(s.T, rng, _edges(p))
+    lr = (logp.astype(np.float64) + x).astype(np.float32)
+    # the fp32 rounding of lr must not move a token across an edge
+    ell = logp.astype(np.float64) - lr.astype(np.float64)
+    assert min(np.min(np.abs(ell - e)) for e in _edges(p)) > 1e-3
+    st = structure_tensors(s)
+    g = mc.rl_loss(torch.from_numpy(logp).cuda(), torch.from_numpy(lr).cuda(), st["mask"],
+                   st["cu"], st["cg"], st["rewards"], to_params(p))
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in g.items()}
+    o = oracle.rl_loss(logp, lr, s.loss_mask, s.cu_seqlens, s.cu_groups, s.rewards, p)
+    assert 0.05 < o["token_frac"] < 0.95                 # the mode really acts
+    assert int(g["n_valid"][0]) == o["n_valid"]
+    assert abs(g["loss"][0] - o["loss"]) <= LOSS_RTOL * abs(o["loss"])
+    np.testing.assert_allclose(g["dlogp"], o["dlogp"], rtol=1e-5, atol=1e-12)
+    assert np.array_equal(g["dlogp"] == 0.0, o["dlogp"] == 0.0)
+    assert abs(g["token_frac"][0] - o["token_frac"]) <= 1e-6
+    assert abs(g["clip_frac"][0] - o["clip_frac"]) <= 1e-6
+
+
+@pytest.mark.parametrize("mode,kw", _TOKEN_MODES)
+def test_token_mode_end_to_end(mode, kw):
+    # GPU forward -> loss with the token mode -> backward, against the oracle
+    from _cases import assert_step_parity, gpu_step
+    cfg = scaled_config(4, T=1200, n_groups=4, group_size=8, d=256, V=1500, hi=200, seed=17,
+                        drift=dict(kind="frac_normal", count=3, mean=0.3, std=0.1))
+    case = small_case(cfg)
+    p = oracle.RLParams(filter="mirrorpop", delta=0.24, token_mode=mode, **kw)
+    s = case["s"]
+    logp, lse = oracle.logprob_fwd(case["H"], case["W"], case["y"])
+    rng = np.random.default_rng(18)
+    x = _wide_offsets(s.T, rng, _edges(p), sigma=0.3)
+    lr = (logp + x).astype(np.float32)
+    o = oracle.rl_loss(logp, lr, s.loss_mask, s.cu_seqlens, s.cu_groups, s.rewards, p)
+    assert 0.05 < o["token_frac"] < 0.95
+    assert np.min(np.abs(o["stat_abs"] - p.delta)) > 1e-3      # unique sequence decisions
+    assert 0 < o["seq_mask"].sum() < s.B
+    dH, dW = oracle.logprob_bwd(case["H"], case["W"], case["y"], lse, o["dlogp"])
+    o = dict(o, logp=logp, lse=lse, dH=dH, dW=dW)
+    g = gpu_step(case, p, lr)
+    assert_step_parity(g, o)
+
+
+def test_side_stream_calls_match_current_stream():
+    # every wrapper records the caller's stream on what it allocates: results
+    # computed on a side stream while the current stream allocates and fills
+    # memory of the same sizes are those of the current stream, bit for bit
+    from _cases import gpu_step
+    cfg = scaled_config(4, T=900, n_groups=2, group_size=8, d=256, V=1300, hi=150, seed=19,
+                        drift=dict(kind="frac_normal", count=2, mean=0.3, std=0.1))
+    case = small_case(cfg)
+    p = oracle.RLParams()
+    lr = (oracle.logprob_fwd(case["H"], case["W"], case["y"])[0]
+          + case["s"].rollout_delta).astype(np.float32)
+    ref = gpu_step(case, p, lr)
+    mc = _mc()
+    H, W, y = device_tensors(case)
+    st = structure_tensors(case["s"])
+    lrd = torch.from_numpy(lr).cuda()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    res = []
+    for _ in range(3):
+        logp, lse = mc.logprob_fwd(H, W, y, stream=side)
+        out = mc.rl_loss(logp, lrd, st["mask"], st["cu"], st["cg"], st["rewards"],
+                         to_params(p), stream=side)
+        dH, dW = mc.logprob_bwd(H, W, y, lse, out["dlogp"], stream=side)
+        # the current stream churns the allocator meanwhile
+        junk = [torch.full((n,), -7.0, device="cuda") for n in
+                (H.shape[0], W.shape[0] * W.shape[1], H.shape[0] * H.shape[1], 1 << 20)]
+        del junk
+        res.append((logp, lse, out["dlogp"], dH, dW))
+    side.synchronize()
+    torch.cuda.synchronize()
+    for logp, lse, dl, dH, dW in res:
+        assert np.array_equal(logp.cpu().numpy(), ref["logp"])
+        assert np.array_equal(lse.cpu().numpy(), ref["lse"])
+        assert np.array_equal(dl.cpu().numpy(), ref["dlogp"])
+        assert np.array_equal(dH.cpu().numpy(), ref["dH"])
+        assert np.array_equal(dW.cpu().numpy(), ref["dW"])
