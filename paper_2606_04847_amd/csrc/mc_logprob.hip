@@ -54,10 +54,17 @@ __device__ __forceinline__ int wrow(int i, int e, int lane) {
 // A 256 x 256 bf16 tile (rows: 256 vocabulary entries of a chunk, columns:
 // 256 tokens) staged in the workgroup's LDS operand buffers for stores of
 // whole panel rows: four 32 KiB panels (64 vocabulary entries each) of 256
-// token rows x 128 bytes, the 16-byte chunk index XOR-ed with t & 7.
+// token rows x 128 bytes, the 16-byte chunk index XOR-ed with (t >> 1) & 7.
+// The 8-byte staging writes of one instruction are served 32 lanes at a time
+// over 64 four-byte banks; those lanes hold 16 consecutive tokens (two 4-row
+// groups each): token parity picks the bank half (rows are 128 bytes) and
+// (t >> 1) & 7 a distinct chunk for each of the 8 tokens of one parity, so
+// the 64 dwords hit 64 distinct banks (XOR-ing with t & 7 put tokens t and
+// t + 8 on the same banks: two cycles per pass).
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ int panel_swz(int t) { return (t >> 1) & 7; }
 __device__ __forceinline__ int panel_stage_off(int v, int t) {
-  return (v >> 6) * 32768 + t * 128 + ((((v & 63) >> 3) ^ (t & 7)) << 4) + ((v & 7) << 1);
+  return (v >> 6) * 32768 + t * 128 + ((((v & 63) >> 3) ^ panel_swz(t)) << 4) + ((v & 7) << 1);
 }
 
 // Each panel's 256 token rows are 32 KiB of contiguous memory: 16-byte
@@ -75,8 +82,9 @@ __device__ __forceinline__ void store_staged_panels(const char* lds, bf16_t* P, 
   constexpr int kRows = kThreads / 8;            // token rows per round
   constexpr int kRounds = 256 / kRows;           // rounds per panel
   constexpr int kIters = 4 * kRounds;
+  static_assert(kRows % 16 == 0, "the swizzle of row r0 + kRows k is that of r0");
   const int ch = threadIdx.x & 7, r0 = threadIdx.x >> 3;
-  const int sw = (ch ^ (r0 & 7)) << 4;           // kRows is a multiple of 8
+  const int sw = (ch ^ panel_swz(r0)) << 4;
   u32x4 v[kIters];
 #pragma unroll
   for (int it = 0; it < kIters; ++it)
