@@ -16,4 +16,5 @@ from .gen import (  # noqa: F401
     sample_targets_numpy,
     sample_targets_torch,
     scaled_config,
+    zipf_targets,
 )
