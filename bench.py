@@ -1,29 +1,45 @@
 #!/usr/bin/env python3
 """Throughput of the fused RL log-prob step on one MI355X.
 
-One step = mc_logprob_fwd_cached (LM-head GEMM + online log-sum-exp +
-target gather, keeping the softmax cache) -> mc_rl_loss (ratios, MirrorPop
-filter, group advantages, clipped surrogate, dlogp) ->
-mc_logprob_bwd_cached (dHidden and dW from the cache), on one stream, over
-one packed batch of synthetic inputs already resident in HBM.  With
---recompute the step uses mc_logprob_fwd / mc_logprob_bwd instead (the
-backward recomputes the logits).
+One step = forward (LM-head GEMM + online log-sum-exp + target gather) ->
+mc_rl_loss (ratios, MirrorPop filter, group advantages, clipped surrogate,
+dlogp) -> backward (dHidden and dW), on one stream, over one packed batch of
+synthetic inputs already resident in HBM.  Two steps are timed on the same
+inputs in one process:
+
+  recompute  mc_logprob_fwd / mc_logprob_bwd: the forward writes no [T, V]
+             tensor (the logits live only in registers), the backward
+             recomputes them.  This is the headline figure.
+  cached     mc_logprob_fwd_cached / mc_logprob_bwd_cached: the forward also
+             writes a [T, V] bf16 softmax cache that the backward reads
+             instead of recomputing the logits (reported under "cached").
 
 Default workload: T = 16384 packed tokens (256 sequences in 32 groups of 8,
 lengths 8-2048, 70% of tokens masked, 10% of sequences drifted), d = 4096,
-V = 151936, bf16 operands with fp32 accumulation.
+V = 151936, bf16 operands with fp32 accumulation.  Other modes:
+  --config 2   forward only, T = 8192 (the 9B-class forward workload)
+  --config 3|5 the 27B-class (d = 5120, T = 32768) and large-vocabulary
+               (V = 248320, T = 65536) workloads
+  --shard      one GPU's vocabulary shard (V / 8 entries) of the headline
+               shape: shard forward (partials) and shard backward
+  --targets zipf  Zipf-like targets (one bucket holds a fifth of the tokens)
 
 Prints one JSON line.  `value` is tokens/s; counted FLOPs are 2TdV forward
 plus 4TdV backward; `mfma_frac` is counted FLOP/s over the dense bf16 peak.
+`python bench.py --summarize DIR` prints the per-kernel summary of a
+rocprofv3 output directory (kernel trace or counters) instead.
 """
 from __future__ import annotations
 
 import argparse
+import csv
 import glob
 import hashlib
 import json
 import os
+import statistics
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -31,25 +47,21 @@ sys.path.insert(0, ROOT)
 
 METRIC = "fused logprob fwd+bwd tokens/s @ d=4096,V=151936; % bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2516.6     # 256 CUs x 4096 FLOP/clk x 2.4 GHz, dense bf16
-PEAK_FP32_TFLOPS = 157.3
+FLOP_PER_CLK = 256 * 4096     # dense bf16 FLOP per clock over the chip
+PEAK_HBM_GBPS = 8000.0
+FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 MB MALL)
 
-# HBM traffic per launch of the step's kernels from rocprofv3 FETCH_SIZE /
-# WRITE_SIZE passes (scaled by the 1 GiB copy calibration), valid only for
-# the kernel sources with this digest (else null).
+# Memory-side traffic per launch of the recompute step's kernels at the
+# headline workload: rocprofv3 TCC_EA0_RDREQ_DRAM_32B_sum (reads) and
+# TCC_EA0_WRREQ_WRITE_DRAM_32B_sum (writes), x 32 bytes; a 1 GiB device copy
+# reads and writes exactly 1 GiB by these counters.  They count L2 misses
+# that go to the memory side, so reads served by the 256 MB Infinity Cache
+# are included: an upper bound on HBM bytes.  Valid only for kernel sources
+# with this digest (else null).
 TRAFFIC = {
-    "sources_sha256":
-        "4fd5ae0e70ff241c11156f6c4cd0eff374332b9ecf5b799e931b940bfc0eb1ae",
-    "bytes_per_launch": {
-        "logprob_fwd_gemm": 35759080788,
-        "logprob_fwd_merge": 78294580,
-        "rl_loss": 91896,
-        "logprob_bwd_bucket": 1338976,
-        "logprob_bwd_cache_probs": 6307710964,
-        "logprob_bwd_transpose": 1378916044,
-        "logprob_bwd_dhidden": 30274365503,
-        "logprob_bwd_dweight": 32536170929,
-        "logprob_bwd_onehot_dw": 176654837,
-    },
+    "sources_sha256": None,
+    "read_bytes_per_launch": {},
+    "write_bytes_per_launch": {},
 }
 
 
@@ -62,19 +74,40 @@ def sources_digest() -> str:
     return h.hexdigest()
 
 
-def workload_name(cfg, s):
+def traffic_of(name):
+    if TRAFFIC["sources_sha256"] != sources_digest():
+        return None
+    r = TRAFFIC["read_bytes_per_launch"].get(name)
+    w = TRAFFIC["write_bytes_per_launch"].get(name)
+    if r is None or w is None:
+        return None
+    return r + w
+
+
+def workload_name(cfg, s, extra=""):
     return (f"{cfg['name']}: T={s.T} packed tokens ({s.B} sequences, {s.NG} groups of "
-            f"{cfg['group_size']}), d={cfg['d']}, V={cfg['V']}, {cfg['dtype']}")
+            f"{cfg['group_size']}), d={cfg['d']}, V={cfg['V']}, {cfg['dtype']}{extra}")
 
 
-def build_inputs(cid, dev):
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# inputs
+# ---------------------------------------------------------------------------
+def build_inputs(cid, dev, targets="model"):
     import torch
     import paper_2606_04847_amd as mc
-    from workloads import CONFIGS, make_structure, make_tensors_torch, sample_targets_torch
+    from workloads import (CONFIGS, make_structure, make_tensors_torch, sample_targets_torch,
+                           zipf_targets)
     cfg = CONFIGS[cid]
     s = make_structure(cid)
     H, W = make_tensors_torch(cfg, s.T, dev)
-    y = sample_targets_torch(cfg, H, W)
+    if targets == "zipf":
+        y = torch.from_numpy(zipf_targets(s.T, cfg["V"], seed=cfg["seed"])).to(dev)
+    else:
+        y = sample_targets_torch(cfg, H, W)
     logp, _ = mc.logprob_fwd(H, W, y)
     # rollout log-probs: the trainer's plus the workload's per-token offset
     lr = (logp.double() + torch.from_numpy(s.rollout_delta).to(dev).double()).float()
@@ -86,18 +119,191 @@ def build_inputs(cid, dev):
     return cfg, s, H, W, y, lr, st
 
 
-def cpu_baseline(cid, H, W, y, s, target_s):
-    """The fp64 oracle on a bounded leading sample of whole groups."""
-    import numpy as np
-    import oracle
+# ---------------------------------------------------------------------------
+# clock and power, sampled live through amdsmi while the timed region runs
+# ---------------------------------------------------------------------------
+class ClockSampler:
+    def __init__(self, period_s=0.004):
+        self.period = period_s
+        self.ok = False
+        self.samples = []
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            self.smi = amdsmi
+            self.h = amdsmi.amdsmi_get_processor_handles()[0]
+            self._metrics()
+            self.ok = True
+        except Exception as e:   # no amdsmi, no permission: report null
+            self.err = str(e)
+
+    def _metrics(self):
+        return self.smi.amdsmi_get_gpu_metrics_info(self.h)
+
+    def _run(self):
+        while not self.stop.is_set():
+            try:
+                m = self._metrics()
+                clks = [c for c in m.get("current_gfxclks", []) if isinstance(c, (int, float))]
+                if clks:
+                    self.samples.append((sum(clks) / len(clks), m.get("current_socket_power")))
+            except Exception:
+                pass
+            time.sleep(self.period)
+
+    def start(self):
+        if not self.ok:
+            return
+        self.samples = []
+        self.m0 = self._metrics()
+        self.stop = threading.Event()
+        self.th = threading.Thread(target=self._run, daemon=True)
+        self.th.start()
+
+    def finish(self):
+        if not self.ok:
+            return None
+        self.stop.set()
+        self.th.join()
+        m1 = self._metrics()
+        if not self.samples:
+            return None
+        clk = [c for c, _ in self.samples]
+        pw = [p for _, p in self.samples if isinstance(p, (int, float))]
+        out = {"gfxclk_mhz_mean": statistics.fmean(clk), "gfxclk_mhz_min": min(clk),
+               "gfxclk_mhz_max": max(clk), "samples": len(clk),
+               "socket_power_w_mean": statistics.fmean(pw) if pw else None,
+               "source": "amdsmi gpu_metrics current_gfxclks (mean over the 8 XCDs), "
+                         "sampled every ~4 ms during the timed region"}
+        try:
+            d_acc = m1["accumulation_counter"] - self.m0["accumulation_counter"]
+            d_ppt = m1["ppt_residency_acc"] - self.m0["ppt_residency_acc"]
+            if d_acc > 0:
+                out["power_limited_frac"] = d_ppt / d_acc
+        except Exception:
+            pass
+        return out
+
+
+# ---------------------------------------------------------------------------
+# timing
+# ---------------------------------------------------------------------------
+def time_steps(step, steps, warmup, sampler=None, flush=None, flush_reps=0):
+    """Warm-up, then exactly `steps` steps in one region bracketed by
+    synchronisation (per-step events inside for the median), with the
+    library's per-kernel profiler on; then `flush_reps` more steps, each
+    after a write of FLUSH_BYTES of scratch, timed one by one."""
+    import torch
+    import paper_2606_04847_amd as mc
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    mc.profiler_reset()
+    mc.profiler_enable(True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    if sampler:
+        sampler.start()
+    torch.cuda.synchronize()
+    ev[0].record()
+    out = None
+    for k in range(steps):
+        out = step()
+        ev[k + 1].record()
+    torch.cuda.synchronize()
+    clock = sampler.finish() if sampler else None
+    mc.profiler_enable(False)
+    kernels = mc.profiler_read()
+    per = [ev[k].elapsed_time(ev[k + 1]) for k in range(steps)]
+    res = {"ms_per_step": ev[0].elapsed_time(ev[steps]) / steps,
+           "median_ms": statistics.median(per), "min_ms": min(per), "max_ms": max(per),
+           "kernels": kernels, "clock": clock, "out": out}
+    if flush is not None and flush_reps > 0:
+        fl = []
+        for k in range(flush_reps):
+            flush.fill_(float(k))
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            step()
+            b.record()
+            fl.append((a, b))
+        torch.cuda.synchronize()
+        res["median_ms_flushed"] = statistics.median(a.elapsed_time(b) for a, b in fl)
+    return res
+
+
+def kernel_table(kernels):
+    return {k: {"ms_per_launch": v["ms"] / v["launches"], "launches": v["launches"],
+                "tflops": (v["flops"] / (v["ms"] * 1e-3) / 1e12) if v["flops"] else None,
+                "GBps_algorithmic": v["bytes"] / (v["ms"] * 1e-3) / 1e9}
+            for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms"])}
+
+
+def roofline_of(kernels):
+    """Roofline object of the kernel with the largest time in the region."""
+    name, k = max(kernels.items(), key=lambda kv: kv[1]["ms"])
+    ms = k["ms"] / k["launches"]
+    if k["flops"]:
+        achieved = k["flops"] / (k["ms"] * 1e-3) / 1e12
+        return {"bound": "mfma", "kernel": name, "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                "traffic": traffic_of(name), "avg_launch_ms": ms,
+                "algorithmic_flops_per_launch": k["flops"] / k["launches"]}
+    achieved = k["bytes"] / (k["ms"] * 1e-3) / 1e9
+    return {"bound": "hbm", "kernel": name, "achieved": achieved, "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic_of(name),
+            "avg_launch_ms": ms}
+
+
+def summary(res, T, counted, executed):
+    ms = res["ms_per_step"]
+    out = {"value": T / (ms * 1e-3), "ms_per_step": ms, "median_ms_per_step": res["median_ms"],
+           "min_ms_per_step": res["min_ms"], "max_ms_per_step": res["max_ms"],
+           "median_ms_per_step_flushed": res.get("median_ms_flushed"),
+           "counted_tflops": counted / (ms * 1e-3) / 1e12,
+           "mfma_frac": counted / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+           "executed_mfma_frac": executed / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+           "clock": res["clock"]}
+    clk = res["clock"]
+    if clk and clk.get("gfxclk_mhz_mean"):
+        peak_at = FLOP_PER_CLK * clk["gfxclk_mhz_mean"] * 1e6
+        out["executed_mfma_frac_at_measured_clock"] = executed / (ms * 1e-3) / peak_at
+        out["mfma_frac_at_measured_clock"] = counted / (ms * 1e-3) / peak_at
+    out["roofline"] = roofline_of(res["kernels"])
+    out["kernels"] = kernel_table(res["kernels"])
+    return out
+
+
+# ---------------------------------------------------------------------------
+# the fp64 oracle on the host cores
+# ---------------------------------------------------------------------------
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def oracle_threads():
     try:
         import threadpoolctl
         info = threadpoolctl.threadpool_info()
-        cores = max([i.get("num_threads", 1) for i in info] + [1])
+        return max([i.get("num_threads", 1) for i in info] + [1])
     except Exception:
-        cores = len(os.sched_getaffinity(0))
+        return len(os.sched_getaffinity(0))
+
+
+def cpu_baseline(H, W, y, s, target_s, fwd_only=False):
+    """The fp64 oracle on a bounded leading sample of whole groups."""
+    import numpy as np
+    import oracle
     Wh = W.float().cpu().numpy()
     cu, cg = s.cu_seqlens, s.cu_groups
+    d, V = Wh.shape[1], Wh.shape[0]
 
     def run(n_groups):
         nseq = int(cg[n_groups])
@@ -106,10 +312,11 @@ def cpu_baseline(cid, H, W, y, s, target_s):
         ys = y[:n].cpu().numpy()
         t0 = time.perf_counter()
         logp, lse = oracle.logprob_fwd(Hs, Wh, ys)
-        lr = logp + s.rollout_delta[:n].astype(np.float64)
-        out = oracle.rl_loss(logp, lr, s.loss_mask[:n], cu[:nseq + 1], cg[:n_groups + 1],
-                             s.rewards[:nseq], oracle.RLParams())
-        oracle.logprob_bwd(Hs, Wh, ys, lse, out["dlogp"])
+        if not fwd_only:
+            lr = logp + s.rollout_delta[:n].astype(np.float64)
+            out = oracle.rl_loss(logp, lr, s.loss_mask[:n], cu[:nseq + 1], cg[:n_groups + 1],
+                                 s.rewards[:nseq], oracle.RLParams())
+            oracle.logprob_bwd(Hs, Wh, ys, lse, out["dlogp"])
         return n, time.perf_counter() - t0
 
     n1, t1 = run(1)
@@ -118,29 +325,87 @@ def cpu_baseline(cid, H, W, y, s, target_s):
     while groups < s.NG and int(cu[int(cg[groups + 1])]) * per_tok <= target_s:
         groups += 1
     n, t = (n1, t1) if groups == 1 else run(groups)
-    return {"value": n / t, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+    # fp64 work the oracle executes: logits 2ndV; backward: logits again,
+    # G W and G^T H, 6ndV
+    flops = (2.0 if fwd_only else 8.0) * n * d * V
+    what = "logprob_fwd" if fwd_only else "logprob_fwd + rl_loss + logprob_bwd (full dH rows and dW)"
+    return {"value": n / t, "unit": "tokens/s", "cores": int(oracle_threads()), "kind": "oracle",
+            "cpu_model": cpu_model(), "fp64_gflops": flops / t / 1e9,
             "sample": (f"first {groups} groups ({n} tokens) of the workload: fp64 oracle "
-                       f"logprob_fwd + rl_loss + logprob_bwd (full dH rows and dW), "
-                       f"{t:.1f} s wall")}
+                       f"{what}, {t:.1f} s wall")}
 
 
+# ---------------------------------------------------------------------------
+# rocprofv3 summaries (measurement aid)
+# ---------------------------------------------------------------------------
+def summarize(path):
+    """Per-kernel summary of a rocprofv3 output directory: average kernel
+    durations from a kernel trace, or per-dispatch counter values."""
+    rows_t, rows_c = [], []
+    for f in glob.glob(os.path.join(path, "**", "*kernel_trace.csv"), recursive=True):
+        rows_t += list(csv.DictReader(open(f)))
+    for f in glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True):
+        rows_c += list(csv.DictReader(open(f)))
+
+    def role(name):
+        for key in ("k_fwd_logits_lse", "k_bwd_probs", "k_bwd_dhidden", "k_bwd_dweight",
+                    "k_cache_to_probs", "k_transpose", "k_onehot_dw", "k_lse_merge",
+                    "k_shard_partial", "k_tail_reduce", "k_surrogate", "k_seq_stats"):
+            if key in name:
+                return key
+        return "other"
+
+    if rows_t:
+        agg = {}
+        for r in rows_t:
+            dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-6
+            agg.setdefault(role(r["Kernel_Name"]), []).append(dur)
+        print(f"{'kernel':24s} {'calls':>6s} {'avg_ms':>9s} {'min_ms':>9s} {'max_ms':>9s}")
+        for k, v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+            print(f"{k:24s} {len(v):6d} {statistics.fmean(v):9.3f} {min(v):9.3f} {max(v):9.3f}")
+    if rows_c:
+        agg = {}
+        for r in rows_c:
+            key = (role(r["Kernel_Name"]), r["Counter_Name"])
+            agg.setdefault(key, []).append(float(r["Counter_Value"]))
+        print(f"{'kernel':24s} {'counter':40s} {'dispatches':>10s} {'mean per dispatch':>20s}")
+        for (k, c), v in sorted(agg.items()):
+            print(f"{k:24s} {c:40s} {len(v):10d} {statistics.fmean(v):20.1f}")
+
+
+# ---------------------------------------------------------------------------
 def main():
     ap = argparse.ArgumentParser(description=__doc__,
                                  formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=4, choices=[3, 4, 5])
+    ap.add_argument("--config", type=int, default=4, choices=[2, 3, 4, 5])
+    ap.add_argument("--step", default="both", choices=["both", "recompute", "cached"],
+                    help="which step(s) to time (default both; the headline is recompute)")
+    ap.add_argument("--shard", action="store_true",
+                    help="time one GPU's vocabulary shard (V/8 entries) of the workload")
+    ap.add_argument("--targets", default="model", choices=["model", "zipf"])
+    ap.add_argument("--flush-reps", type=int, default=10,
+                    help="extra steps timed one by one after a 1 GiB scratch write each")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="target duration of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--recompute", action="store_true",
-                    help="time the recompute path (mc_logprob_fwd / mc_logprob_bwd) instead "
-                         "of the softmax-cache path")
+    ap.add_argument("--no-clock", action="store_true", help="do not sample the clock")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy three times (calibrates the "
-                         "FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
+                         "memory-traffic counters against a known byte count)")
+    ap.add_argument("--summarize", metavar="DIR",
+                    help="print the per-kernel summary of a rocprofv3 output directory")
     args = ap.parse_args()
+    if args.summarize:
+        summarize(args.summarize)
+        return
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this "
+              "single-GPU build (the multi-GPU sharding is a design note only).",
+              file=sys.stderr)
+        sys.exit(2)
     if args.copy_probe:
         import torch
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")
@@ -150,120 +415,131 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes_per_launch": src.numel() * 4}), flush=True)
         return
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this "
-              "single-GPU build (the multi-GPU sharding is a design note only).",
-              file=sys.stderr)
-        sys.exit(2)
 
     import torch
     import paper_2606_04847_amd as mc
-    mc.load_library()
+    lib = mc.load_library()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    cfg, s, H, W, y, lr, st = build_inputs(args.config, dev)
+    cfg, s, H, W, y, lr, st = build_inputs(args.config, dev, args.targets)
     T, d, V = s.T, cfg["d"], cfg["V"]
-
-    lib = mc.load_library()
-    ws_f = torch.empty(lib.mc_logprob_fwd_workspace_size(T, d, V, 1), dtype=torch.uint8,
-                       device=dev)
-    if args.recompute:
-        ws_b = torch.empty(lib.mc_logprob_bwd_workspace_size(T, d, V, 1), dtype=torch.uint8,
-                           device=dev)
-        cache = None
-    else:
-        ws_b = torch.empty(lib.mc_logprob_bwd_cached_workspace_size(T, d, V, 1),
-                           dtype=torch.uint8, device=dev)
-        cache = mc.softmax_cache(H, W)
+    params = mc.RLParams()
+    sampler = None if args.no_clock else ClockSampler()
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
     logp = torch.empty(T, dtype=torch.float32, device=dev)
     lse = torch.empty(T, dtype=torch.float32, device=dev)
-    dH = torch.empty(T, d, dtype=torch.float32, device=dev)
-    dW = torch.empty(V, d, dtype=torch.float32, device=dev)
-    params = mc.RLParams()
+    extra = ", Zipf-like targets (exponent 1.2)" if args.targets == "zipf" else ""
+    config = {"workload": workload_name(cfg, s, extra), "T": T, "d": d, "V": V,
+              "sequences": s.B, "groups": s.NG, "parallelism": "none (1 GPU)",
+              "targets": args.targets}
+    line = {"metric": METRIC, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16", "data": "synthetic"}
+    fwd_only = cfg["fwd_only"]
 
-    def step():
-        if cache is None:
-            mc.logprob_fwd(H, W, y, logp=logp, lse=lse, workspace=ws_f)
-        else:
-            mc.logprob_fwd_cached(H, W, y, cache, logp=logp, lse=lse, workspace=ws_f)
+    if args.shard:
+        # one GPU's part of a vocabulary-parallel LM head: V/8 rows of W; the
+        # merge of the 8 shards' partials (a collective) is not part of it
+        Vs = -(-V // 8)
+        Ws = W[:Vs].contiguous()
+        mc.logprob_fwd(H, W, y, logp=logp, lse=lse)
         out = mc.rl_loss(logp, lr, st["mask"], st["cu"], st["cg"], st["rewards"], params)
-        if cache is None:
-            mc.logprob_bwd(H, W, y, lse, out["dlogp"], dhidden=dH, dweight=dW, workspace=ws_b)
-        else:
-            mc.logprob_bwd_cached(H, W, y, lse, out["dlogp"], cache, dhidden=dH, dweight=dW,
-                                  workspace=ws_b)
-        return out
+        dlogp = out["dlogp"]
+        ws_f = torch.empty(lib.mc_logprob_fwd_workspace_size(T, d, Vs, 1), dtype=torch.uint8,
+                           device=dev)
+        ws_b = torch.empty(lib.mc_logprob_bwd_workspace_size(T, d, Vs, 1), dtype=torch.uint8,
+                           device=dev)
+        part = torch.empty(4, T, dtype=torch.float32, device=dev)
+        dH = torch.empty(T, d, dtype=torch.float32, device=dev)
+        dWs = torch.empty(Vs, d, dtype=torch.float32, device=dev)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    print(f"[bench] warmup done ({args.warmup} steps), timing {args.steps}", file=sys.stderr,
-          flush=True)
+        def step():
+            mc.logprob_fwd_shard(H, Ws, y, 0, V, partial=part, workspace=ws_f)
+            mc.logprob_bwd_shard(H, Ws, y, lse, dlogp, 0, V, dhidden=dH, dweight=dWs,
+                                 workspace=ws_b)
+        res = time_steps(step, args.steps, args.warmup, sampler, flush, args.flush_reps)
+        summ = summary(res, T, 6.0 * T * d * Vs, 8.0 * T * d * Vs)
+        config.update(workload=config["workload"] + f"; vocabulary shard of {Vs} rows (V/8)",
+                      V_shard=Vs, backward="recompute logits (shard)")
+        line.update(summ)
+        line["config"] = config
+        line["metric"] = METRIC + " (one GPU's V/8 shard)"
+    elif fwd_only:
+        ws_f = torch.empty(lib.mc_logprob_fwd_workspace_size(T, d, V, 1), dtype=torch.uint8,
+                           device=dev)
 
-    mc.profiler_reset()
-    mc.profiler_enable(True)
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(args.steps):
-        out = step()
-    e1.record()
-    torch.cuda.synchronize()
-    mc.profiler_enable(False)
-    kernels = mc.profiler_read()
-    ms = e0.elapsed_time(e1) / args.steps
-    n_valid = int(out["n_valid"].item())
-    loss = float(out["loss"].item())
+        def step():
+            mc.logprob_fwd(H, W, y, logp=logp, lse=lse, workspace=ws_f)
+        res = time_steps(step, args.steps, args.warmup, sampler, flush, args.flush_reps)
+        summ = summary(res, T, 2.0 * T * d * V, 2.0 * T * d * V)
+        config.update(backward="none (forward-only workload)")
+        line.update(summ)
+        line["config"] = config
+        line["metric"] = "fused logprob fwd tokens/s (forward-only workload); % bf16 MFMA peak"
+    else:
+        ws_f = torch.empty(lib.mc_logprob_fwd_workspace_size(T, d, V, 1), dtype=torch.uint8,
+                           device=dev)
+        dH = torch.empty(T, d, dtype=torch.float32, device=dev)
+        dW = torch.empty(V, d, dtype=torch.float32, device=dev)
+        results = {}
+        if args.step in ("both", "recompute"):
+            ws_b = torch.empty(lib.mc_logprob_bwd_workspace_size(T, d, V, 1), dtype=torch.uint8,
+                               device=dev)
 
-    counted = 6.0 * T * d * V
-    tflops = counted / (ms * 1e-3) / 1e12
-    dom_name, dom = max(kernels.items(), key=lambda kv: kv[1]["ms"])
-    dom_ms = dom["ms"] / dom["launches"]
-    achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
-    traffic = None
-    if TRAFFIC["sources_sha256"] == sources_digest():
-        traffic = TRAFFIC["bytes_per_launch"].get(dom_name)
-    roofline = {"bound": "mfma", "kernel": dom_name, "achieved": achieved,
-                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                "traffic": traffic, "avg_launch_ms": dom_ms,
-                "algorithmic_flops_per_launch": dom["flops"] / dom["launches"]}
-    phases = {k: {"ms_per_launch": v["ms"] / v["launches"], "launches": v["launches"],
-                  "tflops": (v["flops"] / (v["ms"] * 1e-3) / 1e12) if v["flops"] else None,
-                  "GBps_algorithmic": v["bytes"] / (v["ms"] * 1e-3) / 1e9}
-              for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms"])}
-    print(f"[bench] {ms:.3f} ms/step, {tflops:.1f} TFLOP/s counted", file=sys.stderr, flush=True)
+            def step():
+                mc.logprob_fwd(H, W, y, logp=logp, lse=lse, workspace=ws_f)
+                out = mc.rl_loss(logp, lr, st["mask"], st["cu"], st["cg"], st["rewards"], params)
+                mc.logprob_bwd(H, W, y, lse, out["dlogp"], dhidden=dH, dweight=dW,
+                               workspace=ws_b)
+                return out
+            log("timing the recompute step")
+            results["recompute"] = time_steps(step, args.steps, args.warmup, sampler, flush,
+                                              args.flush_reps)
+            del ws_b
+            torch.cuda.empty_cache()
+        if args.step in ("both", "cached"):
+            ws_c = torch.empty(lib.mc_logprob_bwd_cached_workspace_size(T, d, V, 1),
+                               dtype=torch.uint8, device=dev)
+            cache = mc.softmax_cache(H, W)
 
-    base = None
+            def step():
+                mc.logprob_fwd_cached(H, W, y, cache, logp=logp, lse=lse, workspace=ws_f)
+                out = mc.rl_loss(logp, lr, st["mask"], st["cu"], st["cg"], st["rewards"], params)
+                mc.logprob_bwd_cached(H, W, y, lse, out["dlogp"], cache, dhidden=dH, dweight=dW,
+                                      workspace=ws_c)
+                return out
+            log("timing the cached step")
+            results["cached"] = time_steps(step, args.steps, args.warmup, sampler, flush,
+                                           args.flush_reps)
+            del ws_c, cache
+        head = "recompute" if "recompute" in results else "cached"
+        for name, res in results.items():
+            out = res["out"]
+            summ = summary(res, T, 6.0 * T * d * V,
+                           (8.0 if name == "recompute" else 6.0) * T * d * V)
+            summ["loss"] = float(out["loss"].item())
+            summ["n_valid"] = int(out["n_valid"].item())
+            results[name] = summ
+        line.update(results[head])
+        config["backward"] = ("recompute logits: the forward writes no [T,V] tensor"
+                              if head == "recompute" else "softmax cache: the forward writes a "
+                              "[T,V] bf16 cache")
+        line["config"] = config
+        if head == "recompute" and "cached" in results:
+            line["cached"] = results["cached"]
+        log(f"{head}: {line['ms_per_step']:.3f} ms/step, {line['counted_tflops']:.1f} TFLOP/s "
+            f"counted ({100 * line['mfma_frac']:.1f}% of peak)")
+
     if not args.no_cpu_baseline:
-        print("[bench] timing the fp64 oracle baseline sample", file=sys.stderr, flush=True)
-        base = cpu_baseline(args.config, H, W, y, s, args.cpu_seconds)
-
-    line = {
-        "metric": METRIC,
-        "value": T / (ms * 1e-3),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": workload_name(cfg, s), "T": T, "d": d, "V": V,
-                   "sequences": s.B, "groups": s.NG, "parallelism": "none (1 GPU)",
-                   "backward": "recompute logits" if args.recompute else "softmax cache"},
-        "mfma_frac": tflops / PEAK_BF16_TFLOPS,
-        "counted_tflops": tflops,
-        "roofline": roofline,
-        "cpu_baseline": base,
-        "kernels": phases,
-        "loss": loss,
-        "n_valid": n_valid,
-    }
-    print(json.dumps(line), flush=True)
+        log("timing the fp64 oracle baseline sample")
+        line["cpu_baseline"] = cpu_baseline(H, W, y, s, args.cpu_seconds, fwd_only=fwd_only)
+    else:
+        line["cpu_baseline"] = None
+    order = ["metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+             "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config",
+             "mfma_frac", "roofline", "cpu_baseline"]
+    print(json.dumps({**{k: line[k] for k in order if k in line},
+                      **{k: v for k, v in line.items() if k not in order}}), flush=True)
 
 
 if __name__ == "__main__":
