@@ -273,6 +273,33 @@ mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const float
                        const mc_rl_params_t* params, const mc_rl_outputs_t* out,
                        void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * mc_rl_loss without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation).  Same arguments, outputs and results as
+ * mc_rl_loss (the same kernels), but its scratch is a fixed device array of
+ * MC_RL_LOSS_NOALLOC_SCRATCH_BYTES (4 MiB) inside the library, one copy per
+ * GPU, held until the process ends; the call itself allocates nothing.
+ *   Limit     mc_rl_loss_workspace_size(T, B, NG) must not exceed
+ *             mc_rl_loss_noalloc_max_bytes() (= the array size; it fits
+ *             B <= 65536 sequences in at most 65536 groups, any T);
+ *             larger batches return MC_ERR_UNSUPPORTED and enqueue nothing.
+ *   Stream    must belong to the current device (else MC_ERR_INVALID_ARG).
+ *   Races     every call on one GPU shares that GPU's array: calls whose
+ *             work may overlap on one GPU (other host threads, other
+ *             streams) race and must be serialised by the caller.  The
+ *             array keeps the last call's contents; every value the kernels
+ *             read is written earlier in the same call.
+ * ------------------------------------------------------------------------ */
+#define MC_RL_LOSS_NOALLOC_SCRATCH_BYTES ((size_t)4 << 20)
+size_t mc_rl_loss_noalloc_max_bytes(void);
+mc_status_t mc_rl_loss_noalloc(const float* logp, const float* logp_rollout,
+                               const float* logp_ref, const uint8_t* loss_mask,
+                               const int32_t* cu_seqlens, const int32_t* cu_groups,
+                               const float* rewards, int64_t T, int32_t B, int32_t NG,
+                               const mc_rl_params_t* params, const mc_rl_outputs_t* out,
+                               void* stream);
+
 /* PrimeEcho trajectory rewards (Sec. 4.4.3, Eq. 9-10), one per trajectory:
  *   R_i = alpha s_i1 + (1 - alpha) max_{k <= K_i} s_ik
  *         + beta1 [success_i1] + beta2 [not success_i1 and success_i2]

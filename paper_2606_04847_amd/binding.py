@@ -123,6 +123,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mc_rl_loss.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i32, _c_i32,
                                ctypes.POINTER(RLParamsC), ctypes.POINTER(RLOutputsC),
                                _vp, _c_sz, _vp]
+    lib.mc_rl_loss_noalloc.restype = ctypes.c_int
+    lib.mc_rl_loss_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_i32,
+                                       _c_i32, ctypes.POINTER(RLParamsC),
+                                       ctypes.POINTER(RLOutputsC), _vp]
+    lib.mc_rl_loss_noalloc_max_bytes.restype = _c_sz
+    lib.mc_rl_loss_noalloc_max_bytes.argtypes = []
     lib.mc_primeecho_rewards.restype = ctypes.c_int
     lib.mc_primeecho_rewards.argtypes = [_vp, _vp, _vp, _c_i32, _c_i32, ctypes.c_float,
                                          ctypes.c_float, ctypes.c_float, _vp, _vp]
@@ -464,11 +470,12 @@ def logprob_bwd_cached(hidden, weight, targets, lse, dlogp, cache, *, dhidden=No
 
 def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
             params: RLParams | None = None, *, logp_ref=None, workspace=None, stream=None,
-            out=None):
+            out=None, noalloc=False):
     """RL objective over a packed batch (see mc_rl_loss).  Returns a dict of
     device tensors: loss, dlogp, seq_mask, seq_len, n_valid, adv, stat_abs,
     stat_signed, clip_frac, error_flag, kl, token_frac (`out` may supply
-    them)."""
+    them).  noalloc=True calls mc_rl_loss_noalloc, which takes no workspace
+    (with `out` given, this wrapper allocates nothing either)."""
     torch = _torch()
     lib = load_library()
     p = params or RLParams()
@@ -504,12 +511,18 @@ def rl_loss(logp, logp_rollout, loss_mask, cu_seqlens, cu_groups, rewards,
                       for k in _OUT_FIELDS])
     pc = p.to_c()
     owned = [] if given is not None else list(out.values())
-    need = lib.mc_rl_loss_workspace_size(T, B, NG)
-    ws, nbytes = _workspace(need, dev, workspace, owned)
-    _check(lib.mc_rl_loss(_ptr(logp), _ptr(logp_rollout), _ptr(logp_ref), _ptr(loss_mask),
-                          _ptr(cu_seqlens),
-                          _ptr(cu_groups), _ptr(rewards), T, B, NG, ctypes.byref(pc),
-                          ctypes.byref(oc), _ptr(ws), nbytes, _stream(stream)), "mc_rl_loss")
+    if noalloc:
+        _check(lib.mc_rl_loss_noalloc(_ptr(logp), _ptr(logp_rollout), _ptr(logp_ref),
+                                      _ptr(loss_mask), _ptr(cu_seqlens), _ptr(cu_groups),
+                                      _ptr(rewards), T, B, NG, ctypes.byref(pc),
+                                      ctypes.byref(oc), _stream(stream)), "mc_rl_loss_noalloc")
+    else:
+        need = lib.mc_rl_loss_workspace_size(T, B, NG)
+        ws, nbytes = _workspace(need, dev, workspace, owned)
+        _check(lib.mc_rl_loss(_ptr(logp), _ptr(logp_rollout), _ptr(logp_ref), _ptr(loss_mask),
+                              _ptr(cu_seqlens),
+                              _ptr(cu_groups), _ptr(rewards), T, B, NG, ctypes.byref(pc),
+                              ctypes.byref(oc), _ptr(ws), nbytes, _stream(stream)), "mc_rl_loss")
     _keep_alive(stream, *owned)
     return out
 

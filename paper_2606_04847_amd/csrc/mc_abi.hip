@@ -228,7 +228,7 @@ size_t mc_rl_loss_workspace_size(int64_t T, int32_t B, int32_t NG) {
   return mc::loss_workspace(T, B, NG);
 }
 
-// Argument checks of mc_rl_loss.
+// Argument checks shared by mc_rl_loss and mc_rl_loss_noalloc.
 static mc_status_t check_loss_args(const float* logp, const float* logp_rollout,
                                    const int32_t* cu_seqlens, const int32_t* cu_groups,
                                    const float* rewards, int64_t T, int32_t B, int32_t NG,
@@ -278,6 +278,34 @@ mc_status_t mc_rl_loss(const float* logp, const float* logp_rollout, const float
   return from_hip(mc::launch_loss(logp, logp_rollout, logp_ref, loss_mask, cu_seqlens, cu_groups,
                                   rewards, T, B, NG, *params, *out, ws,
                                   static_cast<hipStream_t>(stream)));
+}
+
+size_t mc_rl_loss_noalloc_max_bytes(void) { return MC_RL_LOSS_NOALLOC_SCRATCH_BYTES; }
+
+mc_status_t mc_rl_loss_noalloc(const float* logp, const float* logp_rollout,
+                               const float* logp_ref, const uint8_t* loss_mask,
+                               const int32_t* cu_seqlens, const int32_t* cu_groups,
+                               const float* rewards, int64_t T, int32_t B, int32_t NG,
+                               const mc_rl_params_t* params, const mc_rl_outputs_t* out,
+                               void* stream) {
+  mc_status_t st = check_loss_args(logp, logp_rollout, cu_seqlens, cu_groups, rewards, T, B, NG,
+                                   params, out);
+  if (st != MC_OK) return st;
+  if (mc::loss_workspace(T, B, NG) > MC_RL_LOSS_NOALLOC_SCRATCH_BYTES) return MC_ERR_UNSUPPORTED;
+  // the scratch is per GPU: the stream must belong to the current device
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return MC_ERR_HIP;
+  if (s != nullptr) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(s, &sdev) != hipSuccess) return MC_ERR_HIP;
+    if (int(sdev) != dev) return MC_ERR_INVALID_ARG;
+  }
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  if (mc::loss_scratch(&ws, &ws_bytes) != hipSuccess) return MC_ERR_HIP;
+  return from_hip(mc::launch_loss(logp, logp_rollout, logp_ref, loss_mask, cu_seqlens, cu_groups,
+                                  rewards, T, B, NG, *params, *out, ws, s, false));
 }
 
 mc_status_t mc_primeecho_rewards(const float* scores, const uint8_t* success,

@@ -85,5 +85,8 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
                        const float* rewards, int64_t T, int32_t B, int32_t NG,
                        const mc_rl_params_t& p, const mc_rl_outputs_t& out, void* ws,
                        hipStream_t s, bool profile = true);
+// Device address and size of the current GPU's fixed loss scratch (no
+// allocation; looked up once per device).
+hipError_t loss_scratch(void** ptr, size_t* bytes);
 
 }  // namespace mc

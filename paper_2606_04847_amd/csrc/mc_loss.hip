@@ -6,7 +6,15 @@
 // sequence, wave-level reductions; all sums in fp64 and in a fixed order.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "mc_internal.hpp"
+
+// Device scratch of the allocation-free loss entry point (mc_rl_loss_noalloc):
+// one copy per GPU, held for the life of the process.  Host code never uses
+// this name as an address (on the host it is a stand-in symbol); it takes
+// the device address that hipGetSymbolAddress returns for the current GPU.
+static __device__ __align__(256) char scratch[MC_RL_LOSS_NOALLOC_SCRATCH_BYTES];
 
 namespace mc {
 
@@ -336,6 +344,32 @@ hipError_t launch_primeecho(const float* scores, const uint8_t* success, const i
   hipLaunchKernelGGL(k_primeecho, dim3(cdiv(B, 256)), dim3(256), 0, s, scores, success, n_turns,
                      B, Kmax, alpha, beta1, beta2, rewards);
   return hipGetLastError();
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// The current GPU's copy of `scratch`, looked up once per device with that
+// device current; no allocation.
+hipError_t loss_scratch(void** ptr, size_t* bytes) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  *bytes = MC_RL_LOSS_NOALLOC_SCRATCH_BYTES;
+  return hipSuccess;
 }
 
 hipError_t launch_loss(const float* logp, const float* logp_rollout, const float* logp_ref,

@@ -212,3 +212,19 @@ def test_cached_argument_checks(lib):
     assert bwd(FAKE_WS, need_c, dh=FAKE + 4) == INVALID
 
 
+
+def test_noalloc_loss_rejects_oversized_batches_on_the_host(lib):
+    # the size check comes before any HIP call
+    cap = lib.mc_rl_loss_noalloc_max_bytes()
+    assert cap == 4 << 20
+    assert lib.mc_rl_loss_workspace_size(0, 65536, 65536) <= cap
+    p = binding.RLParams().to_c()
+    o = binding.RLOutputsC(FAKE, FAKE, *([None] * (len(binding._OUT_FIELDS) - 2)))
+    B = 1 << 20
+    st = lib.mc_rl_loss_noalloc(FAKE, FAKE, None, None, FAKE, FAKE, FAKE, B, B, 1,
+                                ctypes.byref(p), ctypes.byref(o), None)
+    assert st == UNSUP
+    bad = binding.RLParams(filter="none").to_c()
+    bad.delta = -1.0
+    assert lib.mc_rl_loss_noalloc(FAKE, FAKE, None, None, FAKE, FAKE, FAKE, 8, 2, 1,
+                                  ctypes.byref(bad), ctypes.byref(o), None) == INVALID
