@@ -54,17 +54,22 @@ __device__ __forceinline__ int wrow(int i, int e, int lane) {
 // A 256 x 256 bf16 tile (rows: 256 vocabulary entries of a chunk, columns:
 // 256 tokens) staged in the workgroup's LDS operand buffers for stores of
 // whole panel rows: four 32 KiB panels (64 vocabulary entries each) of 256
-// token rows x 128 bytes, the 16-byte chunk index XOR-ed with (t >> 1) & 7.
-// The 8-byte staging writes of one instruction are served 32 lanes at a time
-// over 64 four-byte banks; those lanes hold 16 consecutive tokens (two 4-row
-// groups each): token parity picks the bank half (rows are 128 bytes) and
-// (t >> 1) & 7 a distinct chunk for each of the 8 tokens of one parity, so
-// the 64 dwords hit 64 distinct banks (XOR-ing with t & 7 put tokens t and
-// t + 8 on the same banks: two cycles per pass).
+// token rows x 128 bytes.  A lane stages 4 consecutive vocabulary entries of
+// one token (8 bytes, half of a 16-byte chunk); the 16 lanes of one such
+// write hold 16 consecutive tokens.  The chunk index is XOR-ed with
+// (t >> 1) & 7 and the chunk's two 8-byte halves are swapped when
+// (t ^ (t >> 1)) & 1: the 16 tokens of a lane group then cover 16 distinct
+// (chunk, half) slots, i.e. all 32 banks of a 128-byte row pair, and the 32
+// lanes of two groups all 64 banks of the two rows they touch (XOR-ing the
+// chunk with t & 7 alone put tokens t and t + 8 on the same banks, and
+// (t >> 1) & 7 alone tokens t and t ^ 1: 1023 conflict cycles per tile
+// counted).  The reader swaps the halves back.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int panel_swz(int t) { return (t >> 1) & 7; }
+__device__ __forceinline__ int panel_half(int t) { return (t ^ (t >> 1)) & 1; }
 __device__ __forceinline__ int panel_stage_off(int v, int t) {
-  return (v >> 6) * 32768 + t * 128 + ((((v & 63) >> 3) ^ panel_swz(t)) << 4) + ((v & 7) << 1);
+  return (v >> 6) * 32768 + t * 128 + ((((v & 63) >> 3) ^ panel_swz(t)) << 4) +
+         ((((v >> 2) & 1) ^ panel_half(t)) << 3) + ((v & 3) << 1);
 }
 
 // Each panel's 256 token rows are 32 KiB of contiguous memory: 16-byte
@@ -85,11 +90,14 @@ __device__ __forceinline__ void store_staged_panels(const char* lds, bf16_t* P, 
   static_assert(kRows % 16 == 0, "the swizzle of row r0 + kRows k is that of r0");
   const int ch = threadIdx.x & 7, r0 = threadIdx.x >> 3;
   const int sw = (ch ^ panel_swz(r0)) << 4;
+  const bool swap = panel_half(r0) != 0;
   u32x4 v[kIters];
 #pragma unroll
-  for (int it = 0; it < kIters; ++it)
-    v[it] = *reinterpret_cast<const u32x4*>(lds + (it / kRounds) * 32768 +
-                                            ((it % kRounds) * kRows + r0) * 128 + sw);
+  for (int it = 0; it < kIters; ++it) {
+    const u32x4 x = *reinterpret_cast<const u32x4*>(lds + (it / kRounds) * 32768 +
+                                                    ((it % kRounds) * kRows + r0) * 128 + sw);
+    v[it] = swap ? u32x4{x[2], x[3], x[0], x[1]} : x;
+  }
   bf16_t* const base = P + (m0 / kPanel) * pld * kPanel + (n0 + r0) * kPanel + ch * 8;
 #pragma unroll
   for (int it = 0; it < kIters; ++it) {
@@ -763,49 +771,147 @@ __global__ void k_bucket_rank(const int64_t* __restrict__ y, int64_t T, int64_t 
   const int64_t yy = y[t] - v_off;
   if (yy < 0 || yy >= V) return;
   const int b = offsets[yy], e = offsets[yy + 1];
-  int rank = 0;
-  for (int p = b; p < e; ++p) rank += unsorted[p] < int(t);
+  // 16 independent loads per step: a large bucket's scan is not one load
+  // latency per entry
+  int rank = 0, p = b;
+  for (; p + 16 <= e; p += 16) {
+    int u[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) u[i] = unsorted[p + i];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) rank += u[i] < int(t);
+  }
+  for (; p < e; ++p) rank += unsorted[p] < int(t);
   sorted[b + rank] = int(t);
 }
 
-// dW[v, :] += sum over tokens t with y_t = v (ascending t) of dlogp_t h_t.
-// One block per bucketed position; only the first position of a bucket works.
-// Each thread owns 4 consecutive columns (d is a multiple of 8).
+// dW[v, :] += sum over tokens t with y_t = v (ascending t) of dlogp_t h_t,
+// over the bucketed token list `sorted` (tokens grouped by target, ascending
+// t within a bucket) cut into segments of kSeg positions.  k_onehot_seg:
+// one workgroup per (segment, block of 1024 columns); it walks the segment's
+// positions in order and, for each run of one bucket, sums dlogp_t h_t over
+// the run's tokens with a nonzero dlogp (4 columns per thread).  A bucket
+// that lies wholly inside the segment is added to its row of dW at once; a
+// run of a bucket that crosses the segment's edge goes to a slot of the
+// segment (slot 0: the bucket began in an earlier segment, slot 1: it
+// continues past this one).  k_onehot_join adds each crossing bucket's
+// slots to its row in segment order.  So a large bucket is spread over many
+// workgroups, and every row's sum has a fixed order (run order, then
+// segment order): bit-identical from run to run.  A bucket whose tokens all
+// have zero dlogp (outside the loss mask, filtered, clipped) leaves its row
+// as it is.
+constexpr int kSeg = 16;
+constexpr int kOnehotAhead = 8;
 template <typename T>
-__global__ __launch_bounds__(256) void k_onehot_dw(const T* __restrict__ H,
-                                                   const int64_t* __restrict__ y,
-                                                   const float* __restrict__ dlogp,
-                                                   const int* __restrict__ offsets,
-                                                   const int* __restrict__ sorted, int64_t d,
-                                                   int64_t v_off, int64_t V,
-                                                   float* __restrict__ dW) {
-  const int p = blockIdx.x;
-  if (p >= offsets[V]) return;
-  const int t0 = sorted[p];
-  const int64_t v = y[t0] - v_off;
-  const int b = offsets[v], e = offsets[v + 1];
-  if (p != b) return;
-  // tokens with a zero dlogp (outside the loss mask, filtered, clipped) add
-  // nothing: a bucket of only such tokens leaves its row as it is, and the
-  // others skip their rows of H
-  bool live = false;
-  for (int q = b; q < e && !live; ++q) live = dlogp[sorted[q]] != 0.0f;
-  if (!live) return;
-  float* o = dW + v * d;
-  for (int64_t k = int64_t(threadIdx.x) * 4; k < d; k += 4 * int64_t(blockDim.x)) {
-    f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int q = b; q < e; ++q) {
-      const int t = sorted[q];
-      const float g = dlogp[t];
-      if (g == 0.0f) continue;
-      const T* h = H + int64_t(t) * d + k;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) s[c] += g * float(h[c]);
-    }
-    f32x4 cur = *reinterpret_cast<const f32x4*>(o + k);
-    cur += s;
-    *reinterpret_cast<f32x4*>(o + k) = cur;
+__global__ __launch_bounds__(256) void k_onehot_seg(const T* __restrict__ H,
+                                                    const int64_t* __restrict__ y,
+                                                    const float* __restrict__ dlogp,
+                                                    const int* __restrict__ offsets,
+                                                    const int* __restrict__ sorted, int64_t d,
+                                                    int64_t v_off, int64_t V,
+                                                    float* __restrict__ dW,
+                                                    float* __restrict__ slots,
+                                                    int* __restrict__ slot_live) {
+  __shared__ int s_t[kSeg], s_v[kSeg];
+  __shared__ float s_g[kSeg];
+  const int n_pos = offsets[V];
+  const int x = blockIdx.x;
+  const int p0 = x * kSeg;
+  if (p0 >= n_pos) return;                                   // uniform
+  const int p1 = min(p0 + kSeg, n_pos), n = p1 - p0;
+  if (int(threadIdx.x) < n) {
+    const int t = sorted[p0 + threadIdx.x];
+    s_t[threadIdx.x] = t;
+    s_g[threadIdx.x] = dlogp[t];
+    s_v[threadIdx.x] = int(y[t] - v_off);
   }
+  __syncthreads();
+  const int64_t k = (int64_t(blockIdx.y) * blockDim.x + threadIdx.x) * 4;
+  const bool act = k < d;                                    // d is a multiple of 8
+  for (int q = 0; q < n;) {
+    const int v = s_v[q];
+    int r = q + 1;
+    while (r < n && s_v[r] == v) ++r;                        // run [q, r) of bucket v
+    const int b = offsets[v], e = offsets[v + 1];
+    const bool from_here = b >= p0, to_here = e <= p1;
+    // a bucket wholly in this segment: its row of dW is loaded together with
+    // the rows of H (one memory latency per run, not two)
+    f32x4* const row = reinterpret_cast<f32x4*>(dW + int64_t(v) * d + k);
+    f32x4 cur = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (from_here && to_here && act) cur = *row;
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    bool live = false;
+    for (int u0 = q; u0 < r; u0 += kOnehotAhead) {
+      float g[kOnehotAhead];
+      T h[kOnehotAhead][4];
+#pragma unroll
+      for (int u = 0; u < kOnehotAhead; ++u) {
+        g[u] = u0 + u < r ? s_g[u0 + u] : 0.0f;
+        if (g[u] != 0.0f && act) {
+          const T* hp = H + int64_t(s_t[u0 + u]) * d + k;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) h[u][c] = hp[c];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kOnehotAhead; ++u) {
+        if (g[u] == 0.0f) continue;
+        live = true;
+        if (act) {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) acc[c] += g[u] * float(h[u][c]);
+        }
+      }
+    }
+    if (from_here && to_here) {
+      if (live && act) *row = cur + acc;
+    } else {
+      const int slot = 2 * x + (from_here ? 1 : 0);
+      if (act) *reinterpret_cast<f32x4*>(slots + int64_t(slot) * d + k) = acc;
+      if (threadIdx.x == 0) slot_live[slot] = live ? 1 : 0;
+    }
+    q = r;
+  }
+}
+
+// The buckets that begin in segment x and continue past it: their slots (1
+// of segment x, 0 of the later segments they reach) summed in segment order
+// and added to their rows of dW.
+__global__ __launch_bounds__(256) void k_onehot_join(const int64_t* __restrict__ y,
+                                                     const int* __restrict__ offsets,
+                                                     const int* __restrict__ sorted, int64_t d,
+                                                     int64_t v_off, int64_t V,
+                                                     const float* __restrict__ slots,
+                                                     const int* __restrict__ slot_live,
+                                                     float* __restrict__ dW) {
+  const int n_pos = offsets[V];
+  const int x = blockIdx.x;
+  const int p0 = x * kSeg;
+  if (p0 >= n_pos) return;
+  const int p1 = min(p0 + kSeg, n_pos);
+  const int v = int(y[sorted[p1 - 1]] - v_off);
+  const int b = offsets[v], e = offsets[v + 1];
+  if (!(b >= p0 && e > p1)) return;
+  const int xl = (e - 1) / kSeg;                             // the bucket's last segment
+  bool live = slot_live[2 * x + 1] != 0;
+  for (int c = x + 1; c <= xl && !live; ++c) live = slot_live[2 * c] != 0;
+  if (!live) return;
+  const int64_t k = (int64_t(blockIdx.y) * blockDim.x + threadIdx.x) * 4;
+  if (k >= d) return;
+  f32x4 acc = *reinterpret_cast<const f32x4*>(slots + int64_t(2 * x + 1) * d + k);
+  int c = x + 1;
+  for (; c + 8 <= xl + 1; c += 8) {                          // 8 slot loads in flight
+    f32x4 w[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i] = *reinterpret_cast<const f32x4*>(slots + int64_t(2 * (c + i)) * d + k);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc += w[i];
+  }
+  for (; c <= xl; ++c) acc += *reinterpret_cast<const f32x4*>(slots + int64_t(2 * c) * d + k);
+  f32x4* o = reinterpret_cast<f32x4*>(dW + int64_t(v) * d + k);
+  f32x4 cur = *o;
+  cur += acc;
+  *o = cur;
 }
 
 // Named kernels, one per role of the shared tile core.
@@ -1043,6 +1149,8 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   int* sorted = cv.take<int>(Tn);
   int* scan_sums = cv.take<int>(cdiv(Vs, kScanBlock));
   float* slots = cv.take<float>(tail_slot_floats(d, min(chunk, Vs)));
+  float* seg_slots = cv.take<float>(size_t(2) * cdiv(Tn, kSeg) * d);
+  int* seg_live = cv.take<int>(size_t(2) * cdiv(Tn, kSeg));
   int ncu = 0, dev = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -1146,8 +1254,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   }
   if (dW) {
     ProfScope ps_(s, "logprob_bwd_onehot_dw", 2.0 * Tn * d, (es + 8.0) * Tn * d);
-    hipLaunchKernelGGL(k_onehot_dw<T>, dim3(Tn), dim3(256), 0, s, H, y, dlogp, offsets, sorted,
-                       d, v_off, Vs, dW);
+    const dim3 grid(unsigned(cdiv(Tn, kSeg)), unsigned(cdiv(d, 1024)));
+    hipLaunchKernelGGL(k_onehot_seg<T>, grid, dim3(256), 0, s, H, y, dlogp, offsets, sorted, d,
+                       v_off, Vs, dW, seg_slots, seg_live);
+    hipLaunchKernelGGL(k_onehot_join, grid, dim3(256), 0, s, y, offsets, sorted, d, v_off, Vs,
+                       seg_slots, seg_live, dW);
   }
   return hipGetLastError();
 }
@@ -1161,6 +1272,13 @@ int64_t bwd_chunk_cols(int64_t T, int64_t V, size_t esize) {
   if (cap >= V) return V;
   const int64_t n = cdiv(V, cap);
   return std::min(cap, cdiv(cdiv(V, n), kBN) * kBN);
+}
+
+// Segment slots of the one-hot scatter: 2 rows of d floats and 2 flags per
+// segment of kSeg bucketed positions.
+static size_t onehot_seg_bytes(int64_t T, int64_t d) {
+  const size_t nseg = size_t(cdiv(std::max<int64_t>(T, 1), kSeg));
+  return align_up(2 * nseg * size_t(d) * 4, kWsAlign) + align_up(2 * nseg * 4, kWsAlign);
 }
 
 size_t fwd_workspace(int64_t T, int64_t, int64_t V, mc_dtype_t) {
@@ -1186,6 +1304,7 @@ size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
   n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
   n += align_up(tail_slot_floats(d, V) * 4, kWsAlign);
+  n += onehot_seg_bytes(T, d);
   return n;
 }
 
@@ -1202,6 +1321,7 @@ size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
   n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
   n += align_up(tail_slot_floats(d, std::min(chunk, V)) * 4, kWsAlign);
+  n += onehot_seg_bytes(T, d);
   return n;
 }
 
