@@ -340,7 +340,8 @@ def cpu_baseline(H, W, y, s, target_s, fwd_only=False):
 # ---------------------------------------------------------------------------
 def summarize(path):
     """Per-kernel summary of a rocprofv3 output directory: average kernel
-    durations from a kernel trace, or per-dispatch counter values."""
+    durations from a kernel trace, or per-dispatch counter values with the
+    figures derived from them (clock, MFMA utilisation, memory-side bytes)."""
     rows_t, rows_c = [], []
     for f in glob.glob(os.path.join(path, "**", "*kernel_trace.csv"), recursive=True):
         rows_t += list(csv.DictReader(open(f)))
@@ -349,8 +350,10 @@ def summarize(path):
 
     def role(name):
         for key in ("k_fwd_logits_lse", "k_bwd_probs", "k_bwd_dhidden", "k_bwd_dweight",
-                    "k_cache_to_probs", "k_transpose", "k_onehot_dw", "k_lse_merge",
-                    "k_shard_partial", "k_tail_reduce", "k_surrogate", "k_seq_stats"):
+                    "k_cache_to_probs", "k_transpose", "k_onehot_seg", "k_onehot_join", "k_lse_merge",
+                    "k_shard_partial", "k_tail_reduce", "k_surrogate", "k_seq_stats",
+                    "k_bucket_rank", "k_bucket_fill", "k_hist", "k_scan", "k_fill_i32",
+                    "k_count", "k_finish", "k_loss_init", "copyBuffer"):
             if key in name:
                 return key
         return "other"
@@ -364,13 +367,37 @@ def summarize(path):
         for k, v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
             print(f"{k:24s} {len(v):6d} {statistics.fmean(v):9.3f} {min(v):9.3f} {max(v):9.3f}")
     if rows_c:
-        agg = {}
+        disp = {}
         for r in rows_c:
-            key = (role(r["Kernel_Name"]), r["Counter_Name"])
-            agg.setdefault(key, []).append(float(r["Counter_Value"]))
-        print(f"{'kernel':24s} {'counter':40s} {'dispatches':>10s} {'mean per dispatch':>20s}")
-        for (k, c), v in sorted(agg.items()):
-            print(f"{k:24s} {c:40s} {len(v):10d} {statistics.fmean(v):20.1f}")
+            d = disp.setdefault(r["Dispatch_Id"], {"role": role(r["Kernel_Name"]), "c": {},
+                                                   "ns": int(r["End_Timestamp"]) -
+                                                   int(r["Start_Timestamp"])})
+            d["c"][r["Counter_Name"]] = d["c"].get(r["Counter_Name"], 0.0) + float(
+                r["Counter_Value"])
+        by_role = {}
+        for d in disp.values():
+            by_role.setdefault(d["role"], []).append(d)
+        for k, ds in sorted(by_role.items()):
+            names = sorted({c for d in ds for c in d["c"]})
+            mean = {c: statistics.fmean(d["c"].get(c, 0.0) for d in ds) for c in names}
+            ns = statistics.fmean(d["ns"] for d in ds)
+            print(f"{k}  ({len(ds)} dispatches, {ns * 1e-6:.3f} ms each under counters)")
+            for c in names:
+                print(f"    {c:40s} {mean[c]:20.1f}")
+            g = mean.get("GRBM_GUI_ACTIVE")
+            if g:
+                per_xcd = g / 8.0                       # the counter sums the 8 XCDs
+                print(f"    {'clock (GRBM_GUI_ACTIVE / 8 / duration)':40s} "
+                      f"{per_xcd / ns:17.3f} GHz")
+                if "SQ_VALU_MFMA_BUSY_CYCLES" in mean:
+                    util = mean["SQ_VALU_MFMA_BUSY_CYCLES"] / (4 * 256 * per_xcd)
+                    print(f"    {'MFMA utilisation (busy / 1024 SIMDs)':40s} {100 * util:18.1f} %")
+            if "TCC_EA0_RDREQ_DRAM_32B_sum" in mean:
+                rb = 32.0 * mean["TCC_EA0_RDREQ_DRAM_32B_sum"]
+                print(f"    {'memory-side read bytes':40s} {rb:20.0f}  ({rb / ns:.1f} GB/s)")
+            if "TCC_EA0_WRREQ_WRITE_DRAM_32B_sum" in mean:
+                wb = 32.0 * mean["TCC_EA0_WRREQ_WRITE_DRAM_32B_sum"]
+                print(f"    {'memory-side write bytes':40s} {wb:20.0f}  ({wb / ns:.1f} GB/s)")
 
 
 # ---------------------------------------------------------------------------
