@@ -59,9 +59,30 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # are included: an upper bound on HBM bytes.  Valid only for kernel sources
 # with this digest (else null).
 TRAFFIC = {
-    "sources_sha256": None,
-    "read_bytes_per_launch": {},
-    "write_bytes_per_launch": {},
+    "sources_sha256":
+        "07130914dc5dee98fd696c2613aba6a7a70e46b140ce20a01c125f68f67caf22",
+    "read_bytes_per_launch": {
+        "logprob_fwd_gemm": 35485402208,
+        "logprob_fwd_merge": 78110880,
+        "logprob_bwd_probs": 32063022592,
+        "logprob_bwd_transpose": 689467328,
+        "logprob_bwd_dhidden": 30006559872,
+        "logprob_bwd_dweight": 30052229568,
+        "logprob_bwd_onehot_dw": 294634496,
+        "logprob_bwd_bucket": 5746432,
+        "rl_loss": 340480,
+    },
+    "write_bytes_per_launch": {
+        "logprob_fwd_gemm": 78367648,
+        "logprob_fwd_merge": 131072,
+        "logprob_bwd_probs": 4978934592,
+        "logprob_bwd_transpose": 689438720,
+        "logprob_bwd_dhidden": 268435456,
+        "logprob_bwd_dweight": 2556428416,
+        "logprob_bwd_onehot_dw": 69889056,
+        "logprob_bwd_bucket": 2513504,
+        "rl_loss": 80896,
+    },
 }
 
 
@@ -338,10 +359,11 @@ def cpu_baseline(H, W, y, s, target_s, fwd_only=False):
 # ---------------------------------------------------------------------------
 # rocprofv3 summaries (measurement aid)
 # ---------------------------------------------------------------------------
-def summarize(path):
+def summarize(path, only=None):
     """Per-kernel summary of a rocprofv3 output directory: average kernel
     durations from a kernel trace, or per-dispatch counter values with the
-    figures derived from them (clock, MFMA utilisation, memory-side bytes)."""
+    figures derived from them (clock, MFMA utilisation, memory-side bytes).
+    `only`: kernel roles to print (all when None)."""
     rows_t, rows_c = [], []
     for f in glob.glob(os.path.join(path, "**", "*kernel_trace.csv"), recursive=True):
         rows_t += list(csv.DictReader(open(f)))
@@ -376,16 +398,20 @@ def summarize(path):
                 r["Counter_Value"])
         by_role = {}
         for d in disp.values():
-            by_role.setdefault(d["role"], []).append(d)
+            if only is None or d["role"] in only:
+                by_role.setdefault(d["role"], []).append(d)
         for k, ds in sorted(by_role.items()):
             names = sorted({c for d in ds for c in d["c"]})
             mean = {c: statistics.fmean(d["c"].get(c, 0.0) for d in ds) for c in names}
             ns = statistics.fmean(d["ns"] for d in ds)
             print(f"{k}  ({len(ds)} dispatches, {ns * 1e-6:.3f} ms each under counters)")
+            long = ns >= 1e6      # per-dispatch clocks are meaningful for long dispatches only
             for c in names:
-                print(f"    {c:40s} {mean[c]:20.1f}")
+                if c != "GRBM_COUNT" and (long or c.startswith("TCC_EA0") or
+                                          c == "SQ_LDS_BANK_CONFLICT"):
+                    print(f"    {c:40s} {mean[c]:20.1f}")
             g = mean.get("GRBM_GUI_ACTIVE")
-            if g:
+            if g and long:
                 per_xcd = g / 8.0                       # the counter sums the 8 XCDs
                 print(f"    {'clock (GRBM_GUI_ACTIVE / 8 / duration)':40s} "
                       f"{per_xcd / ns:17.3f} GHz")
@@ -424,9 +450,10 @@ def main():
                          "memory-traffic counters against a known byte count)")
     ap.add_argument("--summarize", metavar="DIR",
                     help="print the per-kernel summary of a rocprofv3 output directory")
+    ap.add_argument("--only", metavar="K1,K2", help="with --summarize: kernels to print")
     args = ap.parse_args()
     if args.summarize:
-        summarize(args.summarize)
+        summarize(args.summarize, args.only.split(",") if args.only else None)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this "
