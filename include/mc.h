@@ -217,7 +217,8 @@ mc_status_t mc_logprob_bwd_shard(const void* hidden, const void* weight_shard,
  * and the backward turns E, in place, into the softmax part of G and runs
  * the two contractions on it.  E adds one rounding to the dtype before the
  * final one of the softmax operand (bf16: each element of that operand is
- * within 2^-8 relative of its exact value instead of 2^-9).
+ * within about 2^-7 relative of its exact value instead of bf16's unit
+ * roundoff 2^-8).
  *   cache     device, 256-byte aligned, at least mc_logprob_cache_size bytes;
  *             owned by the caller; written by mc_logprob_fwd_cached and
  *             consumed (overwritten) by one mc_logprob_bwd_cached call with
