@@ -9,7 +9,7 @@
  *     an online log-sum-exp and a gather of the target logit.  In the plain
  *     pair (mc_logprob_fwd / mc_logprob_bwd) the logits are never written to
  *     memory: the forward keeps only per-row partials and the backward
- *     recomputes the logits, writing their gradient (a bf16 transient per
+ *     recomputes the logits, writing their gradient (a 2-byte transient per
  *     vocabulary chunk) as the operand of its two contractions.  The cached
  *     pair (mc_logprob_fwd_cached / mc_logprob_bwd_cached) trades memory for
  *     that recomputation: its forward writes a [T, V] softmax cache;
@@ -185,8 +185,14 @@ mc_status_t mc_logprob_merge_shards(const float* partials, int32_t S, const int6
  *   dlogp    [T] fp32
  *   dhidden / dweight may be NULL to skip that gradient (not both).
  *   flags    MC_BWD_ACCUMULATE_* bits: accumulate into the outputs.
- * The softmax part is formed per vocabulary chunk as a transient operand
- * (dtype) in the workspace; logits are recomputed, never stored.
+ * The softmax part is formed per vocabulary chunk as a transient operand in
+ * the workspace; logits are recomputed, never stored.  For MC_BF16 inputs
+ * that operand and the transposed hidden and weight rows the contractions
+ * read are fp16, each scaled by a power of two chosen from its magnitude
+ * bound and unscaled exactly in fp32: each element of the softmax part is
+ * within 2^-11 relative of its exact value (elements far below the largest
+ * aside), against 2^-8 for a bf16 operand.  MC_F32 inputs use fp32
+ * operands.
  * ------------------------------------------------------------------------ */
 size_t mc_logprob_bwd_workspace_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dtype);
 mc_status_t mc_logprob_bwd(const void* hidden, const void* weight, const int64_t* targets,
@@ -215,10 +221,10 @@ mc_status_t mc_logprob_bwd_shard(const void* hidden, const void* weight_shard,
  *   E[t, v] = exp(z[t, v] - c_b[t])   (dtype, vocabulary panels)
  *   c_b[t]  = max of z[t, .] over block b of 128 vocabulary entries (fp32)
  * and the backward turns E, in place, into the softmax part of G and runs
- * the two contractions on it.  E adds one rounding to the dtype before the
- * final one of the softmax operand (bf16: each element of that operand is
- * within about 2^-7 relative of its exact value instead of bf16's unit
- * roundoff 2^-8).
+ * the two contractions on it.  The operand stays in the dtype, and E adds
+ * one rounding to it before the final one (bf16: each element of that
+ * operand is within about 2^-7 relative of its exact value, against 2^-11
+ * for the recompute pair's fp16 operand).
  *   cache     device, 256-byte aligned, at least mc_logprob_cache_size bytes;
  *             owned by the caller; written by mc_logprob_fwd_cached and
  *             consumed (overwritten) by one mc_logprob_bwd_cached call with

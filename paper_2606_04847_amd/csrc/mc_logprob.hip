@@ -6,6 +6,8 @@
 // by a deterministic bucketed scatter).
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "mc_internal.hpp"
 #include "mc_tile.hpp"
 
@@ -80,7 +82,8 @@ __device__ __forceinline__ int panel_stage_off(int v, int t) {
 // stored, from one base address per thread: as a loop of read, wait, store
 // (with 64-bit address arithmetic in each step) this took most of the
 // cache's cost in the forward.
-__device__ __forceinline__ void store_staged_panels(const char* lds, bf16_t* P, int64_t m0,
+template <typename TP>   // a 2-byte element type
+__device__ __forceinline__ void store_staged_panels(const char* lds, TP* P, int64_t m0,
                                                     int64_t n0, int64_t Tn, int64_t ld,
                                                     int64_t pld) {
   constexpr int64_t kPanel = 64;
@@ -98,7 +101,7 @@ __device__ __forceinline__ void store_staged_panels(const char* lds, bf16_t* P, 
                                                     ((it % kRounds) * kRows + r0) * 128 + sw);
     v[it] = swap ? u32x4{x[2], x[3], x[0], x[1]} : x;
   }
-  bf16_t* const base = P + (m0 / kPanel) * pld * kPanel + (n0 + r0) * kPanel + ch * 8;
+  TP* const base = P + (m0 / kPanel) * pld * kPanel + (n0 + r0) * kPanel + ch * 8;
 #pragma unroll
   for (int it = 0; it < kIters; ++it) {
     const int pn = it / kRounds, tl = (it % kRounds) * kRows + r0;
@@ -395,6 +398,63 @@ __global__ __launch_bounds__(256) void k_shard_merge(const float* __restrict__ p
 }
 
 // ---------------------------------------------------------------------------
+// Power-of-two scales of the recompute backward's fp16 operands.  The
+// transient operand and the transposed W and H are fp16 there (11 significant
+// bits against bf16's 8), so each needs its magnitudes inside fp16's range;
+// scaling by a power of two (ldexp: exact for any finite value that stays in
+// range) loses nothing, and the contractions' epilogues undo it exactly.  A
+// magnitude bound travels as the bits of a non-negative float in an unsigned
+// word (atomicMax orders them like the floats); a scale travels as its
+// exponent, since the one dlogp near fp32's smallest values needs is beyond
+// fp32's largest.
+// ---------------------------------------------------------------------------
+// e with bound = m 2^e, 0.5 <= m < 1, from the bits alone (subnormal bounds
+// included, whatever the denormal mode); bits != 0.
+__device__ __forceinline__ int bound_exponent(unsigned bits) {
+  const int ef = int(bits >> 23);
+  if (ef > 0) return ef - 126;
+  return (32 - __builtin_clz(bits)) - 149;   // m 2^-149 with m < 2^23
+}
+// -dlogp * softmax: magnitudes up to max |dlogp|, scaled below 2^14.
+__device__ __forceinline__ int probs_shift(unsigned bits) {
+  return (bits == 0u || bits >= 0x7f800000u) ? 0 : 14 - bound_exponent(bits);
+}
+// W and H: left unscaled while their bound lies in [2^-4, 2^15) (so the largest
+// converts to a finite fp16 value and values down to 2^-10 of it stay normal),
+// else scaled below 2^14.
+__device__ __forceinline__ int operand_shift(unsigned bits) {
+  if (bits == 0u || bits >= 0x7f800000u) return 0;
+  const int e = bound_exponent(bits);
+  return (e >= -3 && e <= 15) ? 0 : 14 - e;
+}
+// Undoes the shifts probs_shift(*bp) and operand_shift(*bo), one at a time
+// (their sum alone can leave fp32's exponent range while the result does
+// not).  Null bp: nothing to undo.
+struct Unscale {
+  int a, b;
+  __device__ __forceinline__ Unscale(const unsigned* bp, const unsigned* bo) {
+    a = bp != nullptr ? -probs_shift(*bp) : 0;
+    b = bp != nullptr ? -operand_shift(*bo) : 0;
+  }
+  __device__ __forceinline__ f32x4 operator()(f32x4 v) const {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = ldexpf(ldexpf(v[e], a), b);
+    return v;
+  }
+};
+// Raise *bound to x (>= 0) unless it is already at least x: after a few
+// workgroups the bound is rarely exceeded, so few atomics reach memory.
+__device__ __forceinline__ void raise_bound(unsigned* bound, float x) {
+  const unsigned b = __float_as_uint(x);
+  if (b > *reinterpret_cast<volatile unsigned*>(bound)) atomicMax(bound, b);
+}
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m));
+  return x;
+}
+
+// ---------------------------------------------------------------------------
 // Backward, step 1: recompute the logits of a vocabulary chunk (tile rows =
 // chunk columns v, tile columns = tokens t) and write the transient operand
 // P~[t, v] = -dlogp_t exp(z_tv - lse_t) (zero for ignored tokens and for the
@@ -403,15 +463,18 @@ __global__ __launch_bounds__(256) void k_shard_merge(const float* __restrict__ p
 // the (then idle) LDS operand buffers and written as whole 128-byte panel
 // rows; fp32: 4-element stores straight to memory.
 // ---------------------------------------------------------------------------
-template <typename T>
+// TP: the operand's type (fp16 for bf16 inputs, shifted by probs_shift of the
+// max |dlogp| bound when `bound` is set; the input type otherwise).
+template <typename T, typename TP = T>
 struct EpiProbs {
   const int64_t* y;
   const float* lse;
   const float* dlogp;
   int64_t Tn, V, width, ld, pld;   // V: full vocabulary (target validity); ld: padded chunk
                                    // width; pld: padded token count
-  T* P;                            // panel layout (see Lay::TileTK)
-  static constexpr int64_t kPanel = 128 / sizeof(T);
+  TP* P;                           // panel layout (see Lay::TileTK)
+  const unsigned* bound;           // max |dlogp| (fp16 operand) or null
+  static constexpr int64_t kPanel = 128 / sizeof(TP);
 
   // lse_t log2(e) and -dlogp_t (0 for ignored tokens) of this lane's kTN
   // token columns
@@ -421,6 +484,7 @@ struct EpiProbs {
   __device__ __forceinline__ Pre prologue(int64_t, int64_t n0) const {
     Pre p;
     const int lane = threadIdx.x & 63, wn = wave_n();
+    const int sh = bound != nullptr ? probs_shift(*bound) : 0;
 #pragma unroll
     for (int j = 0; j < kTN; ++j) {
       const int64_t t = n0 + wn * kWaveCols + j * 16 + (lane & 15);
@@ -429,7 +493,7 @@ struct EpiProbs {
       if (t < Tn) {
         const int64_t yy = y[t];
         p.l2[j] = lse[t] * kLog2e;
-        p.g[j] = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
+        p.g[j] = (yy >= 0 && yy < V) ? ldexpf(-dlogp[t], sh) : 0.0f;
       }
     }
     return p;
@@ -459,13 +523,13 @@ struct EpiProbs {
             if (!kFull && r + e >= vlim) p[e] = 0.0f;
           }
           const int vr = wm * kWaveRows + r;   // row of the tile
-          if constexpr (sizeof(T) == 2) {
-            typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+          if constexpr (sizeof(TP) == 2) {
+            typedef TP tp4 __attribute__((ext_vector_type(4)));
             *reinterpret_cast<u32x2*>(lds + panel_stage_off(vr, tl)) =
-                __builtin_bit_cast(u32x2, __builtin_convertvector(p, bf16x4));
+                __builtin_bit_cast(u32x2, __builtin_convertvector(p, tp4));
           } else {
             const int64_t c = m0 + vr;
-            T* dst = P + (c / kPanel) * pld * kPanel + t * kPanel + c % kPanel;
+            TP* dst = P + (c / kPanel) * pld * kPanel + t * kPanel + c % kPanel;
             *reinterpret_cast<f32x4*>(dst) = p;
           }
         }
@@ -484,7 +548,7 @@ struct EpiProbs {
       values<true>(acc, lds, lane, wm, wn, pre, vlim, llim, m0, n0);
     else
       values<false>(acc, lds, lane, wm, wn, pre, vlim, llim, m0, n0);
-    if constexpr (sizeof(T) == 2) {
+    if constexpr (sizeof(TP) == 2) {
       __syncthreads();
       store_staged_panels(lds, P, m0, n0, Tn, ld, pld);
     }
@@ -504,6 +568,11 @@ struct EpiDH {
   const int64_t* y;
   const float* dlogp;
   int64_t v_off, Vs;
+  // fp16 operands: bounds of max |dlogp| and of this chunk's W rows; the
+  // tile's shifts (probs_shift, operand_shift) are undone first (powers of
+  // two: exact).  Null: unscaled operands.
+  const unsigned* bound_p;
+  const unsigned* bound_w;
 
   struct Pre {};
   __device__ __forceinline__ Pre prologue(int64_t, int64_t) const { return Pre{}; }
@@ -518,6 +587,7 @@ struct EpiDH {
                                           char*, const Pre& = Pre{}) const {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wm = wave_m(), wn = wave_n();
+    const Unscale us(bound_p, bound_w);
     constexpr int kChunks = kBN / 4;               // 16-byte chunks per staged row
     constexpr int kIters = kWaveRows * kChunks / kThreads;
     static_assert(kWaveRows * kChunks * 16 <= kLdsGemm, "staging");
@@ -547,6 +617,7 @@ struct EpiDH {
         if (r >= rows || c >= cols) continue;   // cols and ldc are multiples of 4
         f32x4 v = *reinterpret_cast<const f32x4*>(lds + rl * (kChunks * 16) +
                                                   ((c4 ^ (rl & 15)) << 4));
+        v = us(v);
         float* o = C + r * ldc + c;
         if (accumulate) v += *reinterpret_cast<const f32x4*>(o);
         if (W != nullptr) {
@@ -572,6 +643,10 @@ struct EpiStoreT {
   float* C;
   int64_t ldc, rows, cols;
   int accumulate;
+  // fp16 operands: bounds of max |dlogp| and of H; the tile's shifts are
+  // undone (exact).  Null: unscaled.
+  const unsigned* bound_p = nullptr;
+  const unsigned* bound_h = nullptr;
 
   struct Pre {};
   __device__ __forceinline__ Pre prologue(int64_t, int64_t) const { return Pre{}; }
@@ -585,6 +660,7 @@ struct EpiStoreT {
                                           char*, const Pre& = Pre{}) const {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wm = wave_m(), wn = wave_n();
+    const Unscale us(bound_p, bound_h);
     constexpr int kHalf = kBN / 2;                 // columns per pass
     constexpr int kRowChunks = kBM / 4;            // 16-byte chunks per staged column
     static_assert(kHalf * kRowChunks * 16 <= kLdsGemm, "staging");
@@ -610,6 +686,7 @@ struct EpiStoreT {
         if (c < cols && r < rows) {   // rows, ldc and r are multiples of 4
           f32x4 v = *reinterpret_cast<const f32x4*>(lds + cl * (kRowChunks * 16) +
                                                     ((ch ^ (cl & 15)) << 4));
+          v = us(v);
           f32x4* o = reinterpret_cast<f32x4*>(C + c * ldc + r);
           if (accumulate) v += *o;
           *o = v;
@@ -619,6 +696,15 @@ struct EpiStoreT {
     }
   }
 };
+
+
+// bound = max |x| over n values (one wave per 64 values of a block).
+__global__ __launch_bounds__(256) void k_bound_abs(const float* __restrict__ x, int64_t n,
+                                                   unsigned* __restrict__ bound) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const float m = wave_max(i < n ? fabsf(x[i]) : 0.0f);
+  if ((threadIdx.x & 63) == 0) raise_bound(bound, m);
+}
 
 // out[c][r] = in[r][c] for r < rows, c < cols, and out[c][r] = 0 for
 // rows <= r < 64 ceil(rows / 64) (ld_out covers that padding; cols, ld_in and
@@ -631,38 +717,72 @@ struct EpiStoreT {
 // registers and stores it as rows 8b .. of output chunk a; every 8 lanes
 // cover one whole 128-byte row in each access.  Gives the backward's
 // contractions over the vocabulary and over tokens operands that run along K.
-template <typename T>
-__global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ in, int64_t rows,
+// TO != TI (bf16 -> fp16): the values are converted; with `bound` the first
+// pass (rescale = 0) converts unscaled and raises *bound to max |in|, and a
+// second launch (rescale = 1, row tiles strided over grid y) converts again
+// shifted by operand_shift(*bound) when that is not 0, and returns at once
+// otherwise.
+// grid y of the rescaling launch: when no rescaling is needed its
+// workgroups only read the bound and return
+constexpr int64_t kRescaleRows = 64;
+template <typename TI, typename TO>
+__global__ __launch_bounds__(256) void k_transpose(const TI* __restrict__ in, int64_t rows,
                                                    int64_t cols, int64_t ld_in,
-                                                   T* __restrict__ out, int64_t ld_out) {
-  constexpr int CE = 16 / sizeof(T);   // elements per 16-byte access
+                                                   TO* __restrict__ out, int64_t ld_out,
+                                                   unsigned* __restrict__ bound, int rescale) {
+  static_assert(sizeof(TI) == sizeof(TO), "same element size");
+  constexpr bool kConvert = !std::is_same<TI, TO>::value;
+  constexpr int CE = 16 / sizeof(TI);  // elements per 16-byte access
   constexpr int S = 64 / CE;           // lanes per 64-element row: 8 (bf16) or 16 (fp32)
+  int shift = 0;
+  if (rescale) {
+    shift = operand_shift(*bound);
+    if (shift == 0) return;
+  }
   const int lane = threadIdx.x & 63;
-  const int64_t r0 = int64_t(blockIdx.y) * 64;
   const int64_t c0 = (int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6)) * 64;
   if (c0 >= cols) return;
+  const int64_t nby = (rows + 63) / 64;
   constexpr int kPasses = (64 / CE) * (64 / CE) / 64;   // bf16: 1, fp32: 4
+  float mx = 0.0f;
+  for (int64_t by = blockIdx.y; by < nby; by += gridDim.y) {
+    const int64_t r0 = by * 64;
 #pragma unroll
-  for (int pass = 0; pass < kPasses; ++pass) {
-    const int blk = pass * 64 + lane;          // CE x CE block index within the tile
-    const int a = blk / S, b = blk % S;        // row block, column chunk
-    const int64_t c = c0 + int64_t(b) * CE;    // first input column of the chunk
-    T v[CE][CE];
+    for (int pass = 0; pass < kPasses; ++pass) {
+      const int blk = pass * 64 + lane;          // CE x CE block index within the tile
+      const int a = blk / S, b = blk % S;        // row block, column chunk
+      const int64_t c = c0 + int64_t(b) * CE;    // first input column of the chunk
+      TI v[CE][CE];
 #pragma unroll
-    for (int j = 0; j < CE; ++j) {
-      const int64_t r = r0 + int64_t(a) * CE + j;
-      u32x4 raw = {0u, 0u, 0u, 0u};
-      if (r < rows && c < cols) raw = *reinterpret_cast<const u32x4*>(in + r * ld_in + c);
-      *reinterpret_cast<u32x4*>(v[j]) = raw;
+      for (int j = 0; j < CE; ++j) {
+        const int64_t r = r0 + int64_t(a) * CE + j;
+        u32x4 raw = {0u, 0u, 0u, 0u};
+        if (r < rows && c < cols) raw = *reinterpret_cast<const u32x4*>(in + r * ld_in + c);
+        *reinterpret_cast<u32x4*>(v[j]) = raw;
+      }
+      if (c >= cols) continue;
+#pragma unroll
+      for (int i = 0; i < CE; ++i) {
+        TO o[CE];
+#pragma unroll
+        for (int j = 0; j < CE; ++j) {
+          if constexpr (kConvert) {
+            const float x = float(v[j][i]);
+            mx = fmaxf(mx, fabsf(x));
+            o[j] = TO(ldexpf(x, shift));
+          } else {
+            o[j] = v[j][i];
+          }
+        }
+        *reinterpret_cast<u32x4*>(out + (c + i) * ld_out + r0 + int64_t(a) * CE) =
+            *reinterpret_cast<const u32x4*>(o);
+      }
     }
-    if (c >= cols) continue;
-#pragma unroll
-    for (int i = 0; i < CE; ++i) {
-      T o[CE];
-#pragma unroll
-      for (int j = 0; j < CE; ++j) o[j] = v[j][i];
-      *reinterpret_cast<u32x4*>(out + (c + i) * ld_out + r0 + int64_t(a) * CE) =
-          *reinterpret_cast<const u32x4*>(o);
+  }
+  if constexpr (kConvert) {
+    if (bound != nullptr && !rescale) {
+      mx = wave_max(mx);
+      if (lane == 0) raise_bound(bound, mx);
     }
   }
 }
@@ -832,15 +952,16 @@ __global__ __launch_bounds__(256) void k_onehot_seg(const T* __restrict__ H,
     const int v = s_v[q];
     int r = q + 1;
     while (r < n && s_v[r] == v) ++r;                        // run [q, r) of bucket v
+    bool live = false;                                       // a token with nonzero dlogp
+    for (int u = q; u < r && !live; ++u) live = s_g[u] != 0.0f;
     const int b = offsets[v], e = offsets[v + 1];
     const bool from_here = b >= p0, to_here = e <= p1;
-    // a bucket wholly in this segment: its row of dW is loaded together with
-    // the rows of H (one memory latency per run, not two)
+    // a live bucket wholly in this segment: its row of dW is loaded together
+    // with the rows of H (one memory latency per run, not two)
     f32x4* const row = reinterpret_cast<f32x4*>(dW + int64_t(v) * d + k);
     f32x4 cur = {0.0f, 0.0f, 0.0f, 0.0f};
-    if (from_here && to_here && act) cur = *row;
+    if (from_here && to_here && live && act) cur = *row;
     f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-    bool live = false;
     for (int u0 = q; u0 < r; u0 += kOnehotAhead) {
       float g[kOnehotAhead];
       T h[kOnehotAhead][4];
@@ -856,7 +977,6 @@ __global__ __launch_bounds__(256) void k_onehot_seg(const T* __restrict__ H,
 #pragma unroll
       for (int u = 0; u < kOnehotAhead; ++u) {
         if (g[u] == 0.0f) continue;
-        live = true;
         if (act) {
 #pragma unroll
           for (int c = 0; c < 4; ++c) acc[c] += g[u] * float(h[u][c]);
@@ -1001,18 +1121,22 @@ __global__ __launch_bounds__(kThreads, 1) void k_fwd_logits_lse(Operand A, Opera
   gemm_body<T, Lay::KMajor, Lay::KMajor, EpiFwd<T>, 2, kDeepFwdA>(A, B, K, nTm, nTn, epi, lds,
                                                                   kGroupVT);
 }
-template <typename T>
+// T: the inputs' type, TP: the operand's (see EpiProbs)
+template <typename T, typename TP>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B, int64_t K,
-                                                           int nTm, int nTn, EpiProbs<T> epi) {
+                                                           int nTm, int nTn,
+                                                           EpiProbs<T, TP> epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
-  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiProbs<T>, 2, kDeepFwdA>(A, B, K, nTm, nTn, epi, lds,
-                                                                    kGroupVT);
+  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiProbs<T, TP>, 2, kDeepFwdA>(A, B, K, nTm, nTn, epi,
+                                                                        lds, kGroupVT);
 }
-template <typename T>
+// TG: the contraction's operand type (the operand panels and W^T), T: the
+// weight's, read by the one-hot part
+template <typename TG, typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand B, int64_t K,
                                                              int nTm, int nTn, EpiDH<T> epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
-  gemm_body<T, Lay::TileTK, Lay::KMajor, EpiDH<T>, 2, kDeepDhA>(A, B, K, nTm, nTn, epi, lds);
+  gemm_body<TG, Lay::TileTK, Lay::KMajor, EpiDH<T>, 2, kDeepDhA>(A, B, K, nTm, nTn, epi, lds);
 }
 // dW^T = H^T P~ : tile rows are hidden dimensions (A = H^T, along the
 // tokens), tile columns vocabulary entries (B = the operand panels read
@@ -1060,7 +1184,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand 
 __global__ __launch_bounds__(256) void k_tail_reduce(const float* __restrict__ slots,
                                                      TailSplit ts, int nTm, int nTn,
                                                      float* __restrict__ C, int64_t ldc,
-                                                     int64_t rows, int64_t cols, int accumulate) {
+                                                     int64_t rows, int64_t cols, int accumulate,
+                                                     const unsigned* bound_p,
+                                                     const unsigned* bound_h) {
   int tm, tn;
   tile_of_logical(ts.full + int(blockIdx.x), nTm, nTn, kGroupDW, tm, tn);
   const int cl = int(blockIdx.y) * 4 + (threadIdx.x >> 6), rl = (threadIdx.x & 63) * 4;
@@ -1069,6 +1195,7 @@ __global__ __launch_bounds__(256) void k_tail_reduce(const float* __restrict__ s
   const float* src = slots + int64_t(blockIdx.x) * ts.splits * (kBM * kBN) + cl * kBM + rl;
   f32x4 v = *reinterpret_cast<const f32x4*>(src);
   for (int q = 1; q < ts.splits; ++q) v += *reinterpret_cast<const f32x4*>(src + q * (kBM * kBN));
+  v = Unscale(bound_p, bound_h)(v);
   f32x4* o = reinterpret_cast<f32x4*>(C + c * ldc + r);
   if (accumulate) v += *o;
   *o = v;
@@ -1127,21 +1254,27 @@ hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_
 // vocabulary: dH receives this shard's part of G W (the shards' parts sum to
 // dH), dW the shard's rows.  A target outside [0, V) is an ignored token; a
 // target outside the shard contributes only the softmax part here.
-template <typename T>
+// T: the inputs' type; TP: the type of the operand and of the transposes,
+// fp16 (power-of-two scaled, see probs_shift) for bf16 inputs without a
+// cache, T otherwise.
+template <typename T, typename TP>
 hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                     const float* dlogp, int64_t Tn, int64_t d, int64_t Vs, int64_t v_off,
                     int64_t V, float* dH, float* dW, int flags, void* ws, hipStream_t s,
-                    T* cacheE = nullptr, const float* cacheM = nullptr) {
+                    TP* cacheE = nullptr, const float* cacheM = nullptr) {
+  static_assert(sizeof(T) == sizeof(TP), "the operand keeps the input's element size");
+  constexpr bool kScaled = !std::is_same<T, TP>::value;
   // With a softmax cache the whole vocabulary is one chunk and the operand is
   // the cache itself, normalised in place; otherwise the logits of each chunk
   // are recomputed.
   const int64_t chunk = cacheE ? Vs : bwd_chunk_cols(Tn, Vs, sizeof(T));
   const int64_t ld = int64_t(align_up(size_t(min(chunk, Vs)), 64));
   const int64_t pld = cdiv(Tn, 64) * 64;
+  const int64_t nchunks = cdiv(Vs, chunk);
   Carve cv(ws);
-  T* P = cacheE ? cacheE : cv.take<T>(size_t(pld) * ld);
-  T* Wt = cv.take<T>(size_t(d) * ld);    // [d x chunk] transpose of W's chunk rows
-  T* Ht = cv.take<T>(size_t(d) * pld);   // [d x T] transpose of H
+  TP* P = cacheE ? cacheE : cv.take<TP>(size_t(pld) * ld);
+  TP* Wt = cv.take<TP>(size_t(d) * ld);    // [d x chunk] transpose of W's chunk rows
+  TP* Ht = cv.take<TP>(size_t(d) * pld);   // [d x T] transpose of H
   int* counts = cv.take<int>(Vs + 1);   // counts[Vs]: live tokens
   int* cursor = cv.take<int>(Vs);
   int* offsets = cv.take<int>(Vs + 1);
@@ -1151,6 +1284,9 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   float* slots = cv.take<float>(tail_slot_floats(d, min(chunk, Vs)));
   float* seg_slots = cv.take<float>(size_t(2) * cdiv(Tn, kSeg) * d);
   int* seg_live = cv.take<int>(size_t(2) * cdiv(Tn, kSeg));
+  // magnitude bounds of the scaled operands: [0] max |dlogp|, [1] max |H|,
+  // [2 + c] max |W| over chunk c
+  unsigned* bounds = kScaled ? cv.take<unsigned>(size_t(2 + nchunks)) : nullptr;
   int ncu = 0, dev = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -1159,6 +1295,12 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   const int nTd = int(cdiv(d, kBN));
 
   const double es = sizeof(T);
+  if (kScaled) {
+    ProfScope ps_(s, "logprob_bwd_bounds", 0.0, 4.0 * Tn);
+    hipLaunchKernelGGL(k_fill_i32, dim3(cdiv(2 + nchunks, 256)), dim3(256), 0, s,
+                       reinterpret_cast<int*>(bounds), 2 + nchunks, 0);
+    hipLaunchKernelGGL(k_bound_abs, dim3(cdiv(Tn, 256)), dim3(256), 0, s, dlogp, Tn, bounds);
+  }
   if (dW) {
     ProfScope ps_(s, "logprob_bwd_bucket", 0.0, 32.0 * Tn + 16.0 * Vs);
     const int nb = int(cdiv(Vs, 256)), tb = int(cdiv(Tn, 256));
@@ -1175,10 +1317,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   }
   for (int64_t v0 = 0; v0 < Vs; v0 += chunk) {
     const int64_t width = min(chunk, Vs - v0);
+    unsigned* const bound_w = kScaled ? bounds + 2 + v0 / chunk : nullptr;
     const int64_t ldc = int64_t(align_up(size_t(width), 64));   // padded width of this chunk
     const T* Wc = W + v0 * d;
     const size_t wc_bytes = size_t(Vs - v0) * d * sizeof(T);
-    const size_t p_bytes = size_t(pld) * ld * sizeof(T);
+    const size_t p_bytes = size_t(pld) * ld * sizeof(TP);
     if (cacheE) {
       // algorithmic bytes: the writes and per-token values (the reads of
       // the live tokens' cached values depend on dlogp and are not counted)
@@ -1187,7 +1330,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       const int64_t groups = cdiv(panels, kCachePanels), blocks = cdiv(Tn, 32);
       if (groups * blocks > int64_t(0x7fffffff)) return hipErrorInvalidValue;
       // the live-token count comes with the bucketing (run when dW is wanted)
-      hipLaunchKernelGGL(k_cache_to_probs<T>, dim3(unsigned(groups * blocks)), dim3(256), 0, s,
+      hipLaunchKernelGGL(k_cache_to_probs<TP>, dim3(unsigned(groups * blocks)), dim3(256), 0, s,
                          P, cacheM, lse, dlogp, y, Tn, V, pld, panels, uint32_t(groups),
                          dW ? counts + Vs : nullptr);
     } else {
@@ -1196,11 +1339,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       if (!operand_in_bounds<T, Lay::KMajor>(A, wc_bytes) ||
           !operand_in_bounds<T, Lay::KMajor>(B, size_t(Tn) * d * sizeof(T)) || ldc > ld)
         return hipErrorInvalidValue;
-      EpiProbs<T> epi{y, lse, dlogp, Tn, V, width, ldc, pld, P};
+      EpiProbs<T, TP> epi{y, lse, dlogp, Tn, V, width, ldc, pld, P, bounds};
       const int nTv = int(cdiv(ldc, kBM)), nTt = int(cdiv(Tn, kBN));
       ProfScope ps_(s, "logprob_bwd_probs", 2.0 * Tn * d * width,
                     es * (double(Tn) * d + double(width) * d + double(Tn) * width) + 16.0 * Tn);
-      hipLaunchKernelGGL(k_bwd_probs<T>, dim3(nTv * nTt),
+      hipLaunchKernelGGL((k_bwd_probs<T, TP>), dim3(nTv * nTt),
                          dim3(kThreads), 0, s, A, B, d, nTv, nTt, epi);
     }
     if (dH) {
@@ -1208,23 +1351,27 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       // so that both operands run along K
       {
         ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(width) * d);
-        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(d, 256), cdiv(width, 64)), dim3(256), 0, s,
-                           Wc, width, d, d, Wt, ldc);
+        hipLaunchKernelGGL((k_transpose<T, TP>), dim3(cdiv(d, 256), cdiv(width, 64)), dim3(256),
+                           0, s, Wc, width, d, d, Wt, ldc, bound_w, 0);
+        if (kScaled)   // converts again, scaled, only when the bound asks for it
+          hipLaunchKernelGGL((k_transpose<T, TP>),
+                             dim3(cdiv(d, 256), std::min<int64_t>(cdiv(width, 64), kRescaleRows)),
+                             dim3(256), 0, s, Wc, width, d, d, Wt, ldc, bound_w, 1);
       }
       Operand A{P, pld, Tn, ldc}, B{Wt, ldc, d, width};   // ldc = 64 ceil(width / 64)
-      if (!operand_in_bounds<T, Lay::TileTK>(A, p_bytes) ||
-          !operand_in_bounds<T, Lay::KMajor>(B, size_t(d) * ldc * sizeof(T)) ||
+      if (!operand_in_bounds<TP, Lay::TileTK>(A, p_bytes) ||
+          !operand_in_bounds<TP, Lay::KMajor>(B, size_t(d) * ldc * sizeof(TP)) ||
           width > ldc || size_t(d) * ldc > size_t(d) * ld)
         return hipErrorInvalidValue;
       // the one-hot part goes into the last chunk's epilogue
       const bool last = v0 + chunk >= Vs;
       EpiDH<T> epi{dH,      d,     Tn,    d, (v0 > 0 || (flags & MC_BWD_ACCUMULATE_DHIDDEN)) ? 1 : 0,
-                   last ? W : nullptr, y, dlogp, v_off, Vs};
+                   last ? W : nullptr, y, dlogp, v_off, Vs, bounds, bound_w};
       ProfScope ps_(s, "logprob_bwd_dhidden", 2.0 * Tn * d * (width + (last ? 1 : 0)),
                     es * (double(Tn) * width + double(width) * d) +
                         4.0 * Tn * d * (epi.accumulate ? 2 : 1) +
                         (last ? es * double(Tn) * d + 16.0 * Tn : 0.0));
-      hipLaunchKernelGGL(k_bwd_dhidden<T>, dim3(nTm * nTd),
+      hipLaunchKernelGGL((k_bwd_dhidden<TP, T>), dim3(nTm * nTd),
                          dim3(kThreads), 0, s, A, B, ldc, nTm, nTd, epi);
     }
     if (dW) {
@@ -1232,24 +1379,31 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       // [d x pld] (made once) so that the M operand runs along K
       if (v0 == 0) {
         ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(Tn) * d);
-        hipLaunchKernelGGL(k_transpose<T>, dim3(cdiv(d, 256), cdiv(Tn, 64)), dim3(256), 0, s,
-                           H, Tn, d, d, Ht, pld);
+        unsigned* const bound_h = kScaled ? bounds + 1 : nullptr;
+        hipLaunchKernelGGL((k_transpose<T, TP>), dim3(cdiv(d, 256), cdiv(Tn, 64)), dim3(256), 0,
+                           s, H, Tn, d, d, Ht, pld, bound_h, 0);
+        if (kScaled)
+          hipLaunchKernelGGL((k_transpose<T, TP>),
+                             dim3(cdiv(d, 256), std::min<int64_t>(cdiv(Tn, 64), kRescaleRows)),
+                             dim3(256), 0, s, H, Tn, d, d, Ht, pld, bound_h, 1);
       }
       Operand A{Ht, pld, d, Tn}, B{P, pld, ldc, Tn};   // pld = 64 ceil(Tn / 64)
-      if (!operand_in_bounds<T, Lay::KMajor>(A, size_t(d) * pld * sizeof(T)) ||
-          !operand_in_bounds<T, Lay::TileVT>(B, p_bytes))
+      if (!operand_in_bounds<TP, Lay::KMajor>(A, size_t(d) * pld * sizeof(TP)) ||
+          !operand_in_bounds<TP, Lay::TileVT>(B, p_bytes))
         return hipErrorInvalidValue;
-      EpiStoreT epi{dW + v0 * d, d, d, width, (flags & MC_BWD_ACCUMULATE_DWEIGHT) ? 1 : 0};
+      EpiStoreT epi{dW + v0 * d, d, d, width, (flags & MC_BWD_ACCUMULATE_DWEIGHT) ? 1 : 0,
+                    kScaled ? bounds : nullptr, kScaled ? bounds + 1 : nullptr};
       const int nTv = int(cdiv(width, kBM));
       ProfScope ps_(s, "logprob_bwd_dweight", 2.0 * Tn * d * width,
                     es * (double(Tn) * width + double(Tn) * d) +
                         4.0 * width * d * (epi.accumulate ? 2 : 1));
       const TailSplit ts = plan_tail(nTd * nTv, Tn, ncu);
-      hipLaunchKernelGGL(k_bwd_dweight<T>, dim3(ts.full + ts.rem * ts.splits), dim3(kThreads), 0,
-                         s, A, B, Tn, nTd, nTv, epi, ts, slots);
+      hipLaunchKernelGGL(k_bwd_dweight<TP>, dim3(ts.full + ts.rem * ts.splits), dim3(kThreads),
+                         0, s, A, B, Tn, nTd, nTv, epi, ts, slots);
       if (ts.rem > 0)
         hipLaunchKernelGGL(k_tail_reduce, dim3(ts.rem, kBN / 4), dim3(256), 0, s, slots, ts, nTd,
-                           nTv, epi.C, epi.ldc, epi.rows, epi.cols, epi.accumulate);
+                           nTv, epi.C, epi.ldc, epi.rows, epi.cols, epi.accumulate, epi.bound_p,
+                           epi.bound_h);
     }
   }
   if (dW) {
@@ -1322,6 +1476,7 @@ size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
   n += align_up(tail_slot_floats(d, std::min(chunk, V)) * 4, kWsAlign);
   n += onehot_seg_bytes(T, d);
+  if (dt == MC_BF16) n += align_up(size_t(2 + cdiv(V, chunk)) * 4, kWsAlign);   // bounds
   return n;
 }
 
@@ -1349,10 +1504,10 @@ hipError_t launch_bwd(const void* H, const void* W, const int64_t* y, const floa
                       int64_t V, mc_dtype_t dt, float* dH, float* dW, int flags, void* ws,
                       hipStream_t s) {
   if (dt == MC_BF16)
-    return bwd_impl(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W), y, lse, dlogp,
-                    T, d, Vs, v_off, V, dH, dW, flags, ws, s);
-  return bwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, lse, dlogp, T,
-                  d, Vs, v_off, V, dH, dW, flags, ws, s);
+    return bwd_impl<bf16_t, half_t>(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W),
+                                    y, lse, dlogp, T, d, Vs, v_off, V, dH, dW, flags, ws, s);
+  return bwd_impl<float, float>(static_cast<const float*>(H), static_cast<const float*>(W), y, lse,
+                                dlogp, T, d, Vs, v_off, V, dH, dW, flags, ws, s);
 }
 
 // Softmax cache layout: E panels [ldE / BV][pld][BV] in the kernel dtype,
@@ -1390,14 +1545,15 @@ hipError_t launch_bwd_cache(const void* H, const void* W, const int64_t* y, cons
     bf16_t* E;
     float* cm;
     carve_cache(cache, T, V, E, cm);
-    return bwd_impl(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W), y, lse, dlogp,
-                    T, d, V, int64_t(0), V, dH, dW, flags, ws, s, E, cm);
+    return bwd_impl<bf16_t, bf16_t>(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W),
+                                    y, lse, dlogp, T, d, V, int64_t(0), V, dH, dW, flags, ws, s,
+                                    E, cm);
   }
   float* E;
   float* cm;
   carve_cache(cache, T, V, E, cm);
-  return bwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, lse, dlogp, T, d,
-                  V, int64_t(0), V, dH, dW, flags, ws, s, E, cm);
+  return bwd_impl<float, float>(static_cast<const float*>(H), static_cast<const float*>(W), y, lse,
+                                dlogp, T, d, V, int64_t(0), V, dH, dW, flags, ws, s, E, cm);
 }
 
 }  // namespace mc

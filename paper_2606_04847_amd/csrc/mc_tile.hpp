@@ -28,6 +28,8 @@ namespace mc {
 
 typedef __bf16 bf16_t;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half_t;
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -63,6 +65,7 @@ typedef f32x4 Acc[kTM][kTN];
 
 template <typename T> struct Elem;
 template <> struct Elem<bf16_t> { static constexpr int kChunk = 8; };
+template <> struct Elem<half_t> { static constexpr int kChunk = 8; };
 template <> struct Elem<float> { static constexpr int kChunk = 4; };
 
 // Operand of a contraction C[m][n] = sum_k A[m][k] B[n][k].  For A the "rows"
@@ -381,6 +384,30 @@ template <> struct Mfma<bf16_t> {
   }
 };
 
+// fp16 operands (the backward's scaled transient operand and transposes):
+// the same 16 x 16 x 32 shape and rate as bf16, with 11 significant bits.
+template <> struct Mfma<half_t> {
+  __device__ __forceinline__ static void step(Acc& acc, const u32x4 (&a)[kTM],
+                                              const u32x4 (&b)[kTN]) {
+#pragma unroll
+    for (int i = 0; i < kTM; ++i)
+#pragma unroll
+      for (int j = 0; j < kTN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+            __builtin_bit_cast(f16x8, a[i]), __builtin_bit_cast(f16x8, b[j]), acc[i][j], 0, 0, 0);
+  }
+  // the MFMAs r0 .. r1-1 of step()'s order (r = i kTN + j)
+  template <int r0, int r1>
+  __device__ __forceinline__ static void range(Acc& acc, const u32x4 (&a)[kTM],
+                                               const u32x4 (&b)[kTN]) {
+#pragma unroll
+    for (int r = r0; r < r1; ++r)
+      acc[r / kTN][r % kTN] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+          __builtin_bit_cast(f16x8, a[r / kTN]), __builtin_bit_cast(f16x8, b[r % kTN]),
+          acc[r / kTN][r % kTN], 0, 0, 0);
+  }
+};
+
 // fp32: each 16-byte chunk holds 4 K values, consumed by 4 MFMAs of K = 4
 // (element e of lane group g is k = 4 g + e of the step; A and B agree).
 // (The chunks are bit-cast to float vectors as a whole: bit-casting a single
@@ -656,6 +683,7 @@ template <typename T, Lay L, bool kAsm> struct DmaSel<T, L, kAsm, true> {
   typedef DmaCopy<T, L, kAsm> type;
 };
 template <Lay L, bool kAsm> struct DmaSel<bf16_t, L, kAsm, false> { typedef DmaCopyMN<L> type; };
+template <Lay L, bool kAsm> struct DmaSel<half_t, L, kAsm, false> { typedef DmaCopyMN<L> type; };
 
 // All of this wave's direct copies have landed, then a workgroup barrier.
 // The barrier carries no memory fence (the fence of __syncthreads would wait

@@ -5,7 +5,10 @@ both backward pairs (recompute and softmax cache), against the oracle:
     0.1: logits of std ~6.4, so the softmax part of the gradient is a large
     share of it, as in a trained model's head), on sampled rows;
   * skewed (Zipf-like) targets at a mid size, one target bucket holding
-    more than 2048 tokens, every output compared.
+    more than 2048 tokens, every output compared;
+  * magnitudes of H, W and dlogp far outside fp16's range (the recompute
+    pair's fp16 operands are then rescaled by powers of two), every output
+    compared.
 
 The peaked test prints the softmax-part and whole-gradient errors each pair
 reaches (run with -s to see them)."""
@@ -13,9 +16,12 @@ import numpy as np
 import pytest
 
 import oracle
-from _cases import GRAD_RTOL, LOGP_ATOL, PTERM_RTOL, device_tensors, rel_fro
+from _cases import GRAD_RTOL, LOGP_ATOL, PTERM_RTOL, PTERM_RTOL_F16, device_tensors, rel_fro
 from workloads import make_tensors_numpy, make_tensors_torch, sample_targets_torch, scaled_config
-from workloads import zipf_targets
+from workloads import f32_to_bf16_bits, sample_targets_numpy, zipf_targets
+
+# the softmax part's bound per pair: fp16 operand (recompute), bf16 (cache)
+PTERM = {"recompute": PTERM_RTOL_F16, "cached": PTERM_RTOL}
 
 pytestmark = pytest.mark.gpu
 
@@ -99,9 +105,11 @@ def test_peaked_softmax_full_size():
               f"softmax part: dH {s_h:.2e} dW {s_w:.2e}; whole gradient: dH {e_h:.2e} "
               f"dW {e_w:.2e} (bar 1e-3: {'met' if max(e_h, e_w) <= GRAD_RTOL else 'not met'})",
               flush=True)
-        # the softmax part goes through the bf16 operand: 2^-8 relative
-        assert s_h <= PTERM_RTOL and s_w <= PTERM_RTOL, pair
-        assert e_h <= PTERM_RTOL and e_w <= PTERM_RTOL, pair
+        # the softmax part goes through the 2-byte operand
+        assert s_h <= PTERM[pair] and s_w <= PTERM[pair], pair
+        assert e_h <= PTERM[pair] and e_w <= PTERM[pair], pair
+        if pair == "recompute":
+            assert e_h <= GRAD_RTOL and e_w <= GRAD_RTOL
     del res
     torch.cuda.empty_cache()
 
@@ -135,10 +143,55 @@ def test_skewed_targets_both_pairs():
         assert rel_fro(dH_g, dH_o) <= GRAD_RTOL, pair
         assert rel_fro(dW_g, dW_o) <= GRAD_RTOL, pair
         assert np.all(dH_g[dlogp == 0.0] == 0.0), pair
-        assert rel_fro(dH_g - dl64[:, None] * W64[y], soft_h_o) <= PTERM_RTOL, pair
-        assert rel_fro(dW_g - onehot_w, soft_w_o) <= PTERM_RTOL, pair
+        assert rel_fro(dH_g - dl64[:, None] * W64[y], soft_h_o) <= PTERM[pair], pair
+        assert rel_fro(dW_g - onehot_w, soft_w_o) <= PTERM[pair], pair
     # the heaviest bucket's row: its one-hot sum over > 2048 tokens dominates
     top = int(np.argmax(np.bincount(y, minlength=V)))
     for pair, (_, _, _, dW) in res.items():
         row = dW[top].double().cpu().numpy()
         assert rel_fro(row, dW_o[top]) <= GRAD_RTOL, pair
+
+
+@pytest.mark.parametrize("sh,sw,sg", [(17, -17, -40), (-20, 20, 30), (0, 0, -126)])
+def test_extreme_magnitudes_both_pairs(sh, sw, sg):
+    # H 2^sh, W 2^sw, dlogp 2^sg times the usual draws: |H| or |W| beyond
+    # fp16's largest value (65504) or far below its normal range, and dlogp
+    # down to fp32's smallest normals.  H W^T is unchanged (sh + sw = 0), so
+    # the oracle's expected values are the usual ones scaled exactly.
+    T, d, V = 1000, 256, 3000
+    cfg = scaled_config(1, d=d, V=V, dtype="bf16", seed=47)
+    H0, W0, _, _ = make_tensors_numpy(cfg, T)
+    y = sample_targets_numpy(cfg, H0, W0)
+    Hn = (H0 * np.float32(2.0 ** sh)).astype(np.float32)
+    Wn = (W0 * np.float32(2.0 ** sw)).astype(np.float32)
+    rng = np.random.default_rng(48)
+    dlogp = (rng.standard_normal(T) * 2.0 ** sg).astype(np.float32)
+    dlogp[rng.random(T) < 0.1] = 0.0
+    assert np.all(np.isfinite(dlogp)) and np.any(dlogp != 0.0)
+    case = dict(H=Hn, W=Wn, hb=f32_to_bf16_bits(Hn), wb=f32_to_bf16_bits(Wn), y=y)
+    H, W, yd = device_tensors(case)
+    res = _both_pairs(H, W, yd, torch.from_numpy(dlogp).cuda())
+    logp_o, lse_o = oracle.logprob_fwd(Hn, Wn, y)
+    dl64 = dlogp.astype(np.float64)
+    dH_o, dW_o = oracle.logprob_bwd(Hn, Wn, y, lse_o, dl64)
+    H64, W64 = Hn.astype(np.float64), Wn.astype(np.float64)
+    soft_h_o = dH_o - dl64[:, None] * W64[y]
+    onehot_w = np.zeros_like(dW_o)
+    np.add.at(onehot_w, y, dl64[:, None] * H64)
+    for pair, (logp, lse, dH, dW) in res.items():
+        if pair == "cached" and sg < -100:
+            # the cache's bf16 operand -dlogp E is then below bf16's normal
+            # range: only the recompute pair rescales
+            continue
+        assert np.max(np.abs(logp.cpu().numpy() - logp_o)) <= LOGP_ATOL, pair
+        dH_g = dH.cpu().numpy().astype(np.float64)
+        dW_g = dW.cpu().numpy().astype(np.float64)
+        assert np.all(np.isfinite(dH_g)) and np.all(np.isfinite(dW_g)), pair
+        e_h, e_w = rel_fro(dH_g, dH_o), rel_fro(dW_g, dW_o)
+        s_h = rel_fro(dH_g - dl64[:, None] * W64[y], soft_h_o)
+        s_w = rel_fro(dW_g - onehot_w, dW_o - onehot_w)
+        print(f"[extreme 2^{sh} 2^{sw} 2^{sg} {pair}] softmax part: dH {s_h:.2e} dW {s_w:.2e}; "
+              f"whole: dH {e_h:.2e} dW {e_w:.2e}", flush=True)
+        assert e_h <= GRAD_RTOL and e_w <= GRAD_RTOL, pair
+        assert s_h <= PTERM[pair] and s_w <= PTERM[pair], pair
+        assert np.all(dH_g[dlogp == 0.0] == 0.0), pair
