@@ -60,27 +60,29 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "07130914dc5dee98fd696c2613aba6a7a70e46b140ce20a01c125f68f67caf22",
+        "d3211095454560bdaa35b22ba79602e07b19e0a02d9c9e4eeab9cc8e35f3a30d",
     "read_bytes_per_launch": {
-        "logprob_fwd_gemm": 35485402208,
-        "logprob_fwd_merge": 78110880,
-        "logprob_bwd_probs": 32063022592,
-        "logprob_bwd_transpose": 689467328,
-        "logprob_bwd_dhidden": 30006559872,
-        "logprob_bwd_dweight": 30052229568,
-        "logprob_bwd_onehot_dw": 294634496,
-        "logprob_bwd_bucket": 5746432,
+        "logprob_fwd_gemm": 38714633088,
+        "logprob_fwd_merge": 78110528,
+        "logprob_bwd_bounds": 83392,
+        "logprob_bwd_bucket": 5742848,
+        "logprob_bwd_probs": 31953686592,
+        "logprob_bwd_transpose": 689524576,
+        "logprob_bwd_dhidden": 30006579200,
+        "logprob_bwd_dweight": 30051520896,
+        "logprob_bwd_onehot_dw": 107609024,
         "rl_loss": 340480,
     },
     "write_bytes_per_launch": {
-        "logprob_fwd_gemm": 78367648,
+        "logprob_fwd_gemm": 78367680,
         "logprob_fwd_merge": 131072,
-        "logprob_bwd_probs": 4978934592,
+        "logprob_bwd_bounds": 32,
+        "logprob_bwd_bucket": 2513888,
+        "logprob_bwd_probs": 4979199424,
         "logprob_bwd_transpose": 689438720,
         "logprob_bwd_dhidden": 268435456,
-        "logprob_bwd_dweight": 2556428416,
-        "logprob_bwd_onehot_dw": 69889056,
-        "logprob_bwd_bucket": 2513504,
+        "logprob_bwd_dweight": 2556428288,
+        "logprob_bwd_onehot_dw": 69889216,
         "rl_loss": 80896,
     },
 }
@@ -196,6 +198,7 @@ class ClockSampler:
                "socket_power_w_mean": statistics.fmean(pw) if pw else None,
                "source": "amdsmi gpu_metrics current_gfxclks (mean over the 8 XCDs), "
                          "sampled every ~4 ms during the timed region"}
+        d_acc = None
         try:
             d_acc = m1["accumulation_counter"] - self.m0["accumulation_counter"]
             d_ppt = m1["ppt_residency_acc"] - self.m0["ppt_residency_acc"]
@@ -203,6 +206,11 @@ class ClockSampler:
                 out["power_limited_frac"] = d_ppt / d_acc
         except Exception:
             pass
+        # the metrics table did not refresh during the region (seen on some
+        # boxes: every sample identical, the accumulation counter still):
+        # the reading is not a measurement of this region
+        if (d_acc is not None and d_acc <= 0) or (len(clk) > 10 and min(clk) == max(clk)):
+            out["stale"] = True
         return out
 
 
@@ -286,7 +294,7 @@ def summary(res, T, counted, executed):
            "executed_mfma_frac": executed / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
            "clock": res["clock"]}
     clk = res["clock"]
-    if clk and clk.get("gfxclk_mhz_mean"):
+    if clk and clk.get("gfxclk_mhz_mean") and not clk.get("stale"):
         peak_at = FLOP_PER_CLK * clk["gfxclk_mhz_mean"] * 1e6
         out["executed_mfma_frac_at_measured_clock"] = executed / (ms * 1e-3) / peak_at
         out["mfma_frac_at_measured_clock"] = counted / (ms * 1e-3) / peak_at
@@ -374,7 +382,7 @@ def summarize(path, only=None):
         for key in ("k_fwd_logits_lse", "k_bwd_probs", "k_bwd_dhidden", "k_bwd_dweight",
                     "k_cache_to_probs", "k_transpose", "k_onehot_seg", "k_onehot_join", "k_lse_merge",
                     "k_shard_partial", "k_tail_reduce", "k_surrogate", "k_seq_stats",
-                    "k_bucket_rank", "k_bucket_fill", "k_hist", "k_scan", "k_fill_i32",
+                    "k_bucket_rank", "k_bucket_fill", "k_hist", "k_scan", "k_fill_i32", "k_bound_abs",
                     "k_count", "k_finish", "k_loss_init", "copyBuffer"):
             if key in name:
                 return key

@@ -27,7 +27,8 @@ import numpy as np
 import pytest
 
 import oracle
-from _cases import (GRAD_RTOL, LOGP_ATOL, LOSS_RTOL, PTERM_RTOL, fullsize_inputs, rel_fro,
+from _cases import (GRAD_RTOL, LOGP_ATOL, LOSS_RTOL, PTERM_RTOL, PTERM_RTOL_F16,
+                    fullsize_inputs, rel_fro,
                     structure_tensors, to_params)
 from workloads import CONFIGS
 
@@ -273,10 +274,12 @@ def _chain(st):
         assert rel_fro(dH_g, dH_o) <= GRAD_RTOL, pair
         assert np.all(dH_g[~live_rows] == 0.0), pair        # masked / filtered / clipped
         soft_h_g = dH_g - g["dlogp"].astype(np.float64)[rows, None] * Wy
-        assert rel_fro(soft_h_g[live_rows], soft_h_o[live_rows]) <= PTERM_RTOL, pair
+        # operand bound: fp16 (recompute pair), bf16 (softmax cache)
+        pbound = PTERM_RTOL_F16 if pair == "recompute" else PTERM_RTOL
+        assert rel_fro(soft_h_g[live_rows], soft_h_o[live_rows]) <= pbound, pair
         assert rel_fro(dW_g, dW_o) <= GRAD_RTOL, pair
         soft_w_g = dW_g - _onehot_dw(vrows, st.yh, g["dlogp"].astype(np.float64), H64)
-        assert rel_fro(soft_w_g, soft_w_o) <= PTERM_RTOL, pair
+        assert rel_fro(soft_w_g, soft_w_o) <= pbound, pair
         assert col_rel <= GRAD_RTOL, pair
         print(f"[fullsize {st.cid} {pair}] N={o['n_valid']} rows={kinds} "
               f"dH {rel_fro(dH_g, dH_o):.2e} soft {rel_fro(soft_h_g[live_rows], soft_h_o[live_rows]):.2e} "

@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import oracle
-from _cases import (GRAD_RTOL, LOGP_ATOL, LOSS_RTOL, PTERM_RTOL, assert_step_parity,
+from _cases import (GRAD_RTOL, LOGP_ATOL, LOSS_RTOL, PTERM_RTOL_F16, assert_step_parity,
                     device_tensors, fullsize_inputs, gpu_step, oracle_step, rel_fro,
                     sample_rows, small_case, structure_tensors, to_params)
 from workloads import CONFIGS, make_structure, scaled_config
@@ -85,12 +85,13 @@ def test_peaked_softmax_pterm():
     H = case["H"].astype(np.float64)
     onehot_o = o["dlogp"][:, None] * W[y]
     onehot_g = g["dlogp"].astype(np.float64)[:, None] * W[y]
-    assert rel_fro(g["dH"] - onehot_g, o["dH"] - onehot_o) <= PTERM_RTOL
+    # the recompute pair's fp16 operand: 2^-11
+    assert rel_fro(g["dH"] - onehot_g, o["dH"] - onehot_o) <= PTERM_RTOL_F16
     Wo = np.zeros_like(o["dW"])
     Wg = np.zeros_like(o["dW"])
     np.add.at(Wo, y, o["dlogp"][:, None] * H)
     np.add.at(Wg, y, g["dlogp"].astype(np.float64)[:, None] * H)
-    assert rel_fro(g["dW"] - Wg, o["dW"] - Wo) <= PTERM_RTOL
+    assert rel_fro(g["dW"] - Wg, o["dW"] - Wo) <= PTERM_RTOL_F16
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
