@@ -787,6 +787,27 @@ __global__ __launch_bounds__(256) void k_transpose(const TI* __restrict__ in, in
   }
 }
 
+// Hm[t] = H[t] for the tokens whose rows of the softmax operand can be
+// nonzero (dlogp_t != 0 and a target in [0, V)), a zero row otherwise.  The
+// backward's softmax contraction and the H^T operand of dW read Hm instead
+// of H: every result stays the same (the operand is exactly zero on those
+// tokens, so z there only feeds products by zero), while the MFMAs on the
+// zero rows draw less power, and these contractions run power-limited.
+template <typename T>
+__global__ __launch_bounds__(256) void k_live_rows(const T* __restrict__ H,
+                                                   const int64_t* __restrict__ y,
+                                                   const float* __restrict__ dlogp, int64_t Tn,
+                                                   int64_t d, int64_t V, T* __restrict__ Hm) {
+  constexpr int CE = 16 / sizeof(T);   // elements per 16-byte chunk (d is a multiple)
+  const int64_t cpr = d / CE;
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= Tn * cpr) return;
+  const int64_t t = i / cpr, yy = y[t];
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (dlogp[t] != 0.0f && yy >= 0 && yy < V) v = reinterpret_cast<const u32x4*>(H)[i];
+  reinterpret_cast<u32x4*>(Hm)[i] = v;
+}
+
 // --- deterministic bucketing of tokens by target (for the one-hot part of dW)
 __global__ void k_fill_i32(int* __restrict__ p, int64_t n, int v) {
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -1275,6 +1296,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   TP* P = cacheE ? cacheE : cv.take<TP>(size_t(pld) * ld);
   TP* Wt = cv.take<TP>(size_t(d) * ld);    // [d x chunk] transpose of W's chunk rows
   TP* Ht = cv.take<TP>(size_t(d) * pld);   // [d x T] transpose of H
+  T* Hm = cv.take<T>(size_t(Tn) * d);      // H with the dead tokens' rows zeroed
   int* counts = cv.take<int>(Vs + 1);   // counts[Vs]: live tokens
   int* cursor = cv.take<int>(Vs);
   int* offsets = cv.take<int>(Vs + 1);
@@ -1295,6 +1317,13 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   const int nTd = int(cdiv(d, kBN));
 
   const double es = sizeof(T);
+  if (!cacheE || dW) {   // read by the softmax contraction and by H^T
+    ProfScope ps_(s, "logprob_bwd_live_rows", 0.0, 2.0 * es * double(Tn) * d + 12.0 * Tn);
+    const int64_t chunks = Tn * d / (16 / int64_t(sizeof(T)));
+    if (cdiv(chunks, int64_t(256)) > int64_t(0x7fffffff)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_live_rows<T>, dim3(unsigned(cdiv(chunks, int64_t(256)))), dim3(256), 0,
+                       s, H, y, dlogp, Tn, d, V, Hm);
+  }
   if (kScaled) {
     ProfScope ps_(s, "logprob_bwd_bounds", 0.0, 4.0 * Tn);
     hipLaunchKernelGGL(k_fill_i32, dim3(cdiv(2 + nchunks, 256)), dim3(256), 0, s,
@@ -1335,7 +1364,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                          dW ? counts + Vs : nullptr);
     } else {
       // tile rows: chunk columns (up to the padded width ldc), tile columns: tokens
-      Operand A{Wc, d, width, d}, B{H, d, Tn, d};
+      Operand A{Wc, d, width, d}, B{Hm, d, Tn, d};
       if (!operand_in_bounds<T, Lay::KMajor>(A, wc_bytes) ||
           !operand_in_bounds<T, Lay::KMajor>(B, size_t(Tn) * d * sizeof(T)) || ldc > ld)
         return hipErrorInvalidValue;
@@ -1381,11 +1410,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
         ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(Tn) * d);
         unsigned* const bound_h = kScaled ? bounds + 1 : nullptr;
         hipLaunchKernelGGL((k_transpose<T, TP>), dim3(cdiv(d, 256), cdiv(Tn, 64)), dim3(256), 0,
-                           s, H, Tn, d, d, Ht, pld, bound_h, 0);
+                           s, Hm, Tn, d, d, Ht, pld, bound_h, 0);
         if (kScaled)
           hipLaunchKernelGGL((k_transpose<T, TP>),
                              dim3(cdiv(d, 256), std::min<int64_t>(cdiv(Tn, 64), kRescaleRows)),
-                             dim3(256), 0, s, H, Tn, d, d, Ht, pld, bound_h, 1);
+                             dim3(256), 0, s, Hm, Tn, d, d, Ht, pld, bound_h, 1);
       }
       Operand A{Ht, pld, d, Tn}, B{P, pld, ldc, Tn};   // pld = 64 ceil(Tn / 64)
       if (!operand_in_bounds<TP, Lay::KMajor>(A, size_t(d) * pld * sizeof(TP)) ||
@@ -1453,6 +1482,7 @@ size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   const size_t pld = size_t(cdiv(T, 64)) * 64;
   size_t n = align_up(size_t(d) * ld * es, kWsAlign);
   n += align_up(size_t(d) * pld * es, kWsAlign);
+  n += align_up(size_t(T) * size_t(d) * es, kWsAlign);   // H with dead rows zeroed
   n += align_up(size_t(V + 1) * 4, kWsAlign) + align_up(size_t(V) * 4, kWsAlign);
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
@@ -1470,6 +1500,7 @@ size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   size_t n = align_up(pld * ld * es, kWsAlign);
   n += align_up(size_t(d) * ld * es, kWsAlign);
   n += align_up(size_t(d) * pld * es, kWsAlign);
+  n += align_up(size_t(T) * size_t(d) * es, kWsAlign);   // H with dead rows zeroed
   n += align_up(size_t(V + 1) * 4, kWsAlign) + align_up(size_t(V) * 4, kWsAlign);
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
