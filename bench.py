@@ -60,29 +60,31 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "d3211095454560bdaa35b22ba79602e07b19e0a02d9c9e4eeab9cc8e35f3a30d",
+        "df4f20acab829b6d41b31e5dead7423c0b53366b40b69b2e33dece254fed2a08",
     "read_bytes_per_launch": {
-        "logprob_fwd_gemm": 38714633088,
-        "logprob_fwd_merge": 78110528,
+        "logprob_fwd_gemm": 41026162816,
+        "logprob_fwd_merge": 78110784,
+        "logprob_bwd_live_rows": 36083776,
         "logprob_bwd_bounds": 83392,
-        "logprob_bwd_bucket": 5742848,
-        "logprob_bwd_probs": 31953686592,
-        "logprob_bwd_transpose": 689524576,
-        "logprob_bwd_dhidden": 30006579200,
-        "logprob_bwd_dweight": 30051520896,
-        "logprob_bwd_onehot_dw": 107609024,
+        "logprob_bwd_bucket": 5739328,
+        "logprob_bwd_probs": 31962879296,
+        "logprob_bwd_transpose": 689518240,
+        "logprob_bwd_dhidden": 30006582400,
+        "logprob_bwd_dweight": 30050815168,
+        "logprob_bwd_onehot_dw": 107579520,
         "rl_loss": 340480,
     },
     "write_bytes_per_launch": {
-        "logprob_fwd_gemm": 78367680,
+        "logprob_fwd_gemm": 78367648,
         "logprob_fwd_merge": 131072,
+        "logprob_bwd_live_rows": 134217728,
         "logprob_bwd_bounds": 32,
-        "logprob_bwd_bucket": 2513888,
-        "logprob_bwd_probs": 4979199424,
+        "logprob_bwd_bucket": 2513600,
+        "logprob_bwd_probs": 4979874880,
         "logprob_bwd_transpose": 689438720,
         "logprob_bwd_dhidden": 268435456,
         "logprob_bwd_dweight": 2556428288,
-        "logprob_bwd_onehot_dw": 69889216,
+        "logprob_bwd_onehot_dw": 69889056,
         "rl_loss": 80896,
     },
 }
@@ -383,6 +385,7 @@ def summarize(path, only=None):
                     "k_cache_to_probs", "k_transpose", "k_onehot_seg", "k_onehot_join", "k_lse_merge",
                     "k_shard_partial", "k_tail_reduce", "k_surrogate", "k_seq_stats",
                     "k_bucket_rank", "k_bucket_fill", "k_hist", "k_scan", "k_fill_i32", "k_bound_abs",
+                    "k_live_rows",
                     "k_count", "k_finish", "k_loss_init", "copyBuffer"):
             if key in name:
                 return key
