@@ -153,8 +153,7 @@ mc_status_t mc_logprob_bwd_cached(const void* hidden, const void* weight, const 
     return MC_ERR_INVALID_ARG;
   if (T == 0) {
     if (dweight && !(flags & MC_BWD_ACCUMULATE_DWEIGHT))
-      return from_hip(hipMemsetAsync(dweight, 0, size_t(V) * size_t(d) * sizeof(float),
-                                     static_cast<hipStream_t>(stream)));
+      return from_hip(mc::launch_zero(dweight, V * d, static_cast<hipStream_t>(stream)));
     return MC_OK;
   }
   if (!targets || !lse || !dlogp) return MC_ERR_INVALID_ARG;
@@ -210,8 +209,7 @@ static mc_status_t bwd_common(const void* hidden, const void* weight, const int6
   if (T == 0) {
     // no tokens: dhidden is empty; dweight receives a zero gradient
     if (dweight && !(flags & MC_BWD_ACCUMULATE_DWEIGHT))
-      return from_hip(hipMemsetAsync(dweight, 0, size_t(V) * size_t(d) * sizeof(float),
-                                     static_cast<hipStream_t>(stream)));
+      return from_hip(mc::launch_zero(dweight, V * d, static_cast<hipStream_t>(stream)));
     return MC_OK;
   }
   if (!targets || !lse || !dlogp) return MC_ERR_INVALID_ARG;

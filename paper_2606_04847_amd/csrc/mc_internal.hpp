@@ -72,6 +72,9 @@ hipError_t launch_bwd(const void* H, const void* W, const int64_t* y, const floa
 hipError_t launch_fwd_cache(const void* H, const void* W, const int64_t* y, int64_t T, int64_t d,
                             int64_t V, mc_dtype_t dt, float* logp, float* lse, float* entropy,
                             void* cache, void* ws, hipStream_t s);
+// p[0 .. n) = 0 with a kernel (not a memset, so that a captured graph holds
+// only kernel nodes).
+hipError_t launch_zero(float* p, int64_t n, hipStream_t s);
 hipError_t launch_bwd_cache(const void* H, const void* W, const int64_t* y, const float* lse,
                             const float* dlogp, int64_t T, int64_t d, int64_t V, mc_dtype_t dt,
                             void* cache, float* dH, float* dW, int flags, void* ws,

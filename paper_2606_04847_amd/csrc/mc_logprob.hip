@@ -808,6 +808,13 @@ __global__ __launch_bounds__(256) void k_live_rows(const T* __restrict__ H,
   reinterpret_cast<u32x4*>(Hm)[i] = v;
 }
 
+// Zeros, grid-stride (the grid is capped; n may exceed 2^31 elements).
+__global__ __launch_bounds__(256) void k_zero_f32(float* __restrict__ p, int64_t n) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride)
+    p[i] = 0.0f;
+}
+
 // --- deterministic bucketing of tokens by target (for the one-hot part of dW)
 __global__ void k_fill_i32(int* __restrict__ p, int64_t n, int v) {
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -1520,6 +1527,13 @@ hipError_t launch_fwd(const void* H, const void* W, const int64_t* y, int64_t T,
                     v_off, V, logp, lse, entropy, part, with_u, ws, s);
   return fwd_impl(static_cast<const float*>(H), static_cast<const float*>(W), y, T, d, Vs, v_off,
                   V, logp, lse, entropy, part, with_u, ws, s);
+}
+
+hipError_t launch_zero(float* p, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>(cdiv(n, int64_t(256)), int64_t(1) << 16);
+  hipLaunchKernelGGL(k_zero_f32, dim3(unsigned(blocks)), dim3(256), 0, s, p, n);
+  return hipGetLastError();
 }
 
 hipError_t launch_merge(const float* parts, int S, const int64_t* y, int64_t T, int64_t V,
