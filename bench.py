@@ -60,7 +60,7 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "df4f20acab829b6d41b31e5dead7423c0b53366b40b69b2e33dece254fed2a08",
+        "7a902b35a020f3a754a13c4cdf6c97eae23b1ab2811903c3d12719443d3537b1",
     "read_bytes_per_launch": {
         "logprob_fwd_gemm": 41026162816,
         "logprob_fwd_merge": 78110784,
