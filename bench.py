@@ -60,18 +60,18 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "7a902b35a020f3a754a13c4cdf6c97eae23b1ab2811903c3d12719443d3537b1",
+        "6c0f46cf7de4f1d82b3175d8c4e2a7059562cbeaadab95f0c012cdd07f7c1a3f",
     "read_bytes_per_launch": {
-        "logprob_fwd_gemm": 41026162816,
-        "logprob_fwd_merge": 78110784,
+        "logprob_fwd_gemm": 37054925248,
+        "logprob_fwd_merge": 78110848,
         "logprob_bwd_live_rows": 36083776,
         "logprob_bwd_bounds": 83392,
-        "logprob_bwd_bucket": 5739328,
-        "logprob_bwd_probs": 31962879296,
-        "logprob_bwd_transpose": 689518240,
-        "logprob_bwd_dhidden": 30006582400,
-        "logprob_bwd_dweight": 30050815168,
-        "logprob_bwd_onehot_dw": 107579520,
+        "logprob_bwd_bucket": 5744896,
+        "logprob_bwd_probs": 31756688384,
+        "logprob_bwd_transpose": 689530432,
+        "logprob_bwd_dhidden": 30006584448,
+        "logprob_bwd_dweight": 30050872576,
+        "logprob_bwd_onehot_dw": 107646528,
         "rl_loss": 340480,
     },
     "write_bytes_per_launch": {
@@ -79,12 +79,12 @@ TRAFFIC = {
         "logprob_fwd_merge": 131072,
         "logprob_bwd_live_rows": 134217728,
         "logprob_bwd_bounds": 32,
-        "logprob_bwd_bucket": 2513600,
-        "logprob_bwd_probs": 4979874880,
+        "logprob_bwd_bucket": 2513824,
+        "logprob_bwd_probs": 4979734464,
         "logprob_bwd_transpose": 689438720,
         "logprob_bwd_dhidden": 268435456,
         "logprob_bwd_dweight": 2556428288,
-        "logprob_bwd_onehot_dw": 69889056,
+        "logprob_bwd_onehot_dw": 69889120,
         "rl_loss": 80896,
     },
 }
