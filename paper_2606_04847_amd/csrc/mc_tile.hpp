@@ -66,6 +66,9 @@ constexpr int kGroupM = 8;                     // tile rows per scheduling group
 // per recompute step than 0 (forward -0.13 ms, softmax contraction -0.15,
 // dH -0.2), while 1 and 2 were slower than 0.
 constexpr int kDeepLate = 4;
+// The same for the loop with inline-asm copies (dW; all of a stage's deep
+// copies or none): measured 0.1-0.3 ms faster for dW.
+constexpr bool kDeepLateAsm = true;
 constexpr int kXcds = 8;                       // MI355X: 8 XCDs, workgroup i -> XCD i % 8
 
 typedef f32x4 Acc[kTM][kTN];
@@ -818,21 +821,23 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
   // after the barrier of step k - 1, so that fewer copies leave at once
   // (the slot was freed at that barrier; the wait before the barrier of
   // step k + 1 still leaves exactly the deep stage k + 3's copies in flight)
-  constexpr int kLate = kAsm ? 0 : kDeepLate;
+  // (inline-asm path: all of a stage's deep copies or none)
+  constexpr int kLate = kAsm ? (kDeepLateAsm ? kNID : 0) : kDeepLate;
   static_assert(kLate >= 0 && kLate <= kNID, "late copies");
+  constexpr int kCopyGap = 2;   // inline-asm path: MFMAs after each copy
   if constexpr (kDeepA) {
     cb.issue(1, ldsB + kStageBytes);
     ca.issue(1, ldsA + kStageBytes);
     if constexpr (kLate == 0)
       ca.issue(2, ldsA + 2 * kStageBytes);
-    else
+    else if constexpr (kLate < kNID)
       ca.template issue_part<0, kNID - kLate>(2, ldsA + 2 * kStageBytes);
   } else {
     ca.issue(1, ldsA + kStageBytes);
     cb.issue(1, ldsB + kStageBytes);
     if constexpr (kLate == 0)
       cb.issue(2, ldsB + 2 * kStageBytes);
-    else
+    else if constexpr (kLate < kNID)
       cb.template issue_part<0, kNID - kLate>(2, ldsB + 2 * kStageBytes);
   }
   __builtin_amdgcn_s_waitcnt(0x3f70 | (kNIS + 2 * kNID - kLate));
@@ -846,31 +851,54 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     char* const curA = ldsA + sa * kStageBytes;
     char* const curB = ldsB + sb * kStageBytes;
     const int na = sa + 1 == kNA ? 0 : sa + 1, nb = sb + 1 == kNB ? 0 : sb + 1;
-    read_frags<T, SA, SB>(a1, b1, curA, curB, wm, wn, lane, 1);
-    if constexpr (kLate > 0) {
-      // the late copies of deep step kt+2, into the slot step kt-1 freed
-      if constexpr (kDeepA)
-        ca.template issue_part<kNID - kLate, kNID>(
-            kt + 2, ldsA + (sa + 2 < kNA ? sa + 2 : sa + 2 - kNA) * kStageBytes);
-      else
-        cb.template issue_part<kNID - kLate, kNID>(
-            kt + 2, ldsB + (sb + 2 < kNB ? sb + 2 : sb + 2 - kNB) * kStageBytes);
-    }
-    Mfma<T>::step(acc, a0, b0);
-    // issue order: one MFMA, one fragment read, ... so that the reads go out
-    // while the MFMA pipe is busy
+    // the slot of deep step kt+2 (freed at the barrier of step kt-1)
+    char* const deep2 = kDeepA ? ldsA + (sa + 2 < kNA ? sa + 2 : sa + 2 - kNA) * kStageBytes
+                               : ldsB + (sb + 2 < kNB ? sb + 2 : sb + 2 - kNB) * kStageBytes;
+    if constexpr (kAsm && kLate > 0) {
+      // one late copy, then kCopyGap MFMAs, each pair fenced; then the
+      // fragment reads of the second half interleaved with the rest
+      static_assert(kCopyGap * kLate + kRd <= kTM * kTN, "issue slots");
+      const auto& cd = pick<kDeepA>(ca, cb);
+      const auto hd = cd.prep(kt + 2, deep2);
+      static_for<0, kLate>([&](auto c) {
+        constexpr int r = decltype(c)::value;
+        cd.one(hd, r);
+        Mfma<T>::template range<kCopyGap * r, kCopyGap * (r + 1)>(acc, a0, b0);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      read_frags<T, SA, SB>(a1, b1, curA, curB, wm, wn, lane, 1);
+      Mfma<T>::template range<kCopyGap * kLate, kTM * kTN>(acc, a0, b0);
 #pragma unroll
-    for (int r = 0; r < kRd; ++r) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
-    }
+      for (int r = 0; r < kRd; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, kTM * kTN - kCopyGap * kLate - kRd, 0);
+    } else {
+      read_frags<T, SA, SB>(a1, b1, curA, curB, wm, wn, lane, 1);
+      if constexpr (kLate > 0) {
+        // the late copies of deep step kt+2
+        if constexpr (kDeepA)
+          ca.template issue_part<kNID - kLate, kNID>(kt + 2, deep2);
+        else
+          cb.template issue_part<kNID - kLate, kNID>(kt + 2, deep2);
+      }
+      Mfma<T>::step(acc, a0, b0);
+      // issue order: one MFMA, one fragment read, ... so that the reads go out
+      // while the MFMA pipe is busy
 #pragma unroll
-    for (int r = 0; r < kLate; ++r) {
-      __builtin_amdgcn_sched_group_barrier(0x008, kSpread, 0);   // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);         // copy issue
+      for (int r = 0; r < kRd; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+      }
+#pragma unroll
+      for (int r = 0; r < kLate; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, kSpread, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);         // copy issue
+      }
+      static_assert(kRd + kSpread * kLate <= kTM * kTN, "issue slots");
+      __builtin_amdgcn_sched_group_barrier(0x008, kTM * kTN - kRd - kSpread * kLate, 0);
     }
-    static_assert(kRd + kSpread * kLate <= kTM * kTN, "issue slots");
-    __builtin_amdgcn_sched_group_barrier(0x008, kTM * kTN - kRd - kSpread * kLate, 0);
     // this wave: step kt+1 landed (only the deep operand's step kt+2 may be
     // in flight), reads of step kt returned; nothing is scheduled across the
     // barrier
@@ -885,14 +913,15 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
     // fragments of step kt+1 (past the end: unused)
     if constexpr (kAsm) {
       // the scheduler does not see inline-asm copies: one copy, then kCopyGap
-      // MFMAs, in program order, each pair fenced
-      constexpr int kCopyGap = 2;
-      static_assert(kCopyGap * (CA::NI + CB::NI) + kRd <= kTM * kTN, "issue slots");
+      // MFMAs, in program order, each pair fenced (the deep copies only when
+      // they do not go out late)
+      constexpr int kNow = kNIS + kNID - kLate;
+      static_assert(kCopyGap * kNow + kRd <= kTM * kTN, "issue slots");
       const auto& cs = pick<kDeepA>(cb, ca);   // shallow
       const auto& cd = pick<kDeepA>(ca, cb);   // deep
       const auto hs = cs.prep(kt + 2, kDeepA ? curB : curA);
       const auto hd = cd.prep(kt + 3, kDeepA ? curA : curB);
-      static_for<0, CA::NI + CB::NI>([&](auto c) {
+      static_for<0, kNow>([&](auto c) {
         constexpr int r = decltype(c)::value;
         if constexpr (r < kNIS)
           cs.one(hs, r);
@@ -903,7 +932,7 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
       });
       read_frags<T, SA, SB>(a0, b0, ldsA + na * kStageBytes, ldsB + nb * kStageBytes, wm, wn,
                             lane, 0);
-      Mfma<T>::template range<kCopyGap * (CA::NI + CB::NI), kTM * kTN>(acc, a1, b1);
+      Mfma<T>::template range<kCopyGap * kNow, kTM * kTN>(acc, a1, b1);
 #pragma unroll
       for (int r = 0; r < kRd; ++r) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
@@ -913,15 +942,16 @@ __device__ __forceinline__ void gemm_mainloop_dma(const Operand& A, const Operan
       sb = nb;
       continue;
     }
+    // (the inline-asm path has continued above)
     if constexpr (kDeepA) {
       cb.issue(kt + 2, curB);
-      if constexpr (kLate == 0)
+      if constexpr (kLate == 0 || kAsm)
         ca.issue(kt + 3, curA);
       else
         ca.template issue_part<0, kNID - kLate>(kt + 3, curA);
     } else {
       ca.issue(kt + 2, curA);
-      if constexpr (kLate == 0)
+      if constexpr (kLate == 0 || kAsm)
         cb.issue(kt + 3, curB);
       else
         cb.template issue_part<0, kNID - kLate>(kt + 3, curB);
