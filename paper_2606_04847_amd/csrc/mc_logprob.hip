@@ -1159,12 +1159,16 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B,
                                                                         lds, kGroupVT);
 }
 // TG: the contraction's operand type (the operand panels and W^T), T: the
-// weight's, read by the one-hot part
+// weight's, read by the one-hot part.  Groups of 4 token tile rows walk the
+// hidden dimensions (measured against 8 and 16 with the current copy
+// schedule: 0.18 ms faster than 8).
+constexpr int kGroupDH = 4;
 template <typename TG, typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand B, int64_t K,
                                                              int nTm, int nTn, EpiDH<T> epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
-  gemm_body<TG, Lay::TileTK, Lay::KMajor, EpiDH<T>, 2, kDeepDhA>(A, B, K, nTm, nTn, epi, lds);
+  gemm_body<TG, Lay::TileTK, Lay::KMajor, EpiDH<T>, 2, kDeepDhA>(A, B, K, nTm, nTn, epi, lds,
+                                                                 kGroupDH);
 }
 // dW^T = H^T P~ : tile rows are hidden dimensions (A = H^T, along the
 // tokens), tile columns vocabulary entries (B = the operand panels read
