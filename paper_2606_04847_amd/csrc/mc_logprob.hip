@@ -509,18 +509,25 @@ struct EpiProbs {
     for (int j = 0; j < kTN; ++j) {
       const int tl = wn * kWaveCols + j * 16 + (lane & 15);
       const int64_t t = n0 + tl;
-      if (t >= Tn) continue;
       const float lb = pre.l2[j], gs = pre.g[j];
+      // Whether any of the column block's 16 tokens has a nonzero factor
+      // (wave-uniform).  A block of tokens with zero dlogp (outside the loss
+      // mask, filtered, clipped, ignored) has an all-zero operand: its zeros
+      // are written without evaluating the exponentials.
+      const bool live = __builtin_amdgcn_ballot_w64(t < Tn && gs != 0.0f) != 0;
+      if (t >= Tn) continue;
 #pragma unroll
       for (int i = 0; i < kTM; ++i) {
         {
           const int r = wrow(i, 0, lane);   // first of the 4 consecutive rows of block i
           if (!kFull && r >= llim) continue;
-          f32x4 p;
+          f32x4 p = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+          if (live) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            p[e] = gs * __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -lb));
-            if (!kFull && r + e >= vlim) p[e] = 0.0f;
+            for (int e = 0; e < 4; ++e) {
+              p[e] = gs * __builtin_amdgcn_exp2f(fmaf(acc[i][j][e], kLog2e, -lb));
+              if (!kFull && r + e >= vlim) p[e] = 0.0f;
+            }
           }
           const int vr = wm * kWaveRows + r;   // row of the tile
           if constexpr (sizeof(TP) == 2) {
