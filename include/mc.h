@@ -218,13 +218,16 @@ mc_status_t mc_logprob_bwd_shard(const void* hidden, const void* weight_shard,
  * mc_logprob_fwd / mc_logprob_bwd (the numerator of Eq. 4 and its
  * gradient), with the backward reading what the forward kept instead of
  * recomputing the logits.  The forward stores, in `cache`,
- *   E[t, v] = exp(z[t, v] - c_b[t])   (dtype, vocabulary panels)
+ *   E[t, v] = exp(z[t, v] - c_b[t])   (vocabulary panels; fp16 for MC_BF16
+ *                                      inputs: E lies in (0, 1] and the
+ *                                      block maximum is exactly 1; fp32
+ *                                      for MC_F32)
  *   c_b[t]  = max of z[t, .] over block b of 128 vocabulary entries (fp32)
- * and the backward turns E, in place, into the softmax part of G and runs
- * the two contractions on it.  The operand stays in the dtype, and E adds
- * one rounding to it before the final one (bf16: each element of that
- * operand is within about 2^-7 relative of its exact value, against 2^-11
- * for the recompute pair's fp16 operand).
+ * and the backward turns E, in place, into the softmax part of G (for
+ * MC_BF16 the recompute pair's fp16 operand, scaled by the same power of
+ * two) and runs the two contractions on it.  E adds one rounding before
+ * the operand's own: each element of the operand is within about 2^-10
+ * relative of its exact value, against 2^-11 for the recompute pair.
  *   cache     device, 256-byte aligned, at least mc_logprob_cache_size bytes;
  *             owned by the caller; written by mc_logprob_fwd_cached and
  *             consumed (overwritten) by one mc_logprob_bwd_cached call with

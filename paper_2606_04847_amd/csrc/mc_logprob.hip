@@ -123,11 +123,13 @@ __device__ __forceinline__ void store_staged_panels(const char* lds, TP* P, int6
 // v_off + r.
 // With a softmax cache (E non-null) the epilogue also keeps what the
 // backward needs instead of recomputing the logits: E[t, v] =
-// exp(z_tv - cm[b][t]) in the kernel dtype, in the panel layout of the
+// exp(z_tv - cm[b][t]) in TE (fp16 for bf16 inputs: the values lie in
+// (0, 1], the block maximum is exactly 1, and fp16 keeps 11 significant bits
+// against bf16's 8; fp32 for fp32 inputs), in the panel layout of the
 // backward operand, where cm[b][t] is the max over the wave's block b of 128
 // vocabulary rows (zero for rows >= Vs).
 // ---------------------------------------------------------------------------
-template <typename T>
+template <typename T, typename TE = T>   // TE: the softmax cache's element type
 struct EpiFwd {
   const int64_t* y;
   int64_t Tn, Vs, v_off;  // tokens, shard width, shard offset
@@ -135,11 +137,11 @@ struct EpiFwd {
   float* part_s;          // [nTv][Tn]
   float* part_u;          // [nTv][Tn] or null (no entropy)
   float* zy;              // [Tn]: receives z[t, y_t] for targets inside the shard
-  T* E;                   // softmax cache: panels [ldE / BV][pld][BV], or null
+  TE* E;                  // softmax cache: panels [ldE / BV][pld][BV], or null
   float* cm;              // [2 nTv][Tn] block maxima (with E)
   int64_t pld, ldE;       // padded token count, padded vocabulary width
   static constexpr int kLdsExtra = 3 * kWavesM * 256 * 4;
-  static constexpr int64_t kPanel = 128 / sizeof(T);
+  static constexpr int64_t kPanel = 128 / sizeof(TE);
 
   // this lane's targets (shard-local, -1 outside the shard) of its kTN
   // token columns
@@ -163,7 +165,7 @@ struct EpiFwd {
 
   // max / sum exp / sum exp z of block column j over this lane's rows; kFull:
   // all rows of the wave are valid (no per-element mask); kStore: also the
-  // softmax cache values of these rows (staged in LDS for bf16)
+  // softmax cache values of these rows (staged in LDS for a 2-byte cache)
   template <bool kFull, bool kStore>
   __device__ __forceinline__ void column(const Acc& acc, int j, int vlim, int lane, bool with_u,
                                          float& mx, float& s, float& u, char* lds, int wm,
@@ -193,10 +195,10 @@ struct EpiFwd {
       }
       if constexpr (kStore) {
         const int vr = wm * kWaveRows + wrow(i, 0, lane);   // tile row of element 0
-        if constexpr (sizeof(T) == 2) {
-          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+        if constexpr (sizeof(TE) == 2) {
+          typedef TE te4 __attribute__((ext_vector_type(4)));
           *reinterpret_cast<u32x2*>(lds + panel_stage_off(vr, tl)) =
-              __builtin_bit_cast(u32x2, __builtin_convertvector(xs, bf16x4));
+              __builtin_bit_cast(u32x2, __builtin_convertvector(xs, te4));
         } else {
           const int64_t c = m0 + vr;
           if (t < Tn && c < ldE)
@@ -253,7 +255,7 @@ struct EpiFwd {
       }
     }
     __syncthreads();
-    if constexpr (sizeof(T) == 2)
+    if constexpr (sizeof(TE) == 2)
       if (E != nullptr) store_staged_panels(lds, E, m0, n0, Tn, ldE, pld);
     for (int tl = tid; tl < kBN; tl += kThreads) {
       const int64_t t = n0 + tl;
@@ -1097,7 +1099,8 @@ __global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
                                                         const int64_t* __restrict__ y,
                                                         int64_t Tn, int64_t V, int64_t pld,
                                                         int64_t npanels, uint32_t ngroups,
-                                                        const int* __restrict__ live) {
+                                                        const int* __restrict__ live,
+                                                        const unsigned* __restrict__ bound) {
   constexpr int BV = 128 / sizeof(T);   // panel width
   constexpr int CE = 16 / sizeof(T);    // entries per chunk
   const uint32_t nblocks = uint32_t((Tn + 31) / 32);
@@ -1108,7 +1111,8 @@ __global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
   if (t >= Tn) return;
   const int ch = threadIdx.x & 7;
   const int64_t yy = y[t];
-  const float g = (yy >= 0 && yy < V) ? -dlogp[t] : 0.0f;
+  const int sh = bound != nullptr ? probs_shift(*bound) : 0;
+  const float g = (yy >= 0 && yy < V) ? ldexpf(-dlogp[t], sh) : 0.0f;
   const float l = lse[t];
   const int64_t p0 = int64_t(gi) * kCachePanels;
   u32x4 raw[kCachePanels];
@@ -1148,13 +1152,14 @@ constexpr int kGroupVT = 4;
 constexpr bool kDeepFwdA = true;    // forward / softmax: W (A) over H (B)
 constexpr bool kDeepDhA = true;     // dH: the operand panels (A) over W^T (B)
 constexpr bool kDeepDwA = false;    // dW^T: the operand panels (B) over H^T (A)
-template <typename T>
+template <typename T, typename TE = T>
 __global__ __launch_bounds__(kThreads, 1) void k_fwd_logits_lse(Operand A, Operand B, int64_t K,
-                                                                int nTm, int nTn, EpiFwd<T> epi) {
-  static_assert(kLdsGemm + EpiFwd<T>::kLdsExtra <= kLdsRing, "epilogue LDS");
+                                                                int nTm, int nTn,
+                                                                EpiFwd<T, TE> epi) {
+  static_assert(kLdsGemm + EpiFwd<T, TE>::kLdsExtra <= kLdsRing, "epilogue LDS");
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
-  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiFwd<T>, 2, kDeepFwdA>(A, B, K, nTm, nTn, epi, lds,
-                                                                  kGroupVT);
+  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiFwd<T, TE>, 2, kDeepFwdA>(A, B, K, nTm, nTn, epi,
+                                                                      lds, kGroupVT);
 }
 // T: the inputs' type, TP: the operand's (see EpiProbs)
 template <typename T, typename TP>
@@ -1250,10 +1255,11 @@ size_t tail_slot_floats(int64_t d, int64_t width) {
 // Forward over a vocabulary shard [v_off, v_off + Vs) of a V-entry vocabulary
 // (the whole vocabulary when v_off = 0, Vs = V).  part == null: final lse,
 // logp (and entropy when given); otherwise the shard's partial [4][T].
-template <typename T>
+// cacheE: the softmax cache (element type TE), or null.
+template <typename T, typename TE = T>
 hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_t d, int64_t Vs,
                     int64_t v_off, int64_t V, float* logp, float* lse, float* entropy,
-                    float* part, bool with_u, void* ws, hipStream_t s, T* cacheE = nullptr,
+                    float* part, bool with_u, void* ws, hipStream_t s, TE* cacheE = nullptr,
                     float* cacheM = nullptr) {
   // tile rows: vocabulary (the weight's rows), tile columns: tokens
   const int nTv = int(cdiv(Vs, kBM)), nTt = int(cdiv(Tn, kBN));
@@ -1268,13 +1274,13 @@ hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_
       !operand_in_bounds<T, Lay::KMajor>(B, size_t(Tn) * d * sizeof(T)))
     return hipErrorInvalidValue;
   const int64_t pld = cdiv(Tn, 64) * 64, ldE = int64_t(align_up(size_t(Vs), 64));
-  EpiFwd<T> epi{y,  Tn,     Vs,     v_off,  pm,  ps, pu, part ? part + 3 * Tn : logp,
-                cacheE, cacheM, pld, ldE};
+  EpiFwd<T, TE> epi{y,  Tn,     Vs,     v_off,  pm,  ps, pu, part ? part + 3 * Tn : logp,
+                    cacheE, cacheM, pld, ldE};
   {
     ProfScope ps_(s, "logprob_fwd_gemm", 2.0 * Tn * d * Vs,
                   es * (double(Tn) * d + double(Vs) * d) + 12.0 * Tn +
                       (cacheE ? es * double(Tn) * Vs + 8.0 * nTv * Tn : 0.0));
-    hipLaunchKernelGGL(k_fwd_logits_lse<T>, dim3(nTv * nTt), dim3(kThreads), 0,
+    hipLaunchKernelGGL((k_fwd_logits_lse<T, TE>), dim3(nTv * nTt), dim3(kThreads), 0,
                        s, A, B, d, nTv, nTt, epi);
   }
   {
@@ -1294,8 +1300,8 @@ hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_
 // dH), dW the shard's rows.  A target outside [0, V) is an ignored token; a
 // target outside the shard contributes only the softmax part here.
 // T: the inputs' type; TP: the type of the operand and of the transposes,
-// fp16 (power-of-two scaled, see probs_shift) for bf16 inputs without a
-// cache, T otherwise.
+// fp16 (power-of-two scaled, see probs_shift) for bf16 inputs, with or
+// without a cache (the cache is then fp16 too), T otherwise.
 template <typename T, typename TP>
 hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                     const float* dlogp, int64_t Tn, int64_t d, int64_t Vs, int64_t v_off,
@@ -1379,7 +1385,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       // the live-token count comes with the bucketing (run when dW is wanted)
       hipLaunchKernelGGL(k_cache_to_probs<TP>, dim3(unsigned(groups * blocks)), dim3(256), 0, s,
                          P, cacheM, lse, dlogp, y, Tn, V, pld, panels, uint32_t(groups),
-                         dW ? counts + Vs : nullptr);
+                         dW ? counts + Vs : nullptr, bounds);
     } else {
       // tile rows: chunk columns (up to the padded width ldc), tile columns: tokens
       Operand A{Wc, d, width, d}, B{Hm, d, Tn, d};
@@ -1507,6 +1513,7 @@ size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
   n += align_up(tail_slot_floats(d, V) * 4, kWsAlign);
   n += onehot_seg_bytes(T, d);
+  if (dt == MC_BF16) n += align_up(size_t(3) * 4, kWsAlign);   // bounds (one chunk)
   return n;
 }
 
@@ -1566,8 +1573,8 @@ hipError_t launch_bwd(const void* H, const void* W, const int64_t* y, const floa
                                 dlogp, T, d, Vs, v_off, V, dH, dW, flags, ws, s);
 }
 
-// Softmax cache layout: E panels [ldE / BV][pld][BV] in the kernel dtype,
-// then the block maxima [2 nTv][T] fp32.
+// Softmax cache layout: E panels [ldE / BV][pld][BV] (fp16 for bf16 inputs,
+// fp32 for fp32), then the block maxima [2 nTv][T] fp32.
 template <typename T>
 static void carve_cache(void* cache, int64_t T_, int64_t V, T*& E, float*& cm) {
   Carve cv(cache);
@@ -1579,8 +1586,8 @@ static void carve_cache(void* cache, int64_t T_, int64_t V, T*& E, float*& cm) {
 hipError_t launch_fwd_cache(const void* H, const void* W, const int64_t* y, int64_t T, int64_t d,
                             int64_t V, mc_dtype_t dt, float* logp, float* lse, float* entropy,
                             void* cache, void* ws, hipStream_t s) {
-  if (dt == MC_BF16) {
-    bf16_t* E;
+  if (dt == MC_BF16) {   // fp16 cache (see launch_bwd_cache)
+    half_t* E;
     float* cm;
     carve_cache(cache, T, V, E, cm);
     return fwd_impl(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W), y, T, d, V,
@@ -1598,10 +1605,13 @@ hipError_t launch_bwd_cache(const void* H, const void* W, const int64_t* y, cons
                             void* cache, float* dH, float* dW, int flags, void* ws,
                             hipStream_t s) {
   if (dt == MC_BF16) {
-    bf16_t* E;
+    // The cache holds exp(z - c_b) in (0, 1] as fp16 (11 significant bits);
+    // the backward rescales it in place into the power-of-two scaled fp16
+    // operand of the recompute pair and runs the same fp16 contractions.
+    half_t* E;
     float* cm;
     carve_cache(cache, T, V, E, cm);
-    return bwd_impl<bf16_t, bf16_t>(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W),
+    return bwd_impl<bf16_t, half_t>(static_cast<const bf16_t*>(H), static_cast<const bf16_t*>(W),
                                     y, lse, dlogp, T, d, V, int64_t(0), V, dH, dW, flags, ws, s,
                                     E, cm);
   }

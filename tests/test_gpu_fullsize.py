@@ -14,12 +14,14 @@ pairs: recompute (mc_logprob_fwd / mc_logprob_bwd) and softmax cache
     (the heaviest target buckets, untargeted rows, tile and chunk
     boundaries) from the real dlogp over all T tokens;
   * the softmax part of each gradient alone (its one-hot part subtracted on
-    both sides), held to the bf16 rounding bound of the transient operand.
+    both sides), held to the fp16 rounding bound of the transient operand
+    (one rounding in the recompute pair, two with the softmax cache).
 
 Compared: logp and lse on every row (<= 2e-3); seq_mask, seq_len and N bit
 for bit; the loss (relative 1e-3); dlogp (relative Frobenius 1e-4, same zero
 pattern); sampled dH and dW rows (relative Frobenius 1e-3); softmax parts
-(relative Frobenius 2^-8); and, at any size, sum_v dW[v, :] = 0.
+(relative Frobenius 2^-11, 2^-10 with the cache); and, at any size,
+sum_v dW[v, :] = 0.
 """
 import gc
 
