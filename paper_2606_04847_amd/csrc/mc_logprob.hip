@@ -909,6 +909,12 @@ __global__ __launch_bounds__(256) void k_scan_apply(const int* __restrict__ coun
   if (i0 < V && i0 + 4 >= V) offsets[V] = run;   // the thread holding entry V - 1
 }
 
+// Buckets larger than kRankDirect are ordered through a bitmap (see
+// k_bucket_rank); the (unordered) list is filled for the others only.
+constexpr int kRankDirect = 256;
+__host__ __device__ inline int64_t rank_slots(int64_t T) { return T / kRankDirect + 1; }
+__host__ __device__ inline int64_t rank_words(int64_t T) { return (T + 31) / 32; }
+
 __global__ void k_bucket_fill(const int64_t* __restrict__ y, int64_t T, int64_t v_off,
                               int64_t V, const int* __restrict__ offsets,
                               int* __restrict__ cursor, int* __restrict__ unsorted) {
@@ -916,20 +922,36 @@ __global__ void k_bucket_fill(const int64_t* __restrict__ y, int64_t T, int64_t 
   if (t >= T) return;
   const int64_t yy = y[t] - v_off;
   if (yy < 0 || yy >= V) return;
-  unsorted[offsets[yy] + atomicAdd(cursor + yy, 1)] = int(t);
+  const int b = offsets[yy];
+  if (offsets[yy + 1] - b > kRankDirect) return;
+  unsorted[b + atomicAdd(cursor + yy, 1)] = int(t);
 }
 
 // Place each token at its rank among the tokens of its bucket (ascending t).
+// A bucket of at most kRankDirect tokens: each token counts the smaller
+// token indices in the bucket's (unordered) list.  A larger bucket: each
+// token sets its bit in the bucket's bitmap of T bits, and
+// k_bucket_rank_large writes the set bits out in order, so no bucket costs
+// more than O(size + T / 32).  Large buckets start at least kRankDirect
+// positions apart, so b / kRankDirect names a slot of its own.
 __global__ void k_bucket_rank(const int64_t* __restrict__ y, int64_t T, int64_t v_off,
                               int64_t V, const int* __restrict__ offsets,
-                              const int* __restrict__ unsorted, int* __restrict__ sorted) {
+                              const int* __restrict__ unsorted, int* __restrict__ sorted,
+                              unsigned* __restrict__ bits, int* __restrict__ meta) {
   const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (t >= T) return;
   const int64_t yy = y[t] - v_off;
   if (yy < 0 || yy >= V) return;
   const int b = offsets[yy], e = offsets[yy + 1];
-  // 16 independent loads per step: a large bucket's scan is not one load
-  // latency per entry
+  if (e - b > kRankDirect) {
+    const int64_t slot = b / kRankDirect;
+    atomicOr(bits + slot * rank_words(T) + (t >> 5), 1u << (t & 31));
+    meta[2 * slot] = b;       // the same values from every token of the bucket
+    meta[2 * slot + 1] = e;
+    return;
+  }
+  // 16 independent loads per step: a bucket's scan is not one load latency
+  // per entry
   int rank = 0, p = b;
   for (; p + 16 <= e; p += 16) {
     int u[16];
@@ -940,6 +962,36 @@ __global__ void k_bucket_rank(const int64_t* __restrict__ y, int64_t T, int64_t 
   }
   for (; p < e; ++p) rank += unsorted[p] < int(t);
   sorted[b + rank] = int(t);
+}
+
+// One workgroup per slot: the set bits of a large bucket's bitmap in
+// ascending order are its tokens in ascending order; 256 words per round,
+// each word's bits placed after the popcounts of the words before it.
+__global__ __launch_bounds__(256) void k_bucket_rank_large(const unsigned* __restrict__ bits,
+                                                           const int* __restrict__ meta,
+                                                           int64_t T, int* __restrict__ sorted) {
+  __shared__ int part[4];
+  const int64_t slot = blockIdx.x;
+  const int b = meta[2 * slot], e = meta[2 * slot + 1];
+  if (e - b <= kRankDirect) return;   // unused slot (zeroed) or a direct bucket
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int64_t nw = rank_words(T);
+  const unsigned* wb = bits + slot * nw;
+  int base = b;
+  for (int64_t w0 = 0; w0 < nw; w0 += 256) {
+    const unsigned word = w0 + tid < nw ? wb[w0 + tid] : 0u;
+    const int c = __popc(word);
+    const int incl = wave_incl_scan(c, lane);
+    if (lane == 63) part[w] = incl;
+    __syncthreads();
+    int pos = base + incl - c;
+    for (int k = 0; k < w; ++k) pos += part[k];
+    const int total = part[0] + part[1] + part[2] + part[3];
+    for (unsigned x = word; x != 0u; x &= x - 1u)
+      sorted[pos++] = int((w0 + tid) * 32 + __builtin_ctz(x));
+    base += total;
+    __syncthreads();   // part[] is rewritten in the next round
+  }
 }
 
 // dW[v, :] += sum over tokens t with y_t = v (ascending t) of dlogp_t h_t,
@@ -1323,6 +1375,8 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   T* Hm = cv.take<T>(size_t(Tn) * d);      // H with the dead tokens' rows zeroed
   int* counts = cv.take<int>(Vs + 1);   // counts[Vs]: live tokens
   int* cursor = cv.take<int>(Vs);
+  unsigned* rank_bits = cv.take<unsigned>(size_t(rank_slots(Tn) * rank_words(Tn)));
+  int* rank_meta = cv.take<int>(size_t(2 * rank_slots(Tn)));
   int* offsets = cv.take<int>(Vs + 1);
   int* unsorted = cv.take<int>(Tn);
   int* sorted = cv.take<int>(Tn);
@@ -1358,7 +1412,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
     ProfScope ps_(s, "logprob_bwd_bucket", 0.0, 32.0 * Tn + 16.0 * Vs);
     const int nb = int(cdiv(Vs, 256)), tb = int(cdiv(Tn, 256));
     hipLaunchKernelGGL(k_fill_i32, dim3(nb + 1), dim3(256), 0, s, counts, Vs + 1, 0);
-    hipLaunchKernelGGL(k_fill_i32, dim3(nb), dim3(256), 0, s, cursor, Vs, 0);
+    // cursor, the large buckets' bitmaps and their slots: one zero fill
+    const int64_t zspan = reinterpret_cast<int*>(rank_meta + 2 * rank_slots(Tn)) - cursor;
+    if (cdiv(zspan, int64_t(256)) > int64_t(0x7fffffff)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_fill_i32, dim3(unsigned(cdiv(zspan, int64_t(256)))), dim3(256), 0, s,
+                       cursor, zspan, 0);
     hipLaunchKernelGGL(k_hist, dim3(tb), dim3(256), 0, s, y, dlogp, Tn, v_off, Vs, counts);
     const int nsb = int(cdiv(Vs, kScanBlock));
     hipLaunchKernelGGL(k_scan_sums, dim3(nsb), dim3(256), 0, s, counts, Vs, scan_sums);
@@ -1366,7 +1424,9 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
     hipLaunchKernelGGL(k_bucket_fill, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, offsets,
                        cursor, unsorted);
     hipLaunchKernelGGL(k_bucket_rank, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, offsets,
-                       unsorted, sorted);
+                       unsorted, sorted, rank_bits, rank_meta);
+    hipLaunchKernelGGL(k_bucket_rank_large, dim3(unsigned(rank_slots(Tn))), dim3(256), 0, s,
+                       rank_bits, rank_meta, Tn, sorted);
   }
   for (int64_t v0 = 0; v0 < Vs; v0 += chunk) {
     const int64_t width = min(chunk, Vs - v0);
@@ -1508,6 +1568,8 @@ size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += align_up(size_t(d) * pld * es, kWsAlign);
   n += align_up(size_t(T) * size_t(d) * es, kWsAlign);   // H with dead rows zeroed
   n += align_up(size_t(V + 1) * 4, kWsAlign) + align_up(size_t(V) * 4, kWsAlign);
+  n += align_up(size_t(rank_slots(T) * rank_words(T)) * 4, kWsAlign) +
+       align_up(size_t(2 * rank_slots(T)) * 4, kWsAlign);   // large buckets' bitmaps
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
   n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);
@@ -1527,6 +1589,8 @@ size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += align_up(size_t(d) * pld * es, kWsAlign);
   n += align_up(size_t(T) * size_t(d) * es, kWsAlign);   // H with dead rows zeroed
   n += align_up(size_t(V + 1) * 4, kWsAlign) + align_up(size_t(V) * 4, kWsAlign);
+  n += align_up(size_t(rank_slots(T) * rank_words(T)) * 4, kWsAlign) +
+       align_up(size_t(2 * rank_slots(T)) * 4, kWsAlign);   // large buckets' bitmaps
   n += align_up(size_t(V + 1) * 4, kWsAlign);
   n += 2 * align_up(size_t(T) * 4, kWsAlign);
   n += align_up(size_t(cdiv(V, kScanBlock)) * 4, kWsAlign);

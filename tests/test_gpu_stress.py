@@ -151,6 +151,40 @@ def test_skewed_targets_both_pairs():
         assert rel_fro(row, dW_o[top]) <= GRAD_RTOL, pair
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dominant_target_buckets(dtype):
+    # 60% of 20000 tokens share one target and 20% another (buckets far past
+    # the direct-rank size, placed through their bitmaps of 625 words, three
+    # rounds of 256), the rest spread; a tenth ignored (-1 or V) and some
+    # zero dlogp.  Every output against the oracle; two runs bit-identical.
+    T, d, V = 20000, 64, 500
+    cfg = scaled_config(1, d=d, V=V, dtype=dtype, seed=51)
+    Hn, Wn, hb, wb = make_tensors_numpy(cfg, T)
+    rng = np.random.default_rng(52)
+    u = rng.random(T)
+    y = np.where(u < 0.6, 7, np.where(u < 0.8, 123, rng.integers(0, V, size=T))).astype(np.int64)
+    y[rng.random(T) < 0.05] = -1
+    y[rng.random(T) < 0.05] = V
+    dlogp = (rng.standard_normal(T) / T).astype(np.float32)
+    dlogp[rng.random(T) < 0.15] = 0.0
+    case = dict(H=Hn, W=Wn, hb=hb, wb=wb, y=y)
+    H, W, yd = device_tensors(case)
+    dl = torch.from_numpy(dlogp).cuda()
+    res = _both_pairs(H, W, yd, dl)
+    again = _both_pairs(H, W, yd, dl)
+    yc = np.where((y >= 0) & (y < V), y, -1)
+    logp_o, lse_o = oracle.logprob_fwd(Hn, Wn, yc)
+    dl64 = dlogp.astype(np.float64)
+    dH_o, dW_o = oracle.logprob_bwd(Hn, Wn, yc, lse_o, dl64)
+    for pair, (logp, lse, dH, dW) in res.items():
+        assert np.max(np.abs(lse.cpu().numpy() - lse_o)) <= LOGP_ATOL, pair
+        assert rel_fro(dH.double().cpu().numpy(), dH_o) <= GRAD_RTOL, pair
+        assert rel_fro(dW.double().cpu().numpy(), dW_o) <= GRAD_RTOL, pair
+        for v in (7, 123):
+            assert rel_fro(dW[v].double().cpu().numpy(), dW_o[v]) <= GRAD_RTOL, (pair, v)
+        assert torch.equal(dW, again[pair][3]) and torch.equal(dH, again[pair][2]), pair
+
+
 @pytest.mark.parametrize("sh,sw,sg", [(17, -17, -40), (-20, 20, 30), (0, 0, -126)])
 def test_extreme_magnitudes_both_pairs(sh, sw, sg):
     # H 2^sh, W 2^sw, dlogp 2^sg times the usual draws: |H| or |W| beyond
