@@ -60,31 +60,31 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "6933d4a15896c09243c634eeec119447ffbd6579bf052ca6755b0309e729874d",
+        "cb0b8832b15e010c9d810d5f647521a34e6ac1f65a066a50c889998ff8de24ff",
     "read_bytes_per_launch": {
-        "logprob_fwd_gemm": 41736796992,
-        "logprob_fwd_merge": 78110528,
-        "logprob_bwd_live_rows": 36076480,
+        "logprob_fwd_gemm": 35971315648,
+        "logprob_fwd_merge": 78110848,
+        "logprob_bwd_live_rows": 36079808,
         "logprob_bwd_bounds": 83392,
-        "logprob_bwd_bucket": 5745024,
-        "logprob_bwd_probs": 32205121664,
-        "logprob_bwd_transpose": 689527808,
-        "logprob_bwd_dhidden": 30032824576,
-        "logprob_bwd_dweight": 30420539136,
-        "logprob_bwd_onehot_dw": 107569600,
+        "logprob_bwd_bucket": 5811136,
+        "logprob_bwd_probs": 32634861568,
+        "logprob_bwd_transpose": 689531200,
+        "logprob_bwd_dhidden": 30132214464,
+        "logprob_bwd_dweight": 32240192832,
+        "logprob_bwd_onehot_dw": 107625792,
         "rl_loss": 340480,
     },
     "write_bytes_per_launch": {
-        "logprob_fwd_gemm": 78367872,
+        "logprob_fwd_gemm": 78367584,
         "logprob_fwd_merge": 131072,
         "logprob_bwd_live_rows": 134217728,
         "logprob_bwd_bounds": 32,
-        "logprob_bwd_bucket": 2514016,
-        "logprob_bwd_probs": 4978793856,
+        "logprob_bwd_bucket": 2647328,
+        "logprob_bwd_probs": 4978819456,
         "logprob_bwd_transpose": 689438720,
         "logprob_bwd_dhidden": 268435456,
-        "logprob_bwd_dweight": 2556428800,
-        "logprob_bwd_onehot_dw": 69888736,
+        "logprob_bwd_dweight": 2556428288,
+        "logprob_bwd_onehot_dw": 69889696,
         "rl_loss": 80896,
     },
 }
