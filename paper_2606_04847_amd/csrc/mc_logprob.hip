@@ -849,6 +849,13 @@ __global__ __launch_bounds__(256) void k_hist(const int64_t* __restrict__ y,
   }
 }
 
+// A bucket of more than kRankDirect tokens is ordered through a bitmap in
+// slot offsets[v] / kRankDirect (see k_bucket_rank): large buckets start at
+// least kRankDirect positions apart, so the slots are distinct.
+constexpr int kRankDirect = 256;
+__host__ __device__ inline int64_t rank_slots(int64_t T) { return T / kRankDirect + 1; }
+__host__ __device__ inline int64_t rank_words(int64_t T) { return (T + 31) / 32; }
+
 // Exclusive scan of counts[V] into offsets[V + 1] in two passes over blocks
 // of kScanBlock entries (256 threads x 4 consecutive entries, coalesced):
 // k_scan_sums writes each block's total, k_scan_apply adds the totals of the
@@ -879,9 +886,12 @@ __global__ __launch_bounds__(256) void k_scan_sums(const int* __restrict__ count
   if (tid == 0) sums[blockIdx.x] = part[0] + part[1] + part[2] + part[3];
 }
 
+// k_scan_apply also records each large bucket's range [b, e) in its slot of
+// `meta` (zeroed beforehand).
 __global__ __launch_bounds__(256) void k_scan_apply(const int* __restrict__ counts, int64_t V,
                                                     const int* __restrict__ sums,
-                                                    int* __restrict__ offsets) {
+                                                    int* __restrict__ offsets,
+                                                    int* __restrict__ meta) {
   __shared__ int part[4];
   __shared__ int base[4];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -903,7 +913,13 @@ __global__ __launch_bounds__(256) void k_scan_apply(const int* __restrict__ coun
   for (int k = 0; k < w; ++k) run += part[k];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    if (i0 + q < V) offsets[i0 + q] = run;
+    if (i0 + q < V) {
+      offsets[i0 + q] = run;
+      if (c[q] > kRankDirect) {
+        meta[2 * (run / kRankDirect)] = run;
+        meta[2 * (run / kRankDirect) + 1] = run + c[q];
+      }
+    }
     run += c[q];
   }
   if (i0 < V && i0 + 4 >= V) offsets[V] = run;   // the thread holding entry V - 1
@@ -911,10 +927,6 @@ __global__ __launch_bounds__(256) void k_scan_apply(const int* __restrict__ coun
 
 // Buckets larger than kRankDirect are ordered through a bitmap (see
 // k_bucket_rank); the (unordered) list is filled for the others only.
-constexpr int kRankDirect = 256;
-__host__ __device__ inline int64_t rank_slots(int64_t T) { return T / kRankDirect + 1; }
-__host__ __device__ inline int64_t rank_words(int64_t T) { return (T + 31) / 32; }
-
 __global__ void k_bucket_fill(const int64_t* __restrict__ y, int64_t T, int64_t v_off,
                               int64_t V, const int* __restrict__ offsets,
                               int* __restrict__ cursor, int* __restrict__ unsorted) {
@@ -930,14 +942,13 @@ __global__ void k_bucket_fill(const int64_t* __restrict__ y, int64_t T, int64_t 
 // Place each token at its rank among the tokens of its bucket (ascending t).
 // A bucket of at most kRankDirect tokens: each token counts the smaller
 // token indices in the bucket's (unordered) list.  A larger bucket: each
-// token sets its bit in the bucket's bitmap of T bits, and
-// k_bucket_rank_large writes the set bits out in order, so no bucket costs
-// more than O(size + T / 32).  Large buckets start at least kRankDirect
-// positions apart, so b / kRankDirect names a slot of its own.
+// token sets its bit in the bucket's bitmap of T bits (in the bucket's
+// slot), and k_bucket_rank_large writes the set bits out in order, so no
+// bucket costs more than O(size + T / 32).
 __global__ void k_bucket_rank(const int64_t* __restrict__ y, int64_t T, int64_t v_off,
                               int64_t V, const int* __restrict__ offsets,
                               const int* __restrict__ unsorted, int* __restrict__ sorted,
-                              unsigned* __restrict__ bits, int* __restrict__ meta) {
+                              unsigned* __restrict__ bits) {
   const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (t >= T) return;
   const int64_t yy = y[t] - v_off;
@@ -946,8 +957,6 @@ __global__ void k_bucket_rank(const int64_t* __restrict__ y, int64_t T, int64_t 
   if (e - b > kRankDirect) {
     const int64_t slot = b / kRankDirect;
     atomicOr(bits + slot * rank_words(T) + (t >> 5), 1u << (t & 31));
-    meta[2 * slot] = b;       // the same values from every token of the bucket
-    meta[2 * slot + 1] = e;
     return;
   }
   // 16 independent loads per step: a bucket's scan is not one load latency
@@ -1420,11 +1429,12 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
     hipLaunchKernelGGL(k_hist, dim3(tb), dim3(256), 0, s, y, dlogp, Tn, v_off, Vs, counts);
     const int nsb = int(cdiv(Vs, kScanBlock));
     hipLaunchKernelGGL(k_scan_sums, dim3(nsb), dim3(256), 0, s, counts, Vs, scan_sums);
-    hipLaunchKernelGGL(k_scan_apply, dim3(nsb), dim3(256), 0, s, counts, Vs, scan_sums, offsets);
+    hipLaunchKernelGGL(k_scan_apply, dim3(nsb), dim3(256), 0, s, counts, Vs, scan_sums, offsets,
+                       rank_meta);
     hipLaunchKernelGGL(k_bucket_fill, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, offsets,
                        cursor, unsorted);
     hipLaunchKernelGGL(k_bucket_rank, dim3(tb), dim3(256), 0, s, y, Tn, v_off, Vs, offsets,
-                       unsorted, sorted, rank_bits, rank_meta);
+                       unsorted, sorted, rank_bits);
     hipLaunchKernelGGL(k_bucket_rank_large, dim3(unsigned(rank_slots(Tn))), dim3(256), 0, s,
                        rank_bits, rank_meta, Tn, sorted);
   }
