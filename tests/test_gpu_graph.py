@@ -1,8 +1,9 @@
 """The fused step under HIP graph capture, and the empty batch.
 
 Every entry point enqueues kernels only (no memsets, no allocations, no host
-synchronisation), so the whole recompute step — forward, RL loss, backward —
-can be captured once and replayed.  The test replays the captured step
+synchronisation), so the whole step — forward, RL loss, backward, through
+either pair (recompute, or the softmax cache held outside the graph) — can
+be captured once and replayed.  The test replays the captured step
 several times with eager work and synchronisations in between, checks every
 replay bit for bit against the eager step on the same inputs, then changes
 the inputs in place and checks that a replay follows them.  The empty batch
@@ -36,10 +37,16 @@ def _case():
     return small_case(cfg)
 
 
-def _step(mc, H, W, y, lr, st, params):
-    logp, lse = mc.logprob_fwd(H, W, y)
+def _step(mc, H, W, y, lr, st, params, cache=None):
+    if cache is None:
+        logp, lse = mc.logprob_fwd(H, W, y)
+    else:
+        logp, lse = mc.logprob_fwd_cached(H, W, y, cache)
     out = mc.rl_loss(logp, lr, st["mask"], st["cu"], st["cg"], st["rewards"], params)
-    dH, dW = mc.logprob_bwd(H, W, y, lse, out["dlogp"])
+    if cache is None:
+        dH, dW = mc.logprob_bwd(H, W, y, lse, out["dlogp"])
+    else:
+        dH, dW = mc.logprob_bwd_cached(H, W, y, lse, out["dlogp"], cache)
     return dict(logp=logp, lse=lse, loss=out["loss"], dlogp=out["dlogp"],
                 seq_mask=out["seq_mask"], seq_len=out["seq_len"], n_valid=out["n_valid"],
                 error_flag=out["error_flag"], dH=dH, dW=dW)
@@ -54,7 +61,8 @@ def _same(a, b):
         assert np.array_equal(a[k], b[k], equal_nan=True), k
 
 
-def test_recompute_step_graph_replays():
+@pytest.mark.parametrize("pair", ["recompute", "cached"])
+def test_step_graph_replays(pair):
     import paper_2606_04847_amd as mc
     case = _case()
     p = oracle.RLParams()
@@ -63,20 +71,21 @@ def test_recompute_step_graph_replays():
     st = structure_tensors(case["s"])
     lr = torch.from_numpy(o["lr"]).cuda()
     params = to_params(p)
+    cache = mc.softmax_cache(H, W) if pair == "cached" else None
 
-    eager = _host(_step(mc, H, W, y, lr, st, params))
+    eager = _host(_step(mc, H, W, y, lr, st, params, cache))
     assert_step_parity(eager, o)   # the eager step itself matches the oracle
 
     # warm up on a side stream, then capture
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        _step(mc, H, W, y, lr, st, params)
+        _step(mc, H, W, y, lr, st, params, cache)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
-        static = _step(mc, H, W, y, lr, st, params)
+        static = _step(mc, H, W, y, lr, st, params, cache)
     torch.cuda.synchronize()
 
     for rep in range(3):
@@ -90,7 +99,7 @@ def test_recompute_step_graph_replays():
 
     # the graph reads its inputs at replay time
     H.mul_(0.5)
-    eager2 = _host(_step(mc, H, W, y, lr, st, params))
+    eager2 = _host(_step(mc, H, W, y, lr, st, params, cache))
     assert not np.array_equal(eager2["dW"], eager["dW"])
     graph.replay()
     torch.cuda.synchronize()
