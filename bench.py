@@ -60,31 +60,31 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "cb0b8832b15e010c9d810d5f647521a34e6ac1f65a066a50c889998ff8de24ff",
+        "ea321adf5abee0df12a173fe82070a6219f17797607139f563820325c82f8065",
     "read_bytes_per_launch": {
-        "logprob_fwd_gemm": 35971315648,
+        "logprob_fwd_gemm": 38652817024,
         "logprob_fwd_merge": 78110848,
-        "logprob_bwd_live_rows": 36079808,
-        "logprob_bwd_bounds": 83392,
-        "logprob_bwd_bucket": 5811136,
-        "logprob_bwd_probs": 32634861568,
-        "logprob_bwd_transpose": 689531200,
-        "logprob_bwd_dhidden": 30132214464,
-        "logprob_bwd_dweight": 32240192832,
-        "logprob_bwd_onehot_dw": 107625792,
+        "logprob_bwd_live_rows": 36080192,
+        "logprob_bwd_bounds": 83328,
+        "logprob_bwd_bucket": 5812032,
+        "logprob_bwd_probs": 32892538624,
+        "logprob_bwd_transpose": 689528000,
+        "logprob_bwd_dhidden": 30113924864,
+        "logprob_bwd_dweight": 31390125120,
+        "logprob_bwd_onehot_dw": 107582080,
         "rl_loss": 340480,
     },
     "write_bytes_per_launch": {
-        "logprob_fwd_gemm": 78367584,
+        "logprob_fwd_gemm": 78367616,
         "logprob_fwd_merge": 131072,
         "logprob_bwd_live_rows": 134217728,
         "logprob_bwd_bounds": 32,
         "logprob_bwd_bucket": 2647328,
-        "logprob_bwd_probs": 4978819456,
-        "logprob_bwd_transpose": 689438720,
+        "logprob_bwd_probs": 4979009664,
+        "logprob_bwd_transpose": 689438784,
         "logprob_bwd_dhidden": 268435456,
-        "logprob_bwd_dweight": 2556428288,
-        "logprob_bwd_onehot_dw": 69889696,
+        "logprob_bwd_dweight": 2556428416,
+        "logprob_bwd_onehot_dw": 69889408,
         "rl_loss": 80896,
     },
 }
