@@ -276,7 +276,7 @@ def _chain(st):
         assert rel_fro(dH_g, dH_o) <= GRAD_RTOL, pair
         assert np.all(dH_g[~live_rows] == 0.0), pair        # masked / filtered / clipped
         soft_h_g = dH_g - g["dlogp"].astype(np.float64)[rows, None] * Wy
-        # operand bound: fp16 (recompute pair), bf16 (softmax cache)
+        # operand bound: one fp16 rounding (recompute pair), two (softmax cache)
         pbound = PTERM_RTOL_F16 if pair == "recompute" else PTERM_RTOL
         assert rel_fro(soft_h_g[live_rows], soft_h_o[live_rows]) <= pbound, pair
         assert rel_fro(dW_g, dW_o) <= GRAD_RTOL, pair
