@@ -97,6 +97,58 @@ def test_vocab_shards_match_full(dtype):
     assert rel_fro(np.concatenate(dWs), dW_o) <= GRAD_RTOL
 
 
+def test_vocab_shards_full_size():
+    # one GPU's real shard shape: the headline workload (T = 16384, d = 4096,
+    # V = 151936, bf16) split into 8 shards of V/8 = 18992 rows (ragged
+    # 256-row tiles in each).  Merged shard partials against the unsharded
+    # forward on every row and the oracle on sampled rows; the shards' dH parts
+    # (summed) and dW rows (assembled) against the unsharded backward, whose
+    # parity with the oracle at this size is tested elsewhere.
+    from workloads import make_tensors_torch, sample_targets_torch
+    T, d, V, S = 16384, 4096, 151936, 8
+    cfg = scaled_config(4, T=T, d=d, V=V, seed=81)
+    H, W = make_tensors_torch(cfg, T, "cuda")
+    y = sample_targets_torch(cfg, H, W)
+    y[5] = -1
+    mc = _mc()
+    logp_f, lse_f = mc.logprob_fwd(H, W, y)
+    rng = np.random.default_rng(82)
+    dl = (rng.standard_normal(T) / T).astype(np.float32)
+    dl[rng.random(T) < 0.5] = 0.0
+    dld = torch.from_numpy(dl).cuda()
+    dH_f, dW_f = mc.logprob_bwd(H, W, y, lse_f, dld)
+    Vs = V // S
+    bounds = [k * Vs for k in range(S)] + [V]
+    parts = torch.stack([mc.logprob_fwd_shard(H, W[a:b].contiguous(), y, a, V)
+                         for a, b in zip(bounds[:-1], bounds[1:])])
+    logp_s, lse_s, _ = mc.logprob_merge_shards(parts, y, V)
+    dH_s = torch.zeros(T, d, dtype=torch.float64, device="cuda")
+    dW_s = []
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        h, w = mc.logprob_bwd_shard(H, W[a:b].contiguous(), y, lse_s, dld, a, V)
+        dH_s += h.double()
+        dW_s.append(w)
+    dW_s = torch.cat(dW_s)
+    torch.cuda.synchronize()
+    assert torch.max(torch.abs(logp_s - logp_f)).item() <= 1e-4
+    assert torch.max(torch.abs(lse_s - lse_f)).item() <= 1e-4
+    assert logp_s[5].item() == 0.0
+    rows = np.unique(np.concatenate([rng.choice(T, 60, replace=False), [0, T - 1]]))
+    Hh = H[torch.from_numpy(rows).cuda()].float().cpu().numpy()
+    Wh = W.float().cpu().numpy()
+    lo, so = oracle.logprob_fwd(Hh, Wh, y[torch.from_numpy(rows).cuda()].cpu().numpy())
+    assert np.max(np.abs(logp_s.cpu().numpy()[rows] - lo)) <= LOGP_ATOL
+    assert np.max(np.abs(lse_s.cpu().numpy()[rows] - so)) <= LOGP_ATOL
+
+    def rel(a, b):
+        return (torch.linalg.vector_norm((a.double() - b.double()).flatten())
+                / torch.linalg.vector_norm(b.double().flatten())).item()
+    assert rel(dH_s, dH_f) <= 1e-5
+    assert rel(dW_s, dW_f) <= 1e-5
+    print(f"[shards 8 x {Vs}] |dlogp| {torch.max(torch.abs(logp_s - logp_f)).item():.2e} "
+          f"dH {rel(dH_s, dH_f):.2e} dW {rel(dW_s, dW_f):.2e}", flush=True)
+
+
 @pytest.mark.parametrize("beta", [0.05, 0.5])
 def test_kl_term_matches_oracle(beta):
     cfg = scaled_config(4, T=1200, n_groups=4, group_size=8, hi=300, seed=51,
