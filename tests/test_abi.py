@@ -233,3 +233,55 @@ def test_noalloc_loss_rejects_oversized_batches_on_the_host(lib):
     bad.delta = -1.0
     assert lib.mc_rl_loss_noalloc(FAKE, FAKE, None, None, FAKE, FAKE, FAKE, 8, 2, 1,
                                   ctypes.byref(bad), ctypes.byref(o), None) == INVALID
+
+
+def _consumer_source(names):
+    """A program that takes the address of every declared entry point (so the
+    link fails on any missing symbol) and prints the host-only queries."""
+    refs = ",\n    ".join("(const void*)(size_t)&%s" % n for n in names)
+    return f"""#include "mc.h"
+#include <stdio.h>
+#include <stddef.h>
+int main(void) {{
+  const void* volatile fns[] = {{
+    {refs}
+  }};
+  size_t i, n = 0;
+  for (i = 0; i < sizeof fns / sizeof fns[0]; ++i) n += fns[i] != NULL;
+  printf("%zu\\n", n);
+  printf("%s\\n", mc_version());
+  printf("%s\\n", mc_status_string(MC_ERR_WORKSPACE));
+  printf("%zu\\n", mc_rl_loss_noalloc_max_bytes());
+  printf("%zu\\n", mc_logprob_bwd_workspace_size(16384, 4096, 151936, MC_BF16));
+  printf("%zu\\n", mc_logprob_cache_size(16384, 4096, 151936, MC_BF16));
+  return 0;
+}}
+"""
+
+
+@pytest.mark.parametrize("lang", ["c99", "c++17"])
+def test_header_builds_a_plain_consumer(lib, tmp_path, lang):
+    """include/mc.h is a self-contained C header (and C++ through its
+    extern "C" guard): a consumer built with warnings as errors links against
+    libmc.so by name alone and sees the same values as the Python binding."""
+    import shutil
+    import subprocess
+    cc = "gcc" if lang == "c99" else "g++"
+    if shutil.which(cc) is None:
+        pytest.skip(f"{cc} not installed")
+    names = declared_functions()
+    src = tmp_path / ("consumer.c" if lang == "c99" else "consumer.cpp")
+    src.write_text(_consumer_source(names))
+    exe = tmp_path / "consumer"
+    libdir = os.path.dirname(binding.LIB_PATH)
+    subprocess.run([cc, f"-std={lang}", "-Wall", "-Wextra", "-Werror", "-pedantic",
+                    "-I", os.path.join(ROOT, "include"), str(src), "-L", libdir, "-lmc",
+                    f"-Wl,-rpath,{libdir}", "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True,
+                         timeout=60).stdout.split("\n")
+    assert int(out[0]) == len(names)
+    assert out[1] == binding.version()
+    assert out[2] == "MC_ERR_WORKSPACE"
+    assert int(out[3]) == lib.mc_rl_loss_noalloc_max_bytes()
+    assert int(out[4]) == lib.mc_logprob_bwd_workspace_size(16384, 4096, 151936, BF16)
+    assert int(out[5]) == lib.mc_logprob_cache_size(16384, 4096, 151936, BF16)
