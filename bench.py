@@ -286,6 +286,23 @@ def roofline_of(kernels):
             "avg_launch_ms": ms}
 
 
+def recompute_cols(y, dlogp, V):
+    """Token columns that the recompute backward's softmax contraction runs
+    its MFMAs on: the live tokens (nonzero dlogp, target in [0, V)) come first
+    in its token order, and a 256-token tile with none of them only writes its
+    zero rows."""
+    n = int(((dlogp != 0) & (y >= 0) & (y < V)).sum().item())
+    return min(int(y.numel()), -(-n // 256) * 256)
+
+
+def count_recompute(res, cols, d, V):
+    """Replace the library's dense figure for the softmax contraction by the
+    FLOPs it executes (cols token columns per launch)."""
+    k = res["kernels"].get("logprob_bwd_probs")
+    if k:
+        k["flops"] = k["launches"] * 2.0 * cols * d * V
+
+
 def summary(res, T, counted, executed):
     ms = res["ms_per_step"]
     out = {"value": T / (ms * 1e-3), "ms_per_step": ms, "median_ms_per_step": res["median_ms"],
@@ -523,7 +540,10 @@ def main():
             mc.logprob_bwd_shard(H, Ws, y, lse, dlogp, 0, V, dhidden=dH, dweight=dWs,
                                  workspace=ws_b)
         res = time_steps(step, args.steps, args.warmup, sampler, flush, args.flush_reps)
-        summ = summary(res, T, 6.0 * T * d * Vs, 8.0 * T * d * Vs)
+        cols = recompute_cols(y, dlogp, V)
+        count_recompute(res, cols, d, Vs)
+        summ = summary(res, T, 6.0 * T * d * Vs, 6.0 * T * d * Vs + 2.0 * cols * d * Vs)
+        summ["recompute_token_cols"] = cols
         config.update(workload=config["workload"] + f"; vocabulary shard of {Vs} rows (V/8)",
                       V_shard=Vs, backward="recompute logits (shard)")
         line.update(summ)
@@ -580,15 +600,21 @@ def main():
         head = "recompute" if "recompute" in results else "cached"
         for name, res in results.items():
             out = res["out"]
-            summ = summary(res, T, 6.0 * T * d * V,
-                           (8.0 if name == "recompute" else 6.0) * T * d * V)
+            executed = 6.0 * T * d * V
+            if name == "recompute":
+                cols = recompute_cols(y, out["dlogp"], V)
+                count_recompute(res, cols, d, V)
+                executed += 2.0 * cols * d * V
+            summ = summary(res, T, 6.0 * T * d * V, executed)
+            if name == "recompute":
+                summ["recompute_token_cols"] = cols
             summ["loss"] = float(out["loss"].item())
             summ["n_valid"] = int(out["n_valid"].item())
             results[name] = summ
         line.update(results[head])
         config["backward"] = ("recompute logits: the forward writes no [T,V] tensor"
                               if head == "recompute" else "softmax cache: the forward writes a "
-                              "[T,V] bf16 cache")
+                              "[T,V] fp16 cache")
         line["config"] = config
         if head == "recompute" and "cached" in results:
             line["cached"] = results["cached"]

@@ -82,10 +82,13 @@ __device__ __forceinline__ int panel_stage_off(int v, int t) {
 // stored, from one base address per thread: as a loop of read, wait, store
 // (with 64-bit address arithmetic in each step) this took most of the
 // cache's cost in the forward.
+// With `rowmap` set, staged token row n0 + tl goes to row rowmap[n0 + tl] of
+// the panels (a 128-byte row stays one contiguous store).
 template <typename TP>   // a 2-byte element type
 __device__ __forceinline__ void store_staged_panels(const char* lds, TP* P, int64_t m0,
                                                     int64_t n0, int64_t Tn, int64_t ld,
-                                                    int64_t pld) {
+                                                    int64_t pld,
+                                                    const int* __restrict__ rowmap = nullptr) {
   constexpr int64_t kPanel = 64;
   constexpr int kRows = kThreads / 8;            // token rows per round
   constexpr int kRounds = 256 / kRows;           // rounds per panel
@@ -101,6 +104,23 @@ __device__ __forceinline__ void store_staged_panels(const char* lds, TP* P, int6
                                                     ((it % kRounds) * kRows + r0) * 128 + sw);
     v[it] = swap ? u32x4{x[2], x[3], x[0], x[1]} : x;
   }
+  if (rowmap != nullptr) {
+    int64_t row[kRounds];
+#pragma unroll
+    for (int rd = 0; rd < kRounds; ++rd) {
+      const int64_t j = n0 + rd * kRows + r0;
+      row[rd] = j < Tn ? int64_t(rowmap[j]) : -1;
+    }
+    TP* const base = P + (m0 / kPanel) * pld * kPanel + ch * 8;
+#pragma unroll
+    for (int it = 0; it < kIters; ++it) {
+      const int pn = it / kRounds, rd = it % kRounds;
+      if (row[rd] >= 0 && m0 + pn * kPanel < ld)
+        __builtin_nontemporal_store(
+            v[it], reinterpret_cast<u32x4*>(base + pn * pld * kPanel + row[rd] * kPanel));
+    }
+    return;
+  }
   TP* const base = P + (m0 / kPanel) * pld * kPanel + (n0 + r0) * kPanel + ch * 8;
 #pragma unroll
   for (int it = 0; it < kIters; ++it) {
@@ -109,6 +129,34 @@ __device__ __forceinline__ void store_staged_panels(const char* lds, TP* P, int6
       __builtin_nontemporal_store(
           v[it], reinterpret_cast<u32x4*>(base + pn * pld * kPanel +
                                           int64_t((it % kRounds) * kRows) * kPanel));
+  }
+}
+
+// Zero rows of the panels for the tile's 256 token positions n0 .. n0 + 255
+// (row rowmap[j] for position j < Tn) and its 256 chunk columns from m0
+// (panels below ld): 16-byte non-temporal stores, eight lanes per 128-byte
+// row, any element size.
+template <typename TP>
+__device__ __forceinline__ void store_zero_panels(TP* P, int64_t m0, int64_t n0, int64_t Tn,
+                                                  int64_t ld, int64_t pld,
+                                                  const int* __restrict__ rowmap) {
+  constexpr int64_t kPanel = 128 / sizeof(TP);
+  constexpr int kPanels = int(256 / kPanel);     // panels per tile
+  constexpr int kRows = kThreads / 8;
+  constexpr int kRounds = 256 / kRows;
+  const int ch = threadIdx.x & 7, r0 = threadIdx.x >> 3;
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  TP* const base = P + (m0 / kPanel) * pld * kPanel + ch * (16 / int(sizeof(TP)));
+#pragma unroll
+  for (int rd = 0; rd < kRounds; ++rd) {
+    const int64_t j = n0 + rd * kRows + r0;
+    if (j >= Tn) continue;
+    const int64_t row = rowmap[j];
+#pragma unroll
+    for (int pn = 0; pn < kPanels; ++pn)
+      if (m0 + pn * kPanel < ld)
+        __builtin_nontemporal_store(
+            z, reinterpret_cast<u32x4*>(base + pn * pld * kPanel + row * kPanel));
   }
 }
 
@@ -476,10 +524,28 @@ struct EpiProbs {
                                    // width; pld: padded token count
   TP* P;                           // panel layout (see Lay::TileTK)
   const unsigned* bound;           // max |dlogp| (fp16 operand) or null
+  // Tile columns are positions in the live-first token order: the B operand
+  // holds the row of token perm[j] at position j, and P~'s row perm[j] is
+  // written.  Positions from *nlive on hold tokens whose P~ rows are zero, so
+  // a tile whose first position is past them writes its zero rows without
+  // the contraction.  Null: positions are tokens, every tile is computed.
+  const int* perm;
+  const int* nlive;
   static constexpr int64_t kPanel = 128 / sizeof(TP);
 
-  // lse_t log2(e) and -dlogp_t (0 for ignored tokens) of this lane's kTN
-  // token columns
+  __device__ __forceinline__ int64_t token(int64_t j) const {
+    return perm != nullptr ? int64_t(perm[j]) : j;
+  }
+  // No live token at the tile's positions (wave-uniform).
+  __device__ __forceinline__ bool dead_tile(int64_t n0) const {
+    return nlive != nullptr && n0 >= int64_t(*nlive);
+  }
+  __device__ __forceinline__ void zero_tile(int64_t m0, int64_t n0) const {
+    store_zero_panels(P, m0, n0, Tn, ld, pld, perm);
+  }
+
+  // lse_t log2(e) and -dlogp_t (0 for ignored tokens) of the tokens of this
+  // lane's kTN columns
   struct Pre {
     float l2[kTN], g[kTN];
   };
@@ -489,11 +555,11 @@ struct EpiProbs {
     const int sh = bound != nullptr ? probs_shift(*bound) : 0;
 #pragma unroll
     for (int j = 0; j < kTN; ++j) {
-      const int64_t t = n0 + wn * kWaveCols + j * 16 + (lane & 15);
+      const int64_t pos = n0 + wn * kWaveCols + j * 16 + (lane & 15);
       p.l2[j] = 0.0f;
       p.g[j] = 0.0f;
-      if (t < Tn) {
-        const int64_t yy = y[t];
+      if (pos < Tn) {
+        const int64_t t = token(pos), yy = y[t];
         p.l2[j] = lse[t] * kLog2e;
         p.g[j] = (yy >= 0 && yy < V) ? ldexpf(-dlogp[t], sh) : 0.0f;
       }
@@ -510,14 +576,17 @@ struct EpiProbs {
 #pragma unroll
     for (int j = 0; j < kTN; ++j) {
       const int tl = wn * kWaveCols + j * 16 + (lane & 15);
-      const int64_t t = n0 + tl;
+      const int64_t pos = n0 + tl;   // position of the column's token
       const float lb = pre.l2[j], gs = pre.g[j];
       // Whether any of the column block's 16 tokens has a nonzero factor
       // (wave-uniform).  A block of tokens with zero dlogp (outside the loss
       // mask, filtered, clipped, ignored) has an all-zero operand: its zeros
       // are written without evaluating the exponentials.
-      const bool live = __builtin_amdgcn_ballot_w64(t < Tn && gs != 0.0f) != 0;
-      if (t >= Tn) continue;
+      const bool live = __builtin_amdgcn_ballot_w64(pos < Tn && gs != 0.0f) != 0;
+      if (pos >= Tn) continue;
+      // the 4-byte operand's direct stores need the token (not held across
+      // the main loop: registers)
+      const int64_t tok = sizeof(TP) == 2 ? 0 : token(pos);
 #pragma unroll
       for (int i = 0; i < kTM; ++i) {
         {
@@ -538,7 +607,7 @@ struct EpiProbs {
                 __builtin_bit_cast(u32x2, __builtin_convertvector(p, tp4));
           } else {
             const int64_t c = m0 + vr;
-            TP* dst = P + (c / kPanel) * pld * kPanel + t * kPanel + c % kPanel;
+            TP* dst = P + (c / kPanel) * pld * kPanel + tok * kPanel + c % kPanel;
             *reinterpret_cast<f32x4*>(dst) = p;
           }
         }
@@ -559,7 +628,7 @@ struct EpiProbs {
       values<false>(acc, lds, lane, wm, wn, pre, vlim, llim, m0, n0);
     if constexpr (sizeof(TP) == 2) {
       __syncthreads();
-      store_staged_panels(lds, P, m0, n0, Tn, ld, pld);
+      store_staged_panels(lds, P, m0, n0, Tn, ld, pld, perm);
     }
   }
 };
@@ -796,25 +865,123 @@ __global__ __launch_bounds__(256) void k_transpose(const TI* __restrict__ in, in
   }
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(v, o, 64);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+// A token whose row of the softmax operand can be nonzero: dlogp_t != 0
+// and a target in [0, V).
+__device__ __forceinline__ bool token_live(int64_t yy, float g, int64_t V) {
+  return g != 0.0f && yy >= 0 && yy < V;
+}
+
 // Hm[t] = H[t] for the tokens whose rows of the softmax operand can be
 // nonzero (dlogp_t != 0 and a target in [0, V)), a zero row otherwise.  The
 // backward's softmax contraction and the H^T operand of dW read Hm instead
 // of H: every result stays the same (the operand is exactly zero on those
 // tokens, so z there only feeds products by zero), while the MFMAs on the
 // zero rows draw less power, and these contractions run power-limited.
+//
+// With `perm` set (the recompute backward), thread i handles chunk i of the
+// row at position j = i / cpr of the live-first order (k_live_perm): it
+// writes the chunk to row j of Hp and to row perm[j] of Hm, so each chunk
+// of H is read once.
 template <typename T>
 __global__ __launch_bounds__(256) void k_live_rows(const T* __restrict__ H,
                                                    const int64_t* __restrict__ y,
                                                    const float* __restrict__ dlogp, int64_t Tn,
-                                                   int64_t d, int64_t V, T* __restrict__ Hm) {
+                                                   int64_t d, int64_t V, T* __restrict__ Hm,
+                                                   const int* __restrict__ perm,
+                                                   T* __restrict__ Hp) {
   constexpr int CE = 16 / sizeof(T);   // elements per 16-byte chunk (d is a multiple)
   const int64_t cpr = d / CE;
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i >= Tn * cpr) return;
-  const int64_t t = i / cpr, yy = y[t];
+  const int64_t j = i / cpr, c = i - j * cpr;
+  const int64_t t = perm != nullptr ? int64_t(perm[j]) : j;
   u32x4 v = {0u, 0u, 0u, 0u};
-  if (dlogp[t] != 0.0f && yy >= 0 && yy < V) v = reinterpret_cast<const u32x4*>(H)[i];
-  reinterpret_cast<u32x4*>(Hm)[i] = v;
+  if (token_live(y[t], dlogp[t], V)) v = reinterpret_cast<const u32x4*>(H)[t * cpr + c];
+  reinterpret_cast<u32x4*>(Hm)[t * cpr + c] = v;
+  if (perm != nullptr) reinterpret_cast<u32x4*>(Hp)[i] = v;
+}
+
+// Live-first order of the tokens for the recompute backward: the live tokens
+// (a nonzero row of the softmax operand) in index order, then the others in
+// index order.  perm[j] = the token at position j; nlive[0] = the number of
+// live tokens.  Two passes over blocks of kLiveBlock tokens (256 threads x 4
+// consecutive tokens): k_live_count writes each block's live count, and
+// k_live_perm adds the counts of the blocks before its own to an in-block
+// scan (integer sums: exact, the order is deterministic).
+constexpr int kLiveBlock = 1024;
+
+__global__ __launch_bounds__(256) void k_live_count(const int64_t* __restrict__ y,
+                                                    const float* __restrict__ dlogp, int64_t Tn,
+                                                    int64_t V, int* __restrict__ blk) {
+  __shared__ int part[4];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int64_t t0 = int64_t(blockIdx.x) * kLiveBlock + tid * 4;
+  int v = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (t0 + q < Tn) v += token_live(y[t0 + q], dlogp[t0 + q], V) ? 1 : 0;
+  v = wave_incl_scan(v, lane);
+  if (lane == 63) part[tid >> 6] = v;
+  __syncthreads();
+  if (tid == 0) blk[blockIdx.x] = part[0] + part[1] + part[2] + part[3];
+}
+
+__global__ __launch_bounds__(256) void k_live_perm(const int64_t* __restrict__ y,
+                                                   const float* __restrict__ dlogp, int64_t Tn,
+                                                   int64_t V, const int* __restrict__ blk,
+                                                   int nblk, int* __restrict__ perm,
+                                                   int* __restrict__ nlive) {
+  __shared__ int part[4], before[4], total[4];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // live tokens in the blocks before this one, and in all blocks
+  int pre = 0, all = 0;
+  for (int k = tid; k < nblk; k += 256) {
+    const int c = blk[k];
+    all += c;
+    if (k < int(blockIdx.x)) pre += c;
+  }
+  pre = wave_incl_scan(pre, lane);
+  all = wave_incl_scan(all, lane);
+  if (lane == 63) {
+    before[w] = pre;
+    total[w] = all;
+  }
+  const int64_t t0 = int64_t(blockIdx.x) * kLiveBlock + tid * 4;
+  bool lv[4];
+  int own = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    lv[q] = t0 + q < Tn && token_live(y[t0 + q], dlogp[t0 + q], V);
+    own += lv[q] ? 1 : 0;
+  }
+  const int incl = wave_incl_scan(own, lane);
+  if (lane == 63) part[w] = incl;
+  __syncthreads();
+  const int n_live = total[0] + total[1] + total[2] + total[3];
+  const int live_before = before[0] + before[1] + before[2] + before[3];
+  int run = live_before + incl - own;          // live tokens before t0
+  for (int k = 0; k < w; ++k) run += part[k];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int64_t t = t0 + q;
+    if (t < Tn) {
+      // a dead token goes after all live ones, behind the dead tokens before it
+      const int64_t pos = lv[q] ? int64_t(run) : int64_t(n_live) + (t - run);
+      perm[pos] = int(t);
+    }
+    run += lv[q] ? 1 : 0;
+  }
+  if (blockIdx.x == 0 && tid == 0) nlive[0] = n_live;
 }
 
 // Zeros, grid-stride (the grid is capped; n may exceed 2^31 elements).
@@ -861,15 +1028,6 @@ __host__ __device__ inline int64_t rank_words(int64_t T) { return (T + 31) / 32;
 // k_scan_sums writes each block's total, k_scan_apply adds the totals of the
 // blocks before its own to an in-block scan.  Integer sums: exact.
 constexpr int kScanBlock = 1024;
-
-__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int u = __shfl_up(v, o, 64);
-    if (lane >= o) v += u;
-  }
-  return v;
-}
 
 __global__ __launch_bounds__(256) void k_scan_sums(const int* __restrict__ counts, int64_t V,
                                                    int* __restrict__ sums) {
@@ -1223,13 +1381,23 @@ __global__ __launch_bounds__(kThreads, 1) void k_fwd_logits_lse(Operand A, Opera
                                                                       lds, kGroupVT);
 }
 // T: the inputs' type, TP: the operand's (see EpiProbs)
+// A tile of positions past the live tokens only writes its zero rows.
 template <typename T, typename TP>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B, int64_t K,
                                                            int nTm, int nTn,
                                                            EpiProbs<T, TP> epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
-  gemm_body<T, Lay::KMajor, Lay::KMajor, EpiProbs<T, TP>, 2, kDeepFwdA>(A, B, K, nTm, nTn, epi,
-                                                                        lds, kGroupVT);
+  int tm, tn;
+  tile_of(blockIdx.x, nTm, nTn, kGroupVT, tm, tn);
+  const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
+  if (epi.dead_tile(n0)) {
+    epi.zero_tile(m0, n0);
+    return;
+  }
+  const auto pre = epi.prologue(m0, n0);
+  Acc acc;
+  gemm_mainloop<T, Lay::KMajor, Lay::KMajor, 2, kDeepFwdA>(A, B, m0, n0, K, lds, acc);
+  epi.epilogue(acc, tm, tn, m0, n0, lds, lds + kLdsGemm, pre);
 }
 // TG: the contraction's operand type (the operand panels and W^T), T: the
 // weight's, read by the one-hot part.  Groups of 4 token tile rows walk the
@@ -1396,6 +1564,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   // magnitude bounds of the scaled operands: [0] max |dlogp|, [1] max |H|,
   // [2 + c] max |W| over chunk c
   unsigned* bounds = kScaled ? cv.take<unsigned>(size_t(2 + nchunks)) : nullptr;
+  // recompute only: the live-first token order and H's rows in it
+  const int nlb = int(cdiv(Tn, kLiveBlock));
+  int* perm = cacheE ? nullptr : cv.take<int>(Tn);
+  int* live_blk = cacheE ? nullptr : cv.take<int>(size_t(nlb) + 1);   // [nlb]: live tokens
+  T* Hp = cacheE ? nullptr : cv.take<T>(size_t(Tn) * d);
   int ncu = 0, dev = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -1404,12 +1577,19 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   const int nTd = int(cdiv(d, kBN));
 
   const double es = sizeof(T);
+  if (!cacheE) {
+    ProfScope ps_(s, "logprob_bwd_live_order", 0.0, 24.0 * Tn);
+    hipLaunchKernelGGL(k_live_count, dim3(nlb), dim3(256), 0, s, y, dlogp, Tn, V, live_blk);
+    hipLaunchKernelGGL(k_live_perm, dim3(nlb), dim3(256), 0, s, y, dlogp, Tn, V, live_blk, nlb,
+                       perm, live_blk + nlb);
+  }
   if (!cacheE || dW) {   // read by the softmax contraction and by H^T
-    ProfScope ps_(s, "logprob_bwd_live_rows", 0.0, 2.0 * es * double(Tn) * d + 12.0 * Tn);
+    ProfScope ps_(s, "logprob_bwd_live_rows", 0.0,
+                  (cacheE ? 2.0 : 3.0) * es * double(Tn) * d + 12.0 * Tn);
     const int64_t chunks = Tn * d / (16 / int64_t(sizeof(T)));
     if (cdiv(chunks, int64_t(256)) > int64_t(0x7fffffff)) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_live_rows<T>, dim3(unsigned(cdiv(chunks, int64_t(256)))), dim3(256), 0,
-                       s, H, y, dlogp, Tn, d, V, Hm);
+                       s, H, y, dlogp, Tn, d, V, Hm, perm, Hp);
   }
   if (kScaled) {
     ProfScope ps_(s, "logprob_bwd_bounds", 0.0, 4.0 * Tn);
@@ -1458,11 +1638,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                          dW ? counts + Vs : nullptr, bounds);
     } else {
       // tile rows: chunk columns (up to the padded width ldc), tile columns: tokens
-      Operand A{Wc, d, width, d}, B{Hm, d, Tn, d};
+      Operand A{Wc, d, width, d}, B{Hp, d, Tn, d};   // B: H's rows in the live-first order
       if (!operand_in_bounds<T, Lay::KMajor>(A, wc_bytes) ||
           !operand_in_bounds<T, Lay::KMajor>(B, size_t(Tn) * d * sizeof(T)) || ldc > ld)
         return hipErrorInvalidValue;
-      EpiProbs<T, TP> epi{y, lse, dlogp, Tn, V, width, ldc, pld, P, bounds};
+      EpiProbs<T, TP> epi{y, lse, dlogp, Tn, V, width, ldc, pld, P, bounds, perm, live_blk + nlb};
       const int nTv = int(cdiv(ldc, kBM)), nTt = int(cdiv(Tn, kBN));
       ProfScope ps_(s, "logprob_bwd_probs", 2.0 * Tn * d * width,
                     es * (double(Tn) * d + double(width) * d + double(Tn) * width) + 16.0 * Tn);
@@ -1607,6 +1787,9 @@ size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += align_up(tail_slot_floats(d, std::min(chunk, V)) * 4, kWsAlign);
   n += onehot_seg_bytes(T, d);
   if (dt == MC_BF16) n += align_up(size_t(2 + cdiv(V, chunk)) * 4, kWsAlign);   // bounds
+  n += align_up(size_t(T) * 4, kWsAlign);                                      // order
+  n += align_up(size_t(cdiv(T, kLiveBlock) + 1) * 4, kWsAlign);                // its counts
+  n += align_up(size_t(T) * size_t(d) * es, kWsAlign);   // H's rows in that order
   return n;
 }
 

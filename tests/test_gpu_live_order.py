@@ -1,0 +1,110 @@
+"""The recompute backward's live-first token order, on the GPU, against the
+oracle.
+
+The softmax contraction of mc_logprob_bwd visits the tokens whose operand
+row can be nonzero (nonzero dlogp, target in [0, V)) first; a 256-token
+tile of positions holding none of them writes its zero rows without the
+contraction.  Every result must be the one of the plain definition:
+dH and dW against the oracle for live sets of every size around the tile
+edges (none, one, 255, 256, 257, all, scattered, only in the ragged last
+tile, ignored targets with nonzero dlogp), exact zero rows of dH for the
+dead tokens, and dH's live rows bit-identical to a call on the live tokens
+alone (each row's logits, operand and contraction over the vocabulary do
+not depend on where the token sits in the order)."""
+import numpy as np
+import pytest
+
+import oracle
+from _cases import GRAD_RTOL, PTERM_RTOL_F16, device_tensors, rel_fro
+from workloads import make_tensors_numpy, scaled_config
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+T, D, V = 1300, 128, 700     # 5 whole token tiles and a ragged sixth; a ragged vocabulary tile
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_04847_amd as mc
+    mc.load_library()
+
+
+def _live_set(kind, rng):
+    live = np.zeros(T, dtype=bool)
+    if kind == "one":
+        live[T - 7] = True
+    elif kind in ("255", "256", "257"):
+        live[rng.choice(T, size=int(kind), replace=False)] = True
+    elif kind == "all":
+        live[:] = True
+    elif kind == "scattered":
+        live = rng.random(T) < 0.3
+    elif kind == "ragged_tail":
+        live[5 * 256 + 3: T - 2] = True
+    elif kind == "spans":
+        # long runs, like masked prompt / tool-output spans of packed sequences
+        for a, b in ((0, 90), (300, 700), (1100, 1130)):
+            live[a:b] = True
+    return live
+
+
+KINDS = ["none", "one", "255", "256", "257", "all", "scattered", "ragged_tail", "spans",
+         "ignored"]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind", KINDS)
+def test_live_first_order(kind, dtype):
+    import paper_2606_04847_amd as mc
+    cfg = scaled_config(1, d=D, V=V, dtype=dtype, seed=61)
+    Hn, Wn, hb, wb = make_tensors_numpy(cfg, T)
+    rng = np.random.default_rng(62 + KINDS.index(kind))
+    y = rng.integers(0, V, size=T).astype(np.int64)
+    dlogp = (rng.standard_normal(T) / T).astype(np.float32)
+    if kind == "ignored":
+        # a third of the tokens ignored (-1 or V) with nonzero dlogp: dead
+        # all the same; a fifth of the rest with zero dlogp
+        ign = rng.random(T) < 0.33
+        y[ign] = np.where(rng.random(int(ign.sum())) < 0.5, -1, V)
+        dlogp[~ign & (rng.random(T) < 0.2)] = 0.0
+        live = ~ign & (dlogp != 0.0)
+    else:
+        live = _live_set(kind, rng)
+        dlogp[~live] = 0.0
+    case = dict(H=Hn, W=Wn, hb=hb, wb=wb, y=y)
+    H, W, yd = device_tensors(case)
+    dl = torch.from_numpy(dlogp).cuda()
+    _, lse = mc.logprob_fwd(H, W, yd)
+    dH, dW = mc.logprob_bwd(H, W, yd, lse, dl)
+    torch.cuda.synchronize()
+    yc = np.where((y >= 0) & (y < V), y, -1)
+    _, lse_o = oracle.logprob_fwd(Hn, Wn, yc)
+    dl64 = dlogp.astype(np.float64)
+    dH_o, dW_o = oracle.logprob_bwd(Hn, Wn, yc, lse_o, dl64)
+    dH_g = dH.double().cpu().numpy()
+    dW_g = dW.double().cpu().numpy()
+    assert np.all(dH_g[~live] == 0.0), (kind, dtype)
+    if not live.any():
+        assert not dH_g.any() and not dW_g.any(), (kind, dtype)
+        return
+    assert rel_fro(dH_g, dH_o) <= GRAD_RTOL, (kind, dtype)
+    assert rel_fro(dW_g, dW_o) <= GRAD_RTOL, (kind, dtype)
+    # the softmax parts alone (the one-hot parts are exact in fp32)
+    H64, W64 = Hn.astype(np.float64), Wn.astype(np.float64)
+    g = np.where(yc >= 0, dl64, 0.0)
+    onehot_h = g[:, None] * W64[np.maximum(yc, 0)]
+    onehot_w = np.zeros_like(dW_o)
+    np.add.at(onehot_w, np.maximum(yc, 0), g[:, None] * H64)
+    assert rel_fro(dH_g - onehot_h, dH_o - onehot_h) <= PTERM_RTOL_F16, (kind, dtype)
+    assert rel_fro(dW_g - onehot_w, dW_o - onehot_w) <= PTERM_RTOL_F16, (kind, dtype)
+    if kind != "ignored":
+        # the live tokens alone, in one call: the same rows of dH, bit for bit
+        idx = torch.from_numpy(np.flatnonzero(live)).cuda()
+        dH_l, _ = mc.logprob_bwd(H[idx].contiguous(), W, yd[idx].contiguous(),
+                                 lse[idx].contiguous(), dl[idx].contiguous())
+        torch.cuda.synchronize()
+        assert torch.equal(dH[idx], dH_l), (kind, dtype)
