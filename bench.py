@@ -60,31 +60,33 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "ea321adf5abee0df12a173fe82070a6219f17797607139f563820325c82f8065",
+        "b3b6f847582f8c2ccd3411ed2c9c63ac25e3dce72510aed38c3a5ff2b45da58f",
     "read_bytes_per_launch": {
-        "logprob_fwd_gemm": 38652817024,
-        "logprob_fwd_merge": 78110848,
-        "logprob_bwd_live_rows": 36080192,
-        "logprob_bwd_bounds": 83328,
-        "logprob_bwd_bucket": 5812032,
-        "logprob_bwd_probs": 32892538624,
-        "logprob_bwd_transpose": 689528000,
-        "logprob_bwd_dhidden": 30113924864,
-        "logprob_bwd_dweight": 31390125120,
-        "logprob_bwd_onehot_dw": 107582080,
+        "logprob_fwd_gemm": 39494273088,
+        "logprob_fwd_merge": 78110784,
+        "logprob_bwd_live_order": 431104,
+        "logprob_bwd_live_rows": 37180672,
+        "logprob_bwd_bounds": 82752,
+        "logprob_bwd_bucket": 5815424,
+        "logprob_bwd_probs": 19437369472,
+        "logprob_bwd_transpose": 689529824,
+        "logprob_bwd_dhidden": 40123035584,
+        "logprob_bwd_dweight": 9985464256,
+        "logprob_bwd_onehot_dw": 107591744,
         "rl_loss": 340480,
     },
     "write_bytes_per_launch": {
-        "logprob_fwd_gemm": 78367616,
+        "logprob_fwd_gemm": 78367584,
         "logprob_fwd_merge": 131072,
+        "logprob_bwd_live_order": 66912,
         "logprob_bwd_live_rows": 134217728,
         "logprob_bwd_bounds": 32,
-        "logprob_bwd_bucket": 2647328,
-        "logprob_bwd_probs": 4979009664,
-        "logprob_bwd_transpose": 689438784,
+        "logprob_bwd_bucket": 2647360,
+        "logprob_bwd_probs": 1322802816,
+        "logprob_bwd_transpose": 689438720,
         "logprob_bwd_dhidden": 268435456,
-        "logprob_bwd_dweight": 2556428416,
-        "logprob_bwd_onehot_dw": 69889408,
+        "logprob_bwd_dweight": 2556428288,
+        "logprob_bwd_onehot_dw": 69888160,
         "rl_loss": 80896,
     },
 }
@@ -295,12 +297,13 @@ def recompute_cols(y, dlogp, V):
     return min(int(y.numel()), -(-n // 256) * 256)
 
 
-def count_recompute(res, cols, d, V):
-    """Replace the library's dense figure for the softmax contraction by the
-    FLOPs it executes (cols token columns per launch)."""
+def count_recompute(res, cols, T):
+    """Scale the library's dense figure for the softmax contraction (2 T d
+    width per launch, one launch per vocabulary chunk) to the FLOPs it
+    executes: cols of the T token columns."""
     k = res["kernels"].get("logprob_bwd_probs")
     if k:
-        k["flops"] = k["launches"] * 2.0 * cols * d * V
+        k["flops"] *= cols / T
 
 
 def summary(res, T, counted, executed):
@@ -402,7 +405,7 @@ def summarize(path, only=None):
                     "k_cache_to_probs", "k_transpose", "k_onehot_seg", "k_onehot_join", "k_lse_merge",
                     "k_shard_partial", "k_tail_reduce", "k_surrogate", "k_seq_stats",
                     "k_bucket_rank", "k_bucket_fill", "k_hist", "k_scan", "k_fill_i32", "k_bound_abs",
-                    "k_live_rows",
+                    "k_live_rows", "k_live_count", "k_live_perm",
                     "k_count", "k_finish", "k_loss_init", "copyBuffer"):
             if key in name:
                 return key
@@ -541,7 +544,7 @@ def main():
                                  workspace=ws_b)
         res = time_steps(step, args.steps, args.warmup, sampler, flush, args.flush_reps)
         cols = recompute_cols(y, dlogp, V)
-        count_recompute(res, cols, d, Vs)
+        count_recompute(res, cols, T)
         summ = summary(res, T, 6.0 * T * d * Vs, 6.0 * T * d * Vs + 2.0 * cols * d * Vs)
         summ["recompute_token_cols"] = cols
         config.update(workload=config["workload"] + f"; vocabulary shard of {Vs} rows (V/8)",
@@ -603,7 +606,7 @@ def main():
             executed = 6.0 * T * d * V
             if name == "recompute":
                 cols = recompute_cols(y, out["dlogp"], V)
-                count_recompute(res, cols, d, V)
+                count_recompute(res, cols, T)
                 executed += 2.0 * cols * d * V
             summ = summary(res, T, 6.0 * T * d * V, executed)
             if name == "recompute":

@@ -6,6 +6,7 @@
 // by a deterministic bucketed scatter).
 #include <hip/hip_runtime.h>
 
+#include <numeric>
 #include <type_traits>
 
 #include "mc_internal.hpp"
@@ -82,13 +83,10 @@ __device__ __forceinline__ int panel_stage_off(int v, int t) {
 // stored, from one base address per thread: as a loop of read, wait, store
 // (with 64-bit address arithmetic in each step) this took most of the
 // cache's cost in the forward.
-// With `rowmap` set, staged token row n0 + tl goes to row rowmap[n0 + tl] of
-// the panels (a 128-byte row stays one contiguous store).
 template <typename TP>   // a 2-byte element type
 __device__ __forceinline__ void store_staged_panels(const char* lds, TP* P, int64_t m0,
                                                     int64_t n0, int64_t Tn, int64_t ld,
-                                                    int64_t pld,
-                                                    const int* __restrict__ rowmap = nullptr) {
+                                                    int64_t pld) {
   constexpr int64_t kPanel = 64;
   constexpr int kRows = kThreads / 8;            // token rows per round
   constexpr int kRounds = 256 / kRows;           // rounds per panel
@@ -104,23 +102,6 @@ __device__ __forceinline__ void store_staged_panels(const char* lds, TP* P, int6
                                                     ((it % kRounds) * kRows + r0) * 128 + sw);
     v[it] = swap ? u32x4{x[2], x[3], x[0], x[1]} : x;
   }
-  if (rowmap != nullptr) {
-    int64_t row[kRounds];
-#pragma unroll
-    for (int rd = 0; rd < kRounds; ++rd) {
-      const int64_t j = n0 + rd * kRows + r0;
-      row[rd] = j < Tn ? int64_t(rowmap[j]) : -1;
-    }
-    TP* const base = P + (m0 / kPanel) * pld * kPanel + ch * 8;
-#pragma unroll
-    for (int it = 0; it < kIters; ++it) {
-      const int pn = it / kRounds, rd = it % kRounds;
-      if (row[rd] >= 0 && m0 + pn * kPanel < ld)
-        __builtin_nontemporal_store(
-            v[it], reinterpret_cast<u32x4*>(base + pn * pld * kPanel + row[rd] * kPanel));
-    }
-    return;
-  }
   TP* const base = P + (m0 / kPanel) * pld * kPanel + (n0 + r0) * kPanel + ch * 8;
 #pragma unroll
   for (int it = 0; it < kIters; ++it) {
@@ -129,34 +110,6 @@ __device__ __forceinline__ void store_staged_panels(const char* lds, TP* P, int6
       __builtin_nontemporal_store(
           v[it], reinterpret_cast<u32x4*>(base + pn * pld * kPanel +
                                           int64_t((it % kRounds) * kRows) * kPanel));
-  }
-}
-
-// Zero rows of the panels for the tile's 256 token positions n0 .. n0 + 255
-// (row rowmap[j] for position j < Tn) and its 256 chunk columns from m0
-// (panels below ld): 16-byte non-temporal stores, eight lanes per 128-byte
-// row, any element size.
-template <typename TP>
-__device__ __forceinline__ void store_zero_panels(TP* P, int64_t m0, int64_t n0, int64_t Tn,
-                                                  int64_t ld, int64_t pld,
-                                                  const int* __restrict__ rowmap) {
-  constexpr int64_t kPanel = 128 / sizeof(TP);
-  constexpr int kPanels = int(256 / kPanel);     // panels per tile
-  constexpr int kRows = kThreads / 8;
-  constexpr int kRounds = 256 / kRows;
-  const int ch = threadIdx.x & 7, r0 = threadIdx.x >> 3;
-  const u32x4 z = {0u, 0u, 0u, 0u};
-  TP* const base = P + (m0 / kPanel) * pld * kPanel + ch * (16 / int(sizeof(TP)));
-#pragma unroll
-  for (int rd = 0; rd < kRounds; ++rd) {
-    const int64_t j = n0 + rd * kRows + r0;
-    if (j >= Tn) continue;
-    const int64_t row = rowmap[j];
-#pragma unroll
-    for (int pn = 0; pn < kPanels; ++pn)
-      if (m0 + pn * kPanel < ld)
-        __builtin_nontemporal_store(
-            z, reinterpret_cast<u32x4*>(base + pn * pld * kPanel + row * kPanel));
   }
 }
 
@@ -524,11 +477,11 @@ struct EpiProbs {
                                    // width; pld: padded token count
   TP* P;                           // panel layout (see Lay::TileTK)
   const unsigned* bound;           // max |dlogp| (fp16 operand) or null
-  // Tile columns are positions in the live-first token order: the B operand
-  // holds the row of token perm[j] at position j, and P~'s row perm[j] is
-  // written.  Positions from *nlive on hold tokens whose P~ rows are zero, so
-  // a tile whose first position is past them writes its zero rows without
-  // the contraction.  Null: positions are tokens, every tile is computed.
+  // Tile columns, and P~'s rows, are positions in the live-first token
+  // order (see LiveOrder): the B operand holds the row of token perm[j] at
+  // position j.  A tile whose first position is at or past *nlive has no
+  // live token and writes nothing: the contractions that read P~ read its
+  // rows from *nlive on as zeros.  Null: positions are tokens.
   const int* perm;
   const int* nlive;
   static constexpr int64_t kPanel = 128 / sizeof(TP);
@@ -536,12 +489,9 @@ struct EpiProbs {
   __device__ __forceinline__ int64_t token(int64_t j) const {
     return perm != nullptr ? int64_t(perm[j]) : j;
   }
-  // No live token at the tile's positions (wave-uniform).
+  // No live token at the tile's positions (workgroup-uniform).
   __device__ __forceinline__ bool dead_tile(int64_t n0) const {
     return nlive != nullptr && n0 >= int64_t(*nlive);
-  }
-  __device__ __forceinline__ void zero_tile(int64_t m0, int64_t n0) const {
-    store_zero_panels(P, m0, n0, Tn, ld, pld, perm);
   }
 
   // lse_t log2(e) and -dlogp_t (0 for ignored tokens) of the tokens of this
@@ -584,9 +534,6 @@ struct EpiProbs {
       // are written without evaluating the exponentials.
       const bool live = __builtin_amdgcn_ballot_w64(pos < Tn && gs != 0.0f) != 0;
       if (pos >= Tn) continue;
-      // the 4-byte operand's direct stores need the token (not held across
-      // the main loop: registers)
-      const int64_t tok = sizeof(TP) == 2 ? 0 : token(pos);
 #pragma unroll
       for (int i = 0; i < kTM; ++i) {
         {
@@ -607,7 +554,7 @@ struct EpiProbs {
                 __builtin_bit_cast(u32x2, __builtin_convertvector(p, tp4));
           } else {
             const int64_t c = m0 + vr;
-            TP* dst = P + (c / kPanel) * pld * kPanel + tok * kPanel + c % kPanel;
+            TP* dst = P + (c / kPanel) * pld * kPanel + pos * kPanel + c % kPanel;
             *reinterpret_cast<f32x4*>(dst) = p;
           }
         }
@@ -628,7 +575,7 @@ struct EpiProbs {
       values<false>(acc, lds, lane, wm, wn, pre, vlim, llim, m0, n0);
     if constexpr (sizeof(TP) == 2) {
       __syncthreads();
-      store_staged_panels(lds, P, m0, n0, Tn, ld, pld, perm);
+      store_staged_panels(lds, P, m0, n0, Tn, ld, pld);
     }
   }
 };
@@ -651,6 +598,9 @@ struct EpiDH {
   // two: exact).  Null: unscaled operands.
   const unsigned* bound_p;
   const unsigned* bound_w;
+  // Tile rows are positions in the live-first token order: row r of the tile
+  // is dH's row perm[r].  Null: rows are tokens.
+  const int* perm;
 
   struct Pre {};
   __device__ __forceinline__ Pre prologue(int64_t, int64_t) const { return Pre{}; }
@@ -696,12 +646,13 @@ struct EpiDH {
         f32x4 v = *reinterpret_cast<const f32x4*>(lds + rl * (kChunks * 16) +
                                                   ((c4 ^ (rl & 15)) << 4));
         v = us(v);
-        float* o = C + r * ldc + c;
+        const int64_t t = perm != nullptr ? int64_t(perm[r]) : r;
+        float* o = C + t * ldc + c;
         if (accumulate) v += *reinterpret_cast<const f32x4*>(o);
         if (W != nullptr) {
-          const int64_t yy = y[r] - v_off;
+          const int64_t yy = y[t] - v_off;
           if (yy >= 0 && yy < Vs) {
-            const float g = dlogp[r];
+            const float g = dlogp[t];
             const T* w = W + yy * ldc + c;
 #pragma unroll
             for (int k = 0; k < 4; ++k) v[k] += g * float(w[k]);
@@ -888,17 +839,15 @@ __device__ __forceinline__ bool token_live(int64_t yy, float g, int64_t V) {
 // tokens, so z there only feeds products by zero), while the MFMAs on the
 // zero rows draw less power, and these contractions run power-limited.
 //
-// With `perm` set (the recompute backward), thread i handles chunk i of the
-// row at position j = i / cpr of the live-first order (k_live_perm): it
-// writes the chunk to row j of Hp and to row perm[j] of Hm, so each chunk
-// of H is read once.
+// With `perm` set (the recompute backward), row j of Hm is that of the token
+// perm[j] at position j of the live-first order (k_live_perm).
 template <typename T>
 __global__ __launch_bounds__(256) void k_live_rows(const T* __restrict__ H,
                                                    const int64_t* __restrict__ y,
                                                    const float* __restrict__ dlogp, int64_t Tn,
-                                                   int64_t d, int64_t V, T* __restrict__ Hm,
+                                                   int64_t d, int64_t V,
                                                    const int* __restrict__ perm,
-                                                   T* __restrict__ Hp) {
+                                                   T* __restrict__ Hm) {
   constexpr int CE = 16 / sizeof(T);   // elements per 16-byte chunk (d is a multiple)
   const int64_t cpr = d / CE;
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -907,8 +856,7 @@ __global__ __launch_bounds__(256) void k_live_rows(const T* __restrict__ H,
   const int64_t t = perm != nullptr ? int64_t(perm[j]) : j;
   u32x4 v = {0u, 0u, 0u, 0u};
   if (token_live(y[t], dlogp[t], V)) v = reinterpret_cast<const u32x4*>(H)[t * cpr + c];
-  reinterpret_cast<u32x4*>(Hm)[t * cpr + c] = v;
-  if (perm != nullptr) reinterpret_cast<u32x4*>(Hp)[i] = v;
+  reinterpret_cast<u32x4*>(Hm)[i] = v;
 }
 
 // Live-first order of the tokens for the recompute backward: the live tokens
@@ -1381,7 +1329,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_fwd_logits_lse(Operand A, Opera
                                                                       lds, kGroupVT);
 }
 // T: the inputs' type, TP: the operand's (see EpiProbs)
-// A tile of positions past the live tokens only writes its zero rows.
+// A tile of positions past the live tokens exits at once.
 template <typename T, typename TP>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B, int64_t K,
                                                            int nTm, int nTn,
@@ -1390,10 +1338,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B,
   int tm, tn;
   tile_of(blockIdx.x, nTm, nTn, kGroupVT, tm, tn);
   const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
-  if (epi.dead_tile(n0)) {
-    epi.zero_tile(m0, n0);
-    return;
-  }
+  if (epi.dead_tile(n0)) return;
   const auto pre = epi.prologue(m0, n0);
   Acc acc;
   gemm_mainloop<T, Lay::KMajor, Lay::KMajor, 2, kDeepFwdA>(A, B, m0, n0, K, lds, acc);
@@ -1404,12 +1349,31 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B,
 // hidden dimensions (measured against 8 and 16 with the current copy
 // schedule: 0.18 ms faster than 8).
 constexpr int kGroupDH = 4;
+// With `nlive` set (the live-first order), the operand's rows from *nlive on
+// are read as zeros (the copies take the out-of-range offset): they belong
+// to tokens with zero gradient rows and were never written.  Every tile and
+// every MFMA still runs.  The live rows then sit in the first token tile
+// rows, which the XCD-aware map would hand to the first XCDs alone (each XCD
+// takes a contiguous run of tile rows); token tile rows are therefore
+// visited as tm * stride mod nTm (stride coprime to nTm), which deals the
+// live rows out to every XCD and every round.
 template <typename TG, typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand B, int64_t K,
-                                                             int nTm, int nTn, EpiDH<T> epi) {
+                                                             int nTm, int nTn, EpiDH<T> epi,
+                                                             const int* nlive, int stride) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
-  gemm_body<TG, Lay::TileTK, Lay::KMajor, EpiDH<T>, 2, kDeepDhA>(A, B, K, nTm, nTn, epi, lds,
-                                                                 kGroupDH);
+  int tm, tn;
+  tile_of(blockIdx.x, nTm, nTn, kGroupDH, tm, tn);
+  tm = int((int64_t(tm) * stride) % nTm);
+  const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
+  Operand a = A;
+  if (nlive != nullptr) {
+    const int64_t nl = *nlive;
+    if (nl < a.rows) a.rows = nl;
+  }
+  Acc acc;
+  gemm_mainloop<TG, Lay::TileTK, Lay::KMajor, 2, kDeepDhA>(a, B, m0, n0, K, lds, acc);
+  epi.epilogue(acc, tm, tn, m0, n0, lds, lds + kLdsGemm);
 }
 // dW^T = H^T P~ : tile rows are hidden dimensions (A = H^T, along the
 // tokens), tile columns vocabulary entries (B = the operand panels read
@@ -1421,10 +1385,13 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand 
 constexpr int kGroupDW = 4;
 // Workgroups past ts.full compute K slices of the last ts.rem tiles into
 // 256 x 256 fp32 slots (stored [column][row]) for k_tail_reduce.
+// With `nlive` set, both operands' K (token positions) from *nlive on is
+// read as zeros, as in k_bwd_dhidden; the K loop still covers every token.
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand B, int64_t K,
                                                              int nTm, int nTn, EpiStoreT epi,
-                                                             TailSplit ts, float* slots) {
+                                                             TailSplit ts, float* slots,
+                                                             const int* nlive) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
   const int bid = blockIdx.x;
   int tm, tn, j = -1;
@@ -1439,6 +1406,13 @@ __global__ __launch_bounds__(kThreads, 1) void k_bwd_dweight(Operand A, Operand 
     k = K - k0 < ts.ks ? K - k0 : ts.ks;
     a = k_slice<T, Lay::KMajor>(A, k0, k);
     b = k_slice<T, Lay::TileVT>(B, k0, k);
+  }
+  if (nlive != nullptr) {
+    const int64_t k0 = j < 0 ? 0 : int64_t(j % ts.splits) * ts.ks;
+    const int64_t nl = int64_t(*nlive) - k0;
+    const int64_t lim = nl < 0 ? 0 : (nl < k ? nl : k);
+    a.K = lim;
+    b.K = lim;
   }
   const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
   Acc acc;
@@ -1531,6 +1505,15 @@ hipError_t fwd_impl(const T* H, const T* W, const int64_t* y, int64_t Tn, int64_
 // T: the inputs' type; TP: the type of the operand and of the transposes,
 // fp16 (power-of-two scaled, see probs_shift) for bf16 inputs, with or
 // without a cache (the cache is then fp16 too), T otherwise.
+// A stride near n / kXcds that is coprime to n (so tm -> tm * stride mod n
+// permutes the tile rows), 1 for n below 2 kXcds.
+inline int row_stride(int n) {
+  if (n < 2 * kXcds) return 1;
+  int st = n / kXcds;
+  while (std::gcd(st, n) != 1) ++st;
+  return st;
+}
+
 template <typename T, typename TP>
 hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                     const float* dlogp, int64_t Tn, int64_t d, int64_t Vs, int64_t v_off,
@@ -1549,7 +1532,9 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   TP* P = cacheE ? cacheE : cv.take<TP>(size_t(pld) * ld);
   TP* Wt = cv.take<TP>(size_t(d) * ld);    // [d x chunk] transpose of W's chunk rows
   TP* Ht = cv.take<TP>(size_t(d) * pld);   // [d x T] transpose of H
-  T* Hm = cv.take<T>(size_t(Tn) * d);      // H with the dead tokens' rows zeroed
+  // H with the dead tokens' rows zeroed, in the live-first order (recompute
+  // pair) or in token order (cached pair)
+  T* Hm = cv.take<T>(size_t(Tn) * d);
   int* counts = cv.take<int>(Vs + 1);   // counts[Vs]: live tokens
   int* cursor = cv.take<int>(Vs);
   unsigned* rank_bits = cv.take<unsigned>(size_t(rank_slots(Tn) * rank_words(Tn)));
@@ -1564,11 +1549,12 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   // magnitude bounds of the scaled operands: [0] max |dlogp|, [1] max |H|,
   // [2 + c] max |W| over chunk c
   unsigned* bounds = kScaled ? cv.take<unsigned>(size_t(2 + nchunks)) : nullptr;
-  // recompute only: the live-first token order and H's rows in it
+  // recompute only: the live-first token order (position -> token) and the
+  // live counts of its blocks, followed by the number of live tokens
   const int nlb = int(cdiv(Tn, kLiveBlock));
   int* perm = cacheE ? nullptr : cv.take<int>(Tn);
-  int* live_blk = cacheE ? nullptr : cv.take<int>(size_t(nlb) + 1);   // [nlb]: live tokens
-  T* Hp = cacheE ? nullptr : cv.take<T>(size_t(Tn) * d);
+  int* live_blk = cacheE ? nullptr : cv.take<int>(size_t(nlb) + 1);
+  const int* nlive = cacheE ? nullptr : live_blk + nlb;
   int ncu = 0, dev = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -1584,12 +1570,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                        perm, live_blk + nlb);
   }
   if (!cacheE || dW) {   // read by the softmax contraction and by H^T
-    ProfScope ps_(s, "logprob_bwd_live_rows", 0.0,
-                  (cacheE ? 2.0 : 3.0) * es * double(Tn) * d + 12.0 * Tn);
+    ProfScope ps_(s, "logprob_bwd_live_rows", 0.0, 2.0 * es * double(Tn) * d + 12.0 * Tn);
     const int64_t chunks = Tn * d / (16 / int64_t(sizeof(T)));
     if (cdiv(chunks, int64_t(256)) > int64_t(0x7fffffff)) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_live_rows<T>, dim3(unsigned(cdiv(chunks, int64_t(256)))), dim3(256), 0,
-                       s, H, y, dlogp, Tn, d, V, Hm, perm, Hp);
+                       s, H, y, dlogp, Tn, d, V, perm, Hm);
   }
   if (kScaled) {
     ProfScope ps_(s, "logprob_bwd_bounds", 0.0, 4.0 * Tn);
@@ -1638,11 +1623,11 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                          dW ? counts + Vs : nullptr, bounds);
     } else {
       // tile rows: chunk columns (up to the padded width ldc), tile columns: tokens
-      Operand A{Wc, d, width, d}, B{Hp, d, Tn, d};   // B: H's rows in the live-first order
+      Operand A{Wc, d, width, d}, B{Hm, d, Tn, d};   // B: H's rows in the live-first order
       if (!operand_in_bounds<T, Lay::KMajor>(A, wc_bytes) ||
           !operand_in_bounds<T, Lay::KMajor>(B, size_t(Tn) * d * sizeof(T)) || ldc > ld)
         return hipErrorInvalidValue;
-      EpiProbs<T, TP> epi{y, lse, dlogp, Tn, V, width, ldc, pld, P, bounds, perm, live_blk + nlb};
+      EpiProbs<T, TP> epi{y, lse, dlogp, Tn, V, width, ldc, pld, P, bounds, perm, nlive};
       const int nTv = int(cdiv(ldc, kBM)), nTt = int(cdiv(Tn, kBN));
       ProfScope ps_(s, "logprob_bwd_probs", 2.0 * Tn * d * width,
                     es * (double(Tn) * d + double(width) * d + double(Tn) * width) + 16.0 * Tn);
@@ -1669,17 +1654,19 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
       // the one-hot part goes into the last chunk's epilogue
       const bool last = v0 + chunk >= Vs;
       EpiDH<T> epi{dH,      d,     Tn,    d, (v0 > 0 || (flags & MC_BWD_ACCUMULATE_DHIDDEN)) ? 1 : 0,
-                   last ? W : nullptr, y, dlogp, v_off, Vs, bounds, bound_w};
+                   last ? W : nullptr, y, dlogp, v_off, Vs, bounds, bound_w, perm};
       ProfScope ps_(s, "logprob_bwd_dhidden", 2.0 * Tn * d * (width + (last ? 1 : 0)),
                     es * (double(Tn) * width + double(width) * d) +
                         4.0 * Tn * d * (epi.accumulate ? 2 : 1) +
                         (last ? es * double(Tn) * d + 16.0 * Tn : 0.0));
       hipLaunchKernelGGL((k_bwd_dhidden<TP, T>), dim3(nTm * nTd),
-                         dim3(kThreads), 0, s, A, B, ldc, nTm, nTd, epi);
+                         dim3(kThreads), 0, s, A, B, ldc, nTm, nTd, epi, nlive,
+                         nlive != nullptr ? row_stride(nTm) : 1);
     }
     if (dW) {
-      // dW[chunk]^T (+)= H^T P~ : M = d, N = chunk columns, K = T, with H^T
-      // [d x pld] (made once) so that the M operand runs along K
+      // dW[chunk]^T (+)= H^T P~ : M = d, N = chunk columns, K = T (the
+      // positions of P~'s rows), with H^T [d x pld] (made once, from Hm: in
+      // the same order as P~'s rows) so that the M operand runs along K
       if (v0 == 0) {
         ProfScope ps_(s, "logprob_bwd_transpose", 0.0, 2.0 * es * double(Tn) * d);
         unsigned* const bound_h = kScaled ? bounds + 1 : nullptr;
@@ -1702,7 +1689,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                         4.0 * width * d * (epi.accumulate ? 2 : 1));
       const TailSplit ts = plan_tail(nTd * nTv, Tn, ncu);
       hipLaunchKernelGGL(k_bwd_dweight<TP>, dim3(ts.full + ts.rem * ts.splits), dim3(kThreads),
-                         0, s, A, B, Tn, nTd, nTv, epi, ts, slots);
+                         0, s, A, B, Tn, nTd, nTv, epi, ts, slots, nlive);
       if (ts.rem > 0)
         hipLaunchKernelGGL(k_tail_reduce, dim3(ts.rem, kBN / 4), dim3(256), 0, s, slots, ts, nTd,
                            nTv, epi.C, epi.ldc, epi.rows, epi.cols, epi.accumulate, epi.bound_p,
@@ -1789,7 +1776,6 @@ size_t bwd_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   if (dt == MC_BF16) n += align_up(size_t(2 + cdiv(V, chunk)) * 4, kWsAlign);   // bounds
   n += align_up(size_t(T) * 4, kWsAlign);                                      // order
   n += align_up(size_t(cdiv(T, kLiveBlock) + 1) * 4, kWsAlign);                // its counts
-  n += align_up(size_t(T) * size_t(d) * es, kWsAlign);   // H's rows in that order
   return n;
 }
 

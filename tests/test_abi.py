@@ -76,20 +76,19 @@ def test_workspace_sizes(lib):
     assert lib.mc_logprob_fwd_workspace_size(10, 60, 10, BF16) == 0      # invalid -> 0
     bw = lib.mc_logprob_bwd_workspace_size(16384, 4096, 151936, BF16)
     # the headline shape keeps its whole 2-byte softmax operand (one chunk),
-    # the transposes of W and H, two copies of H with the dead tokens' rows
-    # zeroed (in token order and in the live-first order), small index
-    # arrays, the fp32 slots of dW's split last round (at most 256 tiles of
-    # 256 x 256) and the one-hot scatter's two fp32 rows per segment of 16
-    # bucketed tokens
+    # the transposes of W and H, a copy of H with the dead tokens' rows
+    # zeroed (in the live-first token order), small index arrays, the fp32
+    # slots of dW's split last round (at most 256 tiles of 256 x 256) and the
+    # one-hot scatter's two fp32 rows per segment of 16 bucketed tokens
     def seg(T, d):
         return 2 * (-(-T // 16)) * d * 4
-    dense = (151936 * 16384 + 4096 * 151936 + 3 * 4096 * 16384) * 2
+    dense = (151936 * 16384 + 4096 * 151936 + 2 * 4096 * 16384) * 2
     assert dense + seg(16384, 4096) <= bw < dense + seg(16384, 4096) + (16 << 20) + (64 << 20)
     # larger problems are chunked under 8 GiB of softmax operand per chunk;
     # the W transpose covers one chunk
     big = lib.mc_logprob_bwd_workspace_size(65536, 4096, 248320, BF16)
     chunk = (8 << 30) // (65536 * 2)
-    assert big <= ((8 << 30) + (4096 * chunk + 3 * 4096 * 65536) * 2 + seg(65536, 4096)
+    assert big <= ((8 << 30) + (4096 * chunk + 2 * 4096 * 65536) * 2 + seg(65536, 4096)
                    + (32 << 20) + (64 << 20))
     assert lib.mc_rl_loss_workspace_size(100, 8, 2) > 0
     assert lib.mc_rl_loss_workspace_size(-1, 8, 2) == 0

@@ -34,3 +34,24 @@ def test_traffic_key_changes_with_any_kernel_source(tmp_path, monkeypatch):
         assert bench.sources_digest() != d0, name
         p.write_bytes(text)
     assert bench.sources_digest() == d0
+
+
+def test_recompute_flops_follow_the_live_tiles():
+    # the softmax contraction runs its MFMAs on the live tokens' 256-token
+    # tiles only; the executed figure scales the library's dense one (one
+    # launch per vocabulary chunk) by the share of token columns it covers
+    sys.path.insert(0, ROOT)
+    import bench
+    import torch
+    T, d, V = 1000, 64, 3000
+    y = torch.arange(T) % V
+    dl = torch.zeros(T)
+    dl[[3, 300, 700]] = 1.0
+    y[700] = -1                                    # ignored target: dead
+    assert bench.recompute_cols(y, dl, V) == 256   # 2 live tokens -> one tile
+    dl[:] = 1.0
+    assert bench.recompute_cols(y, dl, V) == T     # capped at T
+    dense = 2.0 * T * d * 1500                     # two chunks of 1500 rows
+    res = {"kernels": {"logprob_bwd_probs": {"flops": 4 * dense, "launches": 4}}}
+    bench.count_recompute(res, 256, T)
+    assert res["kernels"]["logprob_bwd_probs"]["flops"] == 4 * 2.0 * 256 * d * 1500

@@ -1,10 +1,12 @@
 """The recompute backward's live-first token order, on the GPU, against the
 oracle.
 
-The softmax contraction of mc_logprob_bwd visits the tokens whose operand
-row can be nonzero (nonzero dlogp, target in [0, V)) first; a 256-token
-tile of positions holding none of them writes its zero rows without the
-contraction.  Every result must be the one of the plain definition:
+The recompute backward puts the tokens whose operand row can be nonzero
+(nonzero dlogp, target in [0, V)) first.  Its softmax contraction skips the
+256-token tiles of positions holding none of them, and the two gradient
+contractions read the operand's rows past the live tokens as zeros (and
+store dH's rows through the order).  Every result must be the one of the
+plain definition:
 dH and dW against the oracle for live sets of every size around the tile
 edges (none, one, 255, 256, 257, all, scattered, only in the ragged last
 tile, ignored targets with nonzero dlogp), exact zero rows of dH for the
