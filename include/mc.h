@@ -188,10 +188,10 @@ mc_status_t mc_logprob_merge_shards(const float* partials, int32_t S, const int6
  * The softmax part is formed per vocabulary chunk as a transient operand in
  * the workspace; logits are recomputed, never stored.  They are recomputed
  * only where the gradient row can be nonzero: the tokens with dlogp_t != 0
- * and a target in [0, V) are taken first, and the operand rows of the others
- * are written as zeros, so this step costs in proportion to the live tokens
- * (the results are the same; both gradient contractions still run over all
- * T tokens).  For MC_BF16 inputs
+ * and a target in [0, V) are ordered first, and the operand rows of the
+ * others are read as zeros without being formed, so this step costs in
+ * proportion to the live tokens (the results are the same; both gradient
+ * contractions still run over all T tokens).  For MC_BF16 inputs
  * that operand and the transposed hidden and weight rows the contractions
  * read are fp16, each scaled by a power of two chosen from its magnitude
  * bound and unscaled exactly in fp32: each element of the softmax part is

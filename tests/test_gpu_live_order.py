@@ -24,7 +24,11 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-T, D, V = 1300, 128, 700     # 5 whole token tiles and a ragged sixth; a ragged vocabulary tile
+D, V = 128, 700   # a ragged vocabulary tile
+# 1300 tokens: 5 whole token tiles and a ragged sixth.  5000 tokens: 20 token
+# tile rows, which dH visits in a strided order (stride 3) once the live
+# tokens come first.
+T_SMALL, T_LARGE = 1300, 5000
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -35,7 +39,7 @@ def _gpu():
     mc.load_library()
 
 
-def _live_set(kind, rng):
+def _live_set(kind, rng, T):
     live = np.zeros(T, dtype=bool)
     if kind == "one":
         live[T - 7] = True
@@ -50,7 +54,7 @@ def _live_set(kind, rng):
     elif kind == "spans":
         # long runs, like masked prompt / tool-output spans of packed sequences
         for a, b in ((0, 90), (300, 700), (1100, 1130)):
-            live[a:b] = True
+            live[a * T // T_SMALL:b * T // T_SMALL] = True
     return live
 
 
@@ -58,13 +62,16 @@ KINDS = ["none", "one", "255", "256", "257", "all", "scattered", "ragged_tail", 
          "ignored"]
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("kind", KINDS)
-def test_live_first_order(kind, dtype):
+CASES = ([(k, dt, T_SMALL) for k in KINDS for dt in ("f32", "bf16")] +
+         [(k, "bf16", T_LARGE) for k in ("scattered", "spans", "ignored")])
+
+
+@pytest.mark.parametrize("kind,dtype,T", CASES)
+def test_live_first_order(kind, dtype, T):
     import paper_2606_04847_amd as mc
     cfg = scaled_config(1, d=D, V=V, dtype=dtype, seed=61)
     Hn, Wn, hb, wb = make_tensors_numpy(cfg, T)
-    rng = np.random.default_rng(62 + KINDS.index(kind))
+    rng = np.random.default_rng(62 + KINDS.index(kind) + T)
     y = rng.integers(0, V, size=T).astype(np.int64)
     dlogp = (rng.standard_normal(T) / T).astype(np.float32)
     if kind == "ignored":
@@ -75,7 +82,7 @@ def test_live_first_order(kind, dtype):
         dlogp[~ign & (rng.random(T) < 0.2)] = 0.0
         live = ~ign & (dlogp != 0.0)
     else:
-        live = _live_set(kind, rng)
+        live = _live_set(kind, rng, T)
         dlogp[~live] = 0.0
     case = dict(H=Hn, W=Wn, hb=hb, wb=wb, y=y)
     H, W, yd = device_tensors(case)
