@@ -60,33 +60,33 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "b3b6f847582f8c2ccd3411ed2c9c63ac25e3dce72510aed38c3a5ff2b45da58f",
+        "1e859ccee75bffaf3ca6424eb3e785ecce3db75a2927c30d06f5eb1b2fbc5cd3",
     "read_bytes_per_launch": {
-        "logprob_fwd_gemm": 39494273088,
+        "logprob_fwd_gemm": 38859475328,
         "logprob_fwd_merge": 78110784,
         "logprob_bwd_live_order": 431104,
-        "logprob_bwd_live_rows": 37180672,
-        "logprob_bwd_bounds": 82752,
-        "logprob_bwd_bucket": 5815424,
-        "logprob_bwd_probs": 19437369472,
-        "logprob_bwd_transpose": 689529824,
-        "logprob_bwd_dhidden": 40123035584,
-        "logprob_bwd_dweight": 9985464256,
-        "logprob_bwd_onehot_dw": 107591744,
+        "logprob_bwd_live_rows": 37180608,
+        "logprob_bwd_bounds": 82688,
+        "logprob_bwd_bucket": 5815168,
+        "logprob_bwd_probs": 9774121600,
+        "logprob_bwd_transpose": 689519968,
+        "logprob_bwd_dhidden": 41865538368,
+        "logprob_bwd_dweight": 10264377024,
+        "logprob_bwd_onehot_dw": 107674304,
         "rl_loss": 340480,
     },
     "write_bytes_per_launch": {
-        "logprob_fwd_gemm": 78367584,
+        "logprob_fwd_gemm": 78367712,
         "logprob_fwd_merge": 131072,
         "logprob_bwd_live_order": 66912,
         "logprob_bwd_live_rows": 134217728,
         "logprob_bwd_bounds": 32,
-        "logprob_bwd_bucket": 2647360,
-        "logprob_bwd_probs": 1322802816,
+        "logprob_bwd_bucket": 2647488,
+        "logprob_bwd_probs": 1322481408,
         "logprob_bwd_transpose": 689438720,
         "logprob_bwd_dhidden": 268435456,
         "logprob_bwd_dweight": 2556428288,
-        "logprob_bwd_onehot_dw": 69888160,
+        "logprob_bwd_onehot_dw": 69888864,
         "rl_loss": 80896,
     },
 }

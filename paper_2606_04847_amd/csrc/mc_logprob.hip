@@ -478,20 +478,16 @@ struct EpiProbs {
   TP* P;                           // panel layout (see Lay::TileTK)
   const unsigned* bound;           // max |dlogp| (fp16 operand) or null
   // Tile columns, and P~'s rows, are positions in the live-first token
-  // order (see LiveOrder): the B operand holds the row of token perm[j] at
-  // position j.  A tile whose first position is at or past *nlive has no
-  // live token and writes nothing: the contractions that read P~ read its
-  // rows from *nlive on as zeros.  Null: positions are tokens.
+  // order (k_live_perm): the B operand holds the row of token perm[j] at
+  // position j.  The tiles of positions from *nlive on hold no live token
+  // and are not computed (k_bwd_probs): the contractions that read P~ read
+  // its rows from *nlive on as zeros.  Null: positions are tokens.
   const int* perm;
   const int* nlive;
   static constexpr int64_t kPanel = 128 / sizeof(TP);
 
   __device__ __forceinline__ int64_t token(int64_t j) const {
     return perm != nullptr ? int64_t(perm[j]) : j;
-  }
-  // No live token at the tile's positions (workgroup-uniform).
-  __device__ __forceinline__ bool dead_tile(int64_t n0) const {
-    return nlive != nullptr && n0 >= int64_t(*nlive);
   }
 
   // lse_t log2(e) and -dlogp_t (0 for ignored tokens) of the tokens of this
@@ -1329,16 +1325,24 @@ __global__ __launch_bounds__(kThreads, 1) void k_fwd_logits_lse(Operand A, Opera
                                                                       lds, kGroupVT);
 }
 // T: the inputs' type, TP: the operand's (see EpiProbs)
-// A tile of positions past the live tokens exits at once.
+// With the live-first order, the first nTm x ntn workgroups take the tiles
+// of the ntn token tiles that hold a live token, in the XCD-aware order of
+// that smaller grid; the rest (tiles of dead tokens only) exit at once, after
+// all of them.
 template <typename T, typename TP>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_probs(Operand A, Operand B, int64_t K,
                                                            int nTm, int nTn,
                                                            EpiProbs<T, TP> epi) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
   int tm, tn;
-  tile_of(blockIdx.x, nTm, nTn, kGroupVT, tm, tn);
+  int ntn = nTn;
+  if (epi.nlive != nullptr) {
+    const int64_t nl = *epi.nlive;
+    ntn = int((nl + kBN - 1) / kBN);
+    if (int64_t(blockIdx.x) >= int64_t(nTm) * ntn) return;
+  }
+  tile_of(blockIdx.x, nTm, ntn, kGroupVT, tm, tn);
   const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
-  if (epi.dead_tile(n0)) return;
   const auto pre = epi.prologue(m0, n0);
   Acc acc;
   gemm_mainloop<T, Lay::KMajor, Lay::KMajor, 2, kDeepFwdA>(A, B, m0, n0, K, lds, acc);
