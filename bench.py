@@ -297,11 +297,12 @@ def recompute_cols(y, dlogp, V):
     return min(int(y.numel()), -(-n // 256) * 256)
 
 
-def count_recompute(res, cols, T):
-    """Scale the library's dense figure for the softmax contraction (2 T d
-    width per launch, one launch per vocabulary chunk) to the FLOPs it
-    executes: cols of the T token columns."""
-    k = res["kernels"].get("logprob_bwd_probs")
+def count_recompute(res, cols, T, name="logprob_bwd_probs"):
+    """Scale the library's dense figure for a contraction over the tokens
+    (2 T d width per launch, one launch per vocabulary chunk) to the FLOPs it
+    executes: cols of the T token columns (the softmax contraction always;
+    dH and dW with MC_BWD_SKIP_DEAD_TOKENS)."""
+    k = res["kernels"].get(name)
     if k:
         k["flops"] *= cols / T
 
@@ -465,7 +466,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=4, choices=[2, 3, 4, 5])
-    ap.add_argument("--step", default="both", choices=["both", "recompute", "cached"],
+    ap.add_argument("--step", default="both", choices=["both", "recompute", "cached", "skip"],
                     help="which step(s) to time (default both; the headline is recompute)")
     ap.add_argument("--shard", action="store_true",
                     help="time one GPU's vocabulary shard (V/8 entries) of the workload")
@@ -583,6 +584,24 @@ def main():
             log("timing the recompute step")
             results["recompute"] = time_steps(step, args.steps, args.warmup, sampler, flush,
                                               args.flush_reps)
+        if args.step in ("both", "skip"):
+            # the same step with MC_BWD_SKIP_DEAD_TOKENS: dH and dW leave out
+            # the dead tokens' zero products (reported beside the headline,
+            # which counts the dense backward)
+            if args.step == "skip":
+                ws_b = torch.empty(lib.mc_logprob_bwd_workspace_size(T, d, V, 1),
+                                   dtype=torch.uint8, device=dev)
+
+            def step():
+                mc.logprob_fwd(H, W, y, logp=logp, lse=lse, workspace=ws_f)
+                out = mc.rl_loss(logp, lr, st["mask"], st["cu"], st["cg"], st["rewards"], params)
+                mc.logprob_bwd(H, W, y, lse, out["dlogp"], dhidden=dH, dweight=dW,
+                               skip_dead_tokens=True, workspace=ws_b)
+                return out
+            log("timing the recompute step with dead tokens skipped")
+            results["skip_dead"] = time_steps(step, args.steps, args.warmup, sampler, flush,
+                                              args.flush_reps)
+        if args.step in ("both", "recompute", "skip"):
             del ws_b
             torch.cuda.empty_cache()
         if args.step in ("both", "cached"):
@@ -600,29 +619,47 @@ def main():
             results["cached"] = time_steps(step, args.steps, args.warmup, sampler, flush,
                                            args.flush_reps)
             del ws_c, cache
-        head = "recompute" if "recompute" in results else "cached"
+        head = ("recompute" if "recompute" in results else
+                "cached" if "cached" in results else "skip_dead")
         for name, res in results.items():
             out = res["out"]
             executed = 6.0 * T * d * V
-            if name == "recompute":
+            if name in ("recompute", "skip_dead"):
                 cols = recompute_cols(y, out["dlogp"], V)
                 count_recompute(res, cols, T)
                 executed += 2.0 * cols * d * V
+            if name == "skip_dead":
+                for k in ("logprob_bwd_dhidden", "logprob_bwd_dweight"):
+                    count_recompute(res, cols, T, k)
+                executed = 2.0 * T * d * V + 6.0 * cols * d * V
             summ = summary(res, T, 6.0 * T * d * V, executed)
-            if name == "recompute":
+            if name in ("recompute", "skip_dead"):
                 summ["recompute_token_cols"] = cols
+            if name == "skip_dead":
+                # not the counted step: the backward leaves out dead tokens'
+                # products, so only the executed figure is meaningful
+                for k in ("mfma_frac", "counted_tflops", "mfma_frac_at_measured_clock"):
+                    summ.pop(k, None)
+                summ["note"] = ("MC_BWD_SKIP_DEAD_TOKENS: dH and dW leave out the zero products "
+                                "of tokens with zero dlogp; same results; executed FLOPs "
+                                "2TdV + 6 T_c d V")
             summ["loss"] = float(out["loss"].item())
             summ["n_valid"] = int(out["n_valid"].item())
             results[name] = summ
         line.update(results[head])
-        config["backward"] = ("recompute logits: the forward writes no [T,V] tensor"
-                              if head == "recompute" else "softmax cache: the forward writes a "
-                              "[T,V] fp16 cache")
+        config["backward"] = {
+            "recompute": "recompute logits: the forward writes no [T,V] tensor",
+            "cached": "softmax cache: the forward writes a [T,V] fp16 cache",
+            "skip_dead": "recompute logits, MC_BWD_SKIP_DEAD_TOKENS (not the counted step)"}[head]
         line["config"] = config
         if head == "recompute" and "cached" in results:
             line["cached"] = results["cached"]
-        log(f"{head}: {line['ms_per_step']:.3f} ms/step, {line['counted_tflops']:.1f} TFLOP/s "
-            f"counted ({100 * line['mfma_frac']:.1f}% of peak)")
+        if head == "recompute" and "skip_dead" in results:
+            line["skip_dead"] = results["skip_dead"]
+        for name, r in results.items():
+            frac = (f"{100 * r['mfma_frac']:.1f}% of peak counted" if "mfma_frac" in r else
+                    f"{100 * r['executed_mfma_frac']:.1f}% of peak executed")
+            log(f"{name}: {r['ms_per_step']:.3f} ms/step ({frac})")
 
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle baseline sample")

@@ -124,6 +124,12 @@ typedef struct {
 /* Flags of mc_logprob_bwd. */
 #define MC_BWD_ACCUMULATE_DHIDDEN 1   /* dhidden += gradient instead of = */
 #define MC_BWD_ACCUMULATE_DWEIGHT 2   /* dweight += gradient instead of = */
+/* mc_logprob_bwd / mc_logprob_bwd_shard only (the cached backward rejects
+ * it): the two gradient contractions also leave out the products of the
+ * tokens whose gradient row is zero (dlogp_t == 0 or an ignored target),
+ * which are exact zeros.  The results are the same; the work of the whole
+ * backward then scales with the live tokens instead of T. */
+#define MC_BWD_SKIP_DEAD_TOKENS 4
 
 /* Human-readable name of a status code (static string). */
 const char* mc_status_string(mc_status_t status);
@@ -184,7 +190,8 @@ mc_status_t mc_logprob_merge_shards(const float* partials, int32_t S, const int6
  *   lse      [T] fp32          as returned by mc_logprob_fwd for the same inputs
  *   dlogp    [T] fp32
  *   dhidden / dweight may be NULL to skip that gradient (not both).
- *   flags    MC_BWD_ACCUMULATE_* bits: accumulate into the outputs.
+ *   flags    MC_BWD_ACCUMULATE_* bits: accumulate into the outputs;
+ *            MC_BWD_SKIP_DEAD_TOKENS: see its definition.
  * The softmax part is formed per vocabulary chunk as a transient operand in
  * the workspace; logits are recomputed, never stored.  They are recomputed
  * only where the gradient row can be nonzero: the tokens with dlogp_t != 0

@@ -20,6 +20,7 @@ MC_FILTER = {"none": 0, "vanilla": 1, "mirrorpop": 2}
 MC_TOKEN = {"none": 0, "tis": 1, "icepop": 2}
 MC_BWD_ACCUMULATE_DHIDDEN = 1
 MC_BWD_ACCUMULATE_DWEIGHT = 2
+MC_BWD_SKIP_DEAD_TOKENS = 4
 
 _c_i64, _c_i32, _c_sz, _vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t, ctypes.c_void_p
 
@@ -302,7 +303,7 @@ def logprob_merge_shards(partials, targets, V_total, *, with_entropy=True, strea
 
 def logprob_bwd_shard(hidden, weight_shard, targets, lse, dlogp, v_offset, V_total, *,
                       dhidden=None, dweight=None, need_dhidden=True, need_dweight=True,
-                      workspace=None, stream=None):
+                      skip_dead_tokens=False, workspace=None, stream=None):
     """Backward on a vocabulary shard (see mc_logprob_bwd_shard).  Returns
     (this shard's part of dhidden, the shard's rows of dW)."""
     torch = _torch()
@@ -321,7 +322,8 @@ def logprob_bwd_shard(hidden, weight_shard, targets, lse, dlogp, v_offset, V_tot
     _check(lib.mc_logprob_bwd_shard(_ptr(hidden), _ptr(weight_shard), _ptr(targets), _ptr(lse),
                                     _ptr(dlogp), T, d, Vs, int(v_offset), int(V_total), dt,
                                     _ptr(dhidden if need_dhidden else None),
-                                    _ptr(dweight if need_dweight else None), 0, _ptr(ws),
+                                    _ptr(dweight if need_dweight else None),
+                                    MC_BWD_SKIP_DEAD_TOKENS if skip_dead_tokens else 0, _ptr(ws),
                                     nbytes, _stream(stream)), "mc_logprob_bwd_shard")
     _keep_alive(stream, *owned)
     return (dhidden if need_dhidden else None), (dweight if need_dweight else None)
@@ -351,9 +353,10 @@ def primeecho_rewards(scores, success=None, n_turns=None, *, alpha=0.75, beta1=0
 
 def logprob_bwd(hidden, weight, targets, lse, dlogp, *, dhidden=None, dweight=None,
                 need_dhidden=True, need_dweight=True, accumulate_dhidden=False,
-                accumulate_dweight=False, workspace=None, stream=None):
-    """Gradients of sum_t dlogp_t logp_t (see mc_logprob_bwd).
-    Returns (dhidden [T,d] fp32 or None, dweight [V,d] fp32 or None)."""
+                accumulate_dweight=False, skip_dead_tokens=False, workspace=None, stream=None):
+    """Gradients of sum_t dlogp_t logp_t (see mc_logprob_bwd).  skip_dead_tokens:
+    MC_BWD_SKIP_DEAD_TOKENS.  Returns (dhidden [T,d] fp32 or None, dweight
+    [V,d] fp32 or None)."""
     torch = _torch()
     lib = load_library()
     T, d = hidden.shape
@@ -376,7 +379,8 @@ def logprob_bwd(hidden, weight, targets, lse, dlogp, *, dhidden=None, dweight=No
     if not need_dweight:
         dweight = None
     flags = ((MC_BWD_ACCUMULATE_DHIDDEN if accumulate_dhidden else 0)
-             | (MC_BWD_ACCUMULATE_DWEIGHT if accumulate_dweight else 0))
+             | (MC_BWD_ACCUMULATE_DWEIGHT if accumulate_dweight else 0)
+             | (MC_BWD_SKIP_DEAD_TOKENS if skip_dead_tokens else 0))
     need = lib.mc_logprob_bwd_workspace_size(T, d, V, dt)
     ws, nbytes = _workspace(need, dev, workspace, owned)
     _check(lib.mc_logprob_bwd(_ptr(hidden), _ptr(weight), _ptr(targets), _ptr(lse), _ptr(dlogp),

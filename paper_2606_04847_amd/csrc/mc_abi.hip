@@ -200,7 +200,8 @@ static mc_status_t bwd_common(const void* hidden, const void* weight, const int6
                               size_t ws_bytes, void* stream) {
   mc_status_t st = check_dims(T, d, V, dt);
   if (st != MC_OK) return st;
-  if (flags & ~(MC_BWD_ACCUMULATE_DHIDDEN | MC_BWD_ACCUMULATE_DWEIGHT)) return MC_ERR_INVALID_ARG;
+  if (flags & ~(MC_BWD_ACCUMULATE_DHIDDEN | MC_BWD_ACCUMULATE_DWEIGHT | MC_BWD_SKIP_DEAD_TOKENS))
+    return MC_ERR_INVALID_ARG;
   if (!dhidden && !dweight) return MC_ERR_INVALID_ARG;
   if (!hidden || !weight) return MC_ERR_INVALID_ARG;
   if (!aligned(hidden, 16) || !aligned(weight, 16) || (dhidden && !aligned(dhidden, 16)) ||

@@ -103,7 +103,8 @@ def bwd(lib, T=16, d=64, V=100, dt=BF16, dh=FAKE, dw=FAKE, flags=0, lse=FAKE, dl
 
 def test_bwd_argument_checks(lib):
     assert bwd(lib, dh=None, dw=None) == INVALID
-    assert bwd(lib, flags=4) == INVALID
+    assert bwd(lib, flags=8) == INVALID            # unknown flag bit
+    assert bwd(lib, flags=4, lse=None) == INVALID  # MC_BWD_SKIP_DEAD_TOKENS is known; null lse
     assert bwd(lib, d=12) == UNSUP
     assert bwd(lib, lse=None) == INVALID
     assert bwd(lib, dl=None) == INVALID
@@ -214,6 +215,7 @@ def test_cached_argument_checks(lib):
     assert bwd(None, need_c) == WS
     assert bwd(FAKE_WS, 0) == WS
     assert bwd(FAKE_WS, need_c, flags=8) == INVALID
+    assert bwd(FAKE_WS, need_c, flags=4) == INVALID   # skipping is the recompute pair's only
     assert bwd(FAKE_WS, need_c, dh=FAKE + 4) == INVALID
 
 

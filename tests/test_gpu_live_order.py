@@ -12,12 +12,19 @@ edges (none, one, 255, 256, 257, all, scattered, only in the ragged last
 tile, ignored targets with nonzero dlogp), exact zero rows of dH for the
 dead tokens, and dH's live rows bit-identical to a call on the live tokens
 alone (each row's logits, operand and contraction over the vocabulary do
-not depend on where the token sits in the order)."""
+not depend on where the token sits in the order).
+
+MC_BWD_SKIP_DEAD_TOKENS makes dH and dW leave out the dead tokens' products,
+which are exact zeros: both gradients must equal those of the call without
+it bit for bit, also when accumulating, and at full size on the headline
+workload and on the 27B-class one (two vocabulary chunks), through the
+chain bench.py times."""
 import numpy as np
 import pytest
 
 import oracle
-from _cases import GRAD_RTOL, PTERM_RTOL_F16, device_tensors, rel_fro
+from _cases import (GRAD_RTOL, PTERM_RTOL_F16, device_tensors, fullsize_inputs, rel_fro,
+                    structure_tensors, to_params)
 from workloads import make_tensors_numpy, scaled_config
 
 pytestmark = pytest.mark.gpu
@@ -89,7 +96,9 @@ def test_live_first_order(kind, dtype, T):
     dl = torch.from_numpy(dlogp).cuda()
     _, lse = mc.logprob_fwd(H, W, yd)
     dH, dW = mc.logprob_bwd(H, W, yd, lse, dl)
+    dH_s, dW_s = mc.logprob_bwd(H, W, yd, lse, dl, skip_dead_tokens=True)
     torch.cuda.synchronize()
+    assert torch.equal(dH, dH_s) and torch.equal(dW, dW_s), (kind, dtype)
     yc = np.where((y >= 0) & (y < V), y, -1)
     _, lse_o = oracle.logprob_fwd(Hn, Wn, yc)
     dl64 = dlogp.astype(np.float64)
@@ -117,3 +126,51 @@ def test_live_first_order(kind, dtype, T):
                                  lse[idx].contiguous(), dl[idx].contiguous())
         torch.cuda.synchronize()
         assert torch.equal(dH[idx], dH_l), (kind, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_skip_dead_tokens_accumulates_the_same(dtype):
+    import paper_2606_04847_amd as mc
+    T = T_LARGE
+    cfg = scaled_config(1, d=D, V=V, dtype=dtype, seed=71)
+    Hn, Wn, hb, wb = make_tensors_numpy(cfg, T)
+    rng = np.random.default_rng(72)
+    y = rng.integers(0, V, size=T).astype(np.int64)
+    dlogp = (rng.standard_normal(T) / T).astype(np.float32)
+    dlogp[_live_set("spans", rng, T) == 0] = 0.0
+    H, W, yd = device_tensors(dict(H=Hn, W=Wn, hb=hb, wb=wb, y=y))
+    dl = torch.from_numpy(dlogp).cuda()
+    _, lse = mc.logprob_fwd(H, W, yd)
+    g = torch.Generator(device="cuda").manual_seed(73)
+    base_h = torch.randn(T, D, device="cuda", generator=g)
+    base_w = torch.randn(V, D, device="cuda", generator=g)
+    out = {}
+    for skip in (False, True):
+        dH, dW = base_h.clone(), base_w.clone()
+        mc.logprob_bwd(H, W, yd, lse, dl, dhidden=dH, dweight=dW, accumulate_dhidden=True,
+                       accumulate_dweight=True, skip_dead_tokens=skip)
+        out[skip] = (dH, dW)
+    torch.cuda.synchronize()
+    assert torch.equal(out[False][0], out[True][0]) and torch.equal(out[False][1], out[True][1])
+    dead = torch.from_numpy(dlogp == 0.0).cuda()
+    assert torch.equal(out[True][0][dead], base_h[dead])     # dead rows left as they were
+
+
+@pytest.mark.parametrize("cid", [4, 3])
+def test_skip_dead_tokens_full_size(cid):
+    # the chain bench.py times, on the workload's own dlogp from the GPU loss
+    import paper_2606_04847_amd as mc
+    s, H, W, y = fullsize_inputs(cid)
+    logp, lse = mc.logprob_fwd(H, W, y)
+    lr = logp + torch.from_numpy(s.rollout_delta).cuda()
+    st = structure_tensors(s)
+    out = mc.rl_loss(logp, lr, st["mask"], st["cu"], st["cg"], st["rewards"],
+                     to_params(oracle.RLParams()))
+    dl = out["dlogp"]
+    n_live = int(((dl != 0) & (y >= 0) & (y < W.shape[0])).sum().item())
+    assert 0 < n_live < s.T
+    dH, dW = mc.logprob_bwd(H, W, y, lse, dl)
+    dH_s, dW_s = mc.logprob_bwd(H, W, y, lse, dl, skip_dead_tokens=True)
+    torch.cuda.synchronize()
+    print(f"[skip {cid}] T={s.T} live={n_live}", flush=True)
+    assert torch.equal(dH, dH_s) and torch.equal(dW, dW_s)
