@@ -60,33 +60,33 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "1e859ccee75bffaf3ca6424eb3e785ecce3db75a2927c30d06f5eb1b2fbc5cd3",
+        "3f6074ab4812437ca04d52d2f1120b49ace3cf65d2121b6caa1776279fa27d0b",
     "read_bytes_per_launch": {
-        "logprob_fwd_gemm": 38859475328,
-        "logprob_fwd_merge": 78110784,
-        "logprob_bwd_live_order": 431104,
-        "logprob_bwd_live_rows": 37180608,
-        "logprob_bwd_bounds": 82688,
-        "logprob_bwd_bucket": 5815168,
-        "logprob_bwd_probs": 9774121600,
-        "logprob_bwd_transpose": 689519968,
-        "logprob_bwd_dhidden": 41865538368,
-        "logprob_bwd_dweight": 10264377024,
-        "logprob_bwd_onehot_dw": 107674304,
+        "logprob_fwd_gemm": 35619319808,
+        "logprob_fwd_merge": 78110848,
+        "logprob_bwd_live_order": 436224,
+        "logprob_bwd_live_rows": 37180160,
+        "logprob_bwd_bounds": 80576,
+        "logprob_bwd_bucket": 5801920,
+        "logprob_bwd_probs": 11017802944,
+        "logprob_bwd_transpose": 689529056,
+        "logprob_bwd_dhidden": 26520335168,
+        "logprob_bwd_dweight": 10480632704,
+        "logprob_bwd_onehot_dw": 107672640,
         "rl_loss": 340480,
     },
     "write_bytes_per_launch": {
-        "logprob_fwd_gemm": 78367712,
+        "logprob_fwd_gemm": 78367648,
         "logprob_fwd_merge": 131072,
         "logprob_bwd_live_order": 66912,
         "logprob_bwd_live_rows": 134217728,
         "logprob_bwd_bounds": 32,
         "logprob_bwd_bucket": 2647488,
-        "logprob_bwd_probs": 1322481408,
+        "logprob_bwd_probs": 1322486528,
         "logprob_bwd_transpose": 689438720,
         "logprob_bwd_dhidden": 268435456,
         "logprob_bwd_dweight": 2556428288,
-        "logprob_bwd_onehot_dw": 69888864,
+        "logprob_bwd_onehot_dw": 69889184,
         "rl_loss": 80896,
     },
 }

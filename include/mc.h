@@ -127,8 +127,11 @@ typedef struct {
 /* mc_logprob_bwd / mc_logprob_bwd_shard only (the cached backward rejects
  * it): the two gradient contractions also leave out the products of the
  * tokens whose gradient row is zero (dlogp_t == 0 or an ignored target),
- * which are exact zeros.  The results are the same; the work of the whole
- * backward then scales with the live tokens instead of T. */
+ * which are exact zeros, so the work of the whole backward scales with the
+ * live tokens instead of T.  dweight is bit-identical to the result without
+ * the flag; dhidden is the same up to the order of fp32 sums (a last round
+ * of tiles that would leave compute units idle is split along the
+ * vocabulary), still deterministic; dead tokens' rows are identical. */
 #define MC_BWD_SKIP_DEAD_TOKENS 4
 
 /* Human-readable name of a status code (static string). */

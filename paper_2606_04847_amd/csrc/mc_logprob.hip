@@ -1364,42 +1364,103 @@ constexpr int kGroupDH = 4;
 // tile of dead tokens only runs its epilogue (zero rows), without the loop,
 // and the live tiles come first in a grid of their own (the strided order
 // measured 10.4 ms against 6.4 there: it left live tiles waiting for CUs
-// behind others).
+// behind others).  When the live tiles' last round would fill at most half
+// of the CUs, its tiles are split along K (plan_tail, computed here from the
+// live count) into fp32 slots that k_dh_tail_reduce sums in split order.
+// The grid then has up to kTailSlots workgroups more than tiles; the spare
+// ones exit.
 template <typename TG, typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_bwd_dhidden(Operand A, Operand B, int64_t K,
                                                              int nTm, int nTn, EpiDH<T> epi,
                                                              const int* nlive, int stride,
-                                                             int skip) {
+                                                             int skip, int ncu, float* slots,
+                                                             int cap) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsRing];
   int tm, tn;
+  int j = -1;   // the K slice of a split tile, or -1
+  Operand a = A, b = B;
+  int64_t k = K;
   if (skip && nlive != nullptr) {
     // the live token tile rows' tiles first, in the XCD-aware order of that
-    // smaller grid; then the tiles of dead tokens (no loop: zero rows)
+    // smaller grid; then the split tiles' slices; then the tiles of dead
+    // tokens (no loop: zero rows)
     const int ntl = int((int64_t(*nlive) + kBM - 1) / kBM);
-    const int nlt = ntl * nTn;
+    const TailSplit ts = plan_tail(ntl * nTn, K, ncu, cap);
+    const int nsp = ts.rem * ts.splits;
     const int bid = blockIdx.x;
-    if (bid < nlt) {
-      tile_of(bid, ntl, nTn, kGroupDH, tm, tn);
+    if (bid < ts.full) {
+      tile_of(bid, ntl, nTn, kGroupDH, tm, tn, ts.full);
+    } else if (bid < ts.full + nsp) {
+      j = bid - ts.full;
+      tile_of_logical(ts.full + j / ts.splits, ntl, nTn, kGroupDH, tm, tn);
+      const int64_t k0 = int64_t(j % ts.splits) * ts.ks;
+      k = K - k0 < ts.ks ? K - k0 : ts.ks;
+      a = k_slice<TG, Lay::TileTK>(A, k0, k);
+      b = k_slice<TG, Lay::KMajor>(B, k0, k);
     } else {
-      const int r = bid - nlt;
+      const int r = bid - ts.full - nsp;
       tm = ntl + r / nTn;
       tn = r % nTn;
+      if (tm >= nTm) return;   // spare workgroup
     }
   } else {
     tile_of(blockIdx.x, nTm, nTn, kGroupDH, tm, tn);
     tm = int((int64_t(tm) * stride) % nTm);
   }
   const int64_t m0 = int64_t(tm) * kBM, n0 = int64_t(tn) * kBN;
-  Operand a = A;
-  int64_t k = K;
   if (nlive != nullptr) {
     const int64_t nl = *nlive;
     if (nl < a.rows) a.rows = nl;
     if (skip && m0 >= nl) k = 0;
   }
   Acc acc;
-  gemm_mainloop<TG, Lay::TileTK, Lay::KMajor, 2, kDeepDhA>(a, B, m0, n0, k, lds, acc);
-  epi.epilogue(acc, tm, tn, m0, n0, lds, lds + kLdsGemm);
+  gemm_mainloop<TG, Lay::TileTK, Lay::KMajor, 2, kDeepDhA>(a, b, m0, n0, k, lds, acc);
+  if (j < 0) {
+    epi.epilogue(acc, tm, tn, m0, n0, lds, lds + kLdsGemm);
+  } else {
+    const EpiStoreT slot{slots + int64_t(j) * (kBM * kBN), kBM, kBM, kBN, 0};
+    slot.epilogue(acc, tm, tn, 0, 0, lds, nullptr);
+  }
+}
+
+// The split tiles of k_bwd_dhidden (same plan, from the live count): each
+// element is the sum of its slots in split order (slot[c][r]), then what
+// EpiDH does to a tile element: unscale, add the stored value when
+// accumulating, add the one-hot part, store to dH's row perm[r].  Grid x:
+// split tiles (spare workgroups exit), y: groups of 4 columns; thread: one
+// row, 4 consecutive columns.
+template <typename T>
+__global__ __launch_bounds__(256) void k_dh_tail_reduce(const float* __restrict__ slots,
+                                                        const int* __restrict__ nlive, int nTn,
+                                                        int64_t K, int ncu, int cap,
+                                                        EpiDH<T> epi) {
+  const int ntl = int((int64_t(*nlive) + kBM - 1) / kBM);
+  const TailSplit ts = plan_tail(ntl * nTn, K, ncu, cap);
+  if (int(blockIdx.x) >= ts.rem) return;
+  int tm, tn;
+  tile_of_logical(ts.full + int(blockIdx.x), ntl, nTn, kGroupDH, tm, tn);
+  const int r = threadIdx.x, c4 = int(blockIdx.y) * 4;
+  const int64_t pos = int64_t(tm) * kBM + r, c = int64_t(tn) * kBN + c4;
+  if (pos >= epi.rows || c >= epi.cols) return;   // cols and ldc are multiples of 4
+  f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+  const float* sl = slots + int64_t(blockIdx.x) * ts.splits * (kBM * kBN);
+  for (int q = 0; q < ts.splits; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] += sl[int64_t(q) * (kBM * kBN) + (c4 + e) * kBM + r];
+  v = Unscale(epi.bound_p, epi.bound_w)(v);
+  const int64_t t = epi.perm != nullptr ? int64_t(epi.perm[pos]) : pos;
+  float* o = epi.C + t * epi.ldc + c;
+  if (epi.accumulate) v += *reinterpret_cast<const f32x4*>(o);
+  if (epi.W != nullptr) {
+    const int64_t yy = epi.y[t] - epi.v_off;
+    if (yy >= 0 && yy < epi.Vs) {
+      const float g = epi.dlogp[t];
+      const T* w = epi.W + yy * epi.ldc + c;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] += g * float(w[e]);
+    }
+  }
+  *reinterpret_cast<f32x4*>(o) = v;
 }
 // dW^T = H^T P~ : tile rows are hidden dimensions (A = H^T, along the
 // tokens), tile columns vocabulary entries (B = the operand panels read
@@ -1690,9 +1751,15 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
                     es * (double(Tn) * width + double(width) * d) +
                         4.0 * Tn * d * (epi.accumulate ? 2 : 1) +
                         (last ? es * double(Tn) * d + 16.0 * Tn : 0.0));
-      hipLaunchKernelGGL((k_bwd_dhidden<TP, T>), dim3(nTm * nTd),
+      // skipping: up to kTailSlots spare workgroups for the split tiles'
+      // slices (dW's tail slots, free until dW runs)
+      const int cap = int(tail_slot_floats(d, min(chunk, Vs)) / (kBM * kBN));
+      hipLaunchKernelGGL((k_bwd_dhidden<TP, T>), dim3(nTm * nTd + (skip ? kTailSlots : 0)),
                          dim3(kThreads), 0, s, A, B, ldc, nTm, nTd, epi, nlive,
-                         nlive != nullptr ? row_stride(nTm) : 1, skip ? 1 : 0);
+                         nlive != nullptr ? row_stride(nTm) : 1, skip ? 1 : 0, ncu, slots, cap);
+      if (skip)
+        hipLaunchKernelGGL(k_dh_tail_reduce<T>, dim3(kTailSlots / 2, kBN / 4), dim3(256), 0, s,
+                           slots, nlive, nTd, ldc, ncu, cap, epi);
     }
     if (dW) {
       // dW[chunk]^T (+)= H^T P~ : M = d, N = chunk columns, K = T (the

@@ -209,15 +209,18 @@ struct TailSplit {
   int full, rem, splits;
   int64_t ks;
 };
-inline TailSplit plan_tail(int total, int64_t K, int ncu) {
+// `cap`: the slots available.  Host and device (a kernel may plan from a
+// tile count it reads from device memory).
+__host__ __device__ inline TailSplit plan_tail(int total, int64_t K, int ncu,
+                                               int cap = kTailSlots) {
   constexpr int64_t kStage = 64;   // K columns of one bf16 stage (32 for fp32; a multiple works)
   TailSplit t{total, 0, 1, K};
   if (ncu <= 0) return t;
   const int rem = total % ncu;
   if (rem == 0 || 2 * rem > ncu) return t;
+  const int room = ncu < cap ? ncu : cap;
   int splits = 1;
-  while (splits < 8 && rem * splits * 2 <= std::min(ncu, kTailSlots) &&
-         K >= int64_t(splits) * 2 * 4 * kStage)
+  while (splits < 8 && rem * splits * 2 <= room && K >= int64_t(splits) * 2 * 4 * kStage)
     splits *= 2;
   const int64_t nst = (K + kStage - 1) / kStage;
   int64_t ks = (nst + splits - 1) / splits * kStage;
