@@ -404,7 +404,7 @@ def summarize(path, only=None):
     def role(name):
         for key in ("k_fwd_logits_lse", "k_bwd_probs", "k_bwd_dhidden", "k_bwd_dweight",
                     "k_cache_to_probs", "k_transpose", "k_onehot_seg", "k_onehot_join", "k_lse_merge",
-                    "k_shard_partial", "k_tail_reduce", "k_surrogate", "k_seq_stats",
+                    "k_shard_partial", "k_dh_tail_reduce", "k_tail_reduce", "k_surrogate", "k_seq_stats",
                     "k_bucket_rank", "k_bucket_fill", "k_hist", "k_scan", "k_fill_i32", "k_bound_abs",
                     "k_live_rows", "k_live_count", "k_live_perm",
                     "k_count", "k_finish", "k_loss_init", "copyBuffer"):
