@@ -95,6 +95,20 @@ def test_vocab_shards_match_full(dtype):
     dH_o, dW_o = oracle.logprob_bwd(case["H"], case["W"], case["y"], so, dl.astype(np.float64))
     assert rel_fro(dH, dH_o) <= GRAD_RTOL
     assert rel_fro(np.concatenate(dWs), dW_o) <= GRAD_RTOL
+    # each shard's backward with MC_BWD_SKIP_DEAD_TOKENS (two thirds of the
+    # tokens with zero dlogp): the shard's dW rows bit for bit, its dH part up
+    # to the order of fp32 sums, dead rows exactly zero
+    dl[rng.random(T) < 0.67] = 0.0
+    dld = torch.from_numpy(dl).cuda()
+    dead = torch.from_numpy(dl == 0.0).cuda()
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        Ws = W[a:b].contiguous()
+        h, w = mc.logprob_bwd_shard(H, Ws, y, lse, dld, a, V)
+        hs, ws = mc.logprob_bwd_shard(H, Ws, y, lse, dld, a, V, skip_dead_tokens=True)
+        torch.cuda.synchronize()
+        assert torch.equal(w, ws), (a, b)
+        assert not hs[dead].any() and not h[dead].any(), (a, b)
+        assert rel_fro(hs.double().cpu().numpy(), h.double().cpu().numpy()) <= 1e-6, (a, b)
 
 
 def test_vocab_shards_full_size():
