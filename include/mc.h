@@ -121,13 +121,12 @@ typedef struct {
                                     or dropped (IcePop); 0 for MC_TOKEN_NONE */
 } mc_rl_outputs_t;
 
-/* Flags of mc_logprob_bwd. */
+/* Flags of mc_logprob_bwd, mc_logprob_bwd_shard and mc_logprob_bwd_cached. */
 #define MC_BWD_ACCUMULATE_DHIDDEN 1   /* dhidden += gradient instead of = */
 #define MC_BWD_ACCUMULATE_DWEIGHT 2   /* dweight += gradient instead of = */
-/* mc_logprob_bwd / mc_logprob_bwd_shard only (the cached backward rejects
- * it): the two gradient contractions also leave out the products of the
- * tokens whose gradient row is zero (dlogp_t == 0 or an ignored target),
- * which are exact zeros, so the work of the whole backward scales with the
+/* The two gradient contractions also leave out the products of the tokens
+ * whose gradient row is zero (dlogp_t == 0 or an ignored target), which
+ * are exact zeros, so the work of the whole backward scales with the
  * live tokens instead of T.  dweight is bit-identical to the result without
  * the flag; dhidden is the same up to the order of fp32 sums (a last round
  * of tiles that would leave compute units idle is split along the
@@ -238,20 +237,23 @@ mc_status_t mc_logprob_bwd_shard(const void* hidden, const void* weight_shard,
  *                                      block maximum is exactly 1; fp32
  *                                      for MC_F32)
  *   c_b[t]  = max of z[t, .] over block b of 128 vocabulary entries (fp32)
- * and the backward turns E, in place, into the softmax part of G (for
- * MC_BF16 the recompute pair's fp16 operand, scaled by the same power of
- * two) and runs the two contractions on it.  E adds one rounding before
+ * and the backward gathers from E the softmax part of G for the tokens whose
+ * gradient row can be nonzero (for MC_BF16 the recompute pair's fp16
+ * operand, scaled by the same power of two) into its workspace and runs the
+ * two contractions on it as mc_logprob_bwd does.  E adds one rounding before
  * the operand's own: each element of the operand is within about 2^-10
  * relative of its exact value, against 2^-11 for the recompute pair.
  *   cache     device, 256-byte aligned, at least mc_logprob_cache_size bytes;
  *             owned by the caller; written by mc_logprob_fwd_cached and
- *             consumed (overwritten) by one mc_logprob_bwd_cached call with
- *             the same hidden, weight, targets and shapes.  Its contents
- *             between the two calls must not be touched.
+ *             read (not modified) by mc_logprob_bwd_cached calls with the
+ *             same hidden, weight, targets and shapes, any number of them
+ *             (several upstream gradients of one forward).
  *   The forward takes the workspace of mc_logprob_fwd
  *   (mc_logprob_fwd_workspace_size); the backward takes
- *   mc_logprob_bwd_cached_workspace_size bytes.  Errors as for the plain
- *   entry points; a missing or short cache returns MC_ERR_WORKSPACE.
+ *   mc_logprob_bwd_cached_workspace_size bytes (it holds the gathered
+ *   operand: about the cache's size).  Flags as for mc_logprob_bwd.  Errors
+ *   as for the plain entry points; a missing or short cache returns
+ *   MC_ERR_WORKSPACE.
  * ------------------------------------------------------------------------ */
 size_t mc_logprob_cache_size(int64_t T, int64_t d, int64_t V, mc_dtype_t dtype);
 mc_status_t mc_logprob_fwd_cached(const void* hidden, const void* weight,

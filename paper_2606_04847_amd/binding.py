@@ -435,10 +435,10 @@ def logprob_fwd_cached(hidden, weight, targets, cache, *, logp=None, lse=None, e
 
 def logprob_bwd_cached(hidden, weight, targets, lse, dlogp, cache, *, dhidden=None,
                        dweight=None, need_dhidden=True, need_dweight=True,
-                       accumulate_dhidden=False, accumulate_dweight=False, workspace=None,
-                       stream=None):
+                       accumulate_dhidden=False, accumulate_dweight=False,
+                       skip_dead_tokens=False, workspace=None, stream=None):
     """mc_logprob_bwd_cached: logprob_bwd from the cache the forward filled
-    (the cache is consumed)."""
+    (read only)."""
     torch = _torch()
     lib = load_library()
     T, d = hidden.shape
@@ -461,7 +461,8 @@ def logprob_bwd_cached(hidden, weight, targets, lse, dlogp, cache, *, dhidden=No
     if not need_dweight:
         dweight = None
     flags = ((MC_BWD_ACCUMULATE_DHIDDEN if accumulate_dhidden else 0)
-             | (MC_BWD_ACCUMULATE_DWEIGHT if accumulate_dweight else 0))
+             | (MC_BWD_ACCUMULATE_DWEIGHT if accumulate_dweight else 0)
+             | (MC_BWD_SKIP_DEAD_TOKENS if skip_dead_tokens else 0))
     need = lib.mc_logprob_bwd_cached_workspace_size(T, d, V, dt)
     ws, nbytes = _workspace(need, dev, workspace, owned)
     _check(lib.mc_logprob_bwd_cached(_ptr(hidden), _ptr(weight), _ptr(targets), _ptr(lse),

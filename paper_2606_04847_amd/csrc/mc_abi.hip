@@ -145,7 +145,8 @@ mc_status_t mc_logprob_bwd_cached(const void* hidden, const void* weight, const 
                                   size_t ws_bytes, void* stream) {
   mc_status_t st = check_dims(T, d, V, dt);
   if (st != MC_OK) return st;
-  if (flags & ~(MC_BWD_ACCUMULATE_DHIDDEN | MC_BWD_ACCUMULATE_DWEIGHT)) return MC_ERR_INVALID_ARG;
+  if (flags & ~(MC_BWD_ACCUMULATE_DHIDDEN | MC_BWD_ACCUMULATE_DWEIGHT | MC_BWD_SKIP_DEAD_TOKENS))
+    return MC_ERR_INVALID_ARG;
   if (!dhidden && !dweight) return MC_ERR_INVALID_ARG;
   if (!hidden || !weight) return MC_ERR_INVALID_ARG;
   if (!aligned(hidden, 16) || !aligned(weight, 16) || (dhidden && !aligned(dhidden, 16)) ||

@@ -1237,41 +1237,37 @@ __global__ __launch_bounds__(256) void k_onehot_join(const int64_t* __restrict__
 // Named kernels, one per role of the shared tile core.
 // Softmax cache -> backward operand, in place: P~[t, v] = -dlogp_t
 // exp(cm[v / kWaveRows][t] - lse_t) E[t, v] (0 for ignored tokens).
-// Workgroup = one group of kCachePanels consecutive panels x one block of
-// 32 tokens; thread = one 16-byte chunk of one row of each of those panels
-// (8 lanes per 128-byte row).  The order of the workgroups follows the
-// number of live tokens (nonzero factor), counted by the bucketing pass:
-// with few of them the pass is mostly writes, and walking the panels of one
-// token block first spreads the 4 KiB pieces in flight over many panels
-// (headline workload, 27% live: 1.36 ms against 1.50); with most tokens live
-// it streams reads and writes in place, and walking the tokens of one panel
-// group first is faster (all live: 1.68 against 1.86 ms at the headline
-// shape, 11.35 against 12.19 ms at T = 65536, V = 248320).  4 panels per
-// thread: 1, 2, 3, 6 or 8 measured 1.45-2.6 ms.  The stream is touched
-// once: non-temporal loads and stores.  Where the factor is exactly zero (a
-// token whose dlogp is zero: outside the loss mask, in a filtered sequence
-// or clipped; an ignored target; a block past the vocabulary) the chunk is
-// written as zeros without reading it: the cached values are finite, so
-// the product would be zeros of the same sign.
+// The cached pair's operand: P~ = -dlogp_t exp(c_b - lse_t) E[t] for the live
+// tokens, written to row j of the workspace operand for the token t =
+// perm[j] at position j of the live-first order; rows past the live tokens
+// are not written (the contractions read them as zeros), and the cache is
+// only read.  Workgroup = one group of kCachePanels consecutive panels x one
+// block of 32 positions, the panels of one block first; thread = one
+// 16-byte chunk of one row of each of those panels (8 lanes per 128-byte
+// row).  4 panels per thread (1, 2, 3, 6 or 8 measured slower for the
+// in-place pass this replaces).  Touched once: non-temporal loads and
+// stores.  Where the factor is exactly zero (a vocabulary block past V, or
+// a factor that underflows) the chunk is written as zeros without reading
+// it: the cached values are finite.
 constexpr int kCachePanels = 4;
 template <typename T>
-__global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
-                                                        const float* __restrict__ cm,
-                                                        const float* __restrict__ lse,
-                                                        const float* __restrict__ dlogp,
-                                                        const int64_t* __restrict__ y,
-                                                        int64_t Tn, int64_t V, int64_t pld,
-                                                        int64_t npanels, uint32_t ngroups,
-                                                        const int* __restrict__ live,
-                                                        const unsigned* __restrict__ bound) {
+__global__ __launch_bounds__(256) void k_cache_gather(const T* __restrict__ E,
+                                                      const float* __restrict__ cm,
+                                                      const float* __restrict__ lse,
+                                                      const float* __restrict__ dlogp,
+                                                      const int64_t* __restrict__ y,
+                                                      const int* __restrict__ perm,
+                                                      const int* __restrict__ nlive,
+                                                      int64_t Tn, int64_t V, int64_t pld,
+                                                      int64_t npanels, uint32_t ngroups,
+                                                      const unsigned* __restrict__ bound,
+                                                      T* __restrict__ P) {
   constexpr int BV = 128 / sizeof(T);   // panel width
   constexpr int CE = 16 / sizeof(T);    // entries per chunk
-  const uint32_t nblocks = uint32_t((Tn + 31) / 32);
-  const bool sparse = live != nullptr && 2 * int64_t(*live) < Tn;
-  const uint32_t gi = sparse ? blockIdx.x % ngroups : blockIdx.x / nblocks;
-  const uint32_t tb = sparse ? blockIdx.x / ngroups : blockIdx.x % nblocks;
-  const int64_t t = int64_t(tb) * 32 + (threadIdx.x >> 3);
-  if (t >= Tn) return;
+  const uint32_t gi = blockIdx.x % ngroups, jb = blockIdx.x / ngroups;
+  const int64_t j = int64_t(jb) * 32 + (threadIdx.x >> 3);
+  if (j >= int64_t(*nlive)) return;
+  const int64_t t = perm[j];
   const int ch = threadIdx.x & 7;
   const int64_t yy = y[t];
   const int sh = bound != nullptr ? probs_shift(*bound) : 0;
@@ -1302,7 +1298,7 @@ __global__ __launch_bounds__(256) void k_cache_to_probs(T* __restrict__ E,
 #pragma unroll
       for (int e = 0; e < CE; ++e) vals[e] = T(float(vals[e]) * f[q]);
       __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(vals),
-                                  reinterpret_cast<u32x4*>(E + (pn * pld + t) * BV + ch * CE));
+                                  reinterpret_cast<u32x4*>(P + (pn * pld + j) * BV + ch * CE));
     }
   }
 }
@@ -1612,14 +1608,14 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   static_assert(sizeof(T) == sizeof(TP), "the operand keeps the input's element size");
   constexpr bool kScaled = !std::is_same<T, TP>::value;
   // With a softmax cache the whole vocabulary is one chunk and the operand is
-  // the cache itself, normalised in place; otherwise the logits of each chunk
-  // are recomputed.
+  // gathered from the cache; otherwise the logits of each chunk are
+  // recomputed.
   const int64_t chunk = cacheE ? Vs : bwd_chunk_cols(Tn, Vs, sizeof(T));
   const int64_t ld = int64_t(align_up(size_t(min(chunk, Vs)), 64));
   const int64_t pld = cdiv(Tn, 64) * 64;
   const int64_t nchunks = cdiv(Vs, chunk);
   Carve cv(ws);
-  TP* P = cacheE ? cacheE : cv.take<TP>(size_t(pld) * ld);
+  TP* P = cv.take<TP>(size_t(pld) * ld);
   TP* Wt = cv.take<TP>(size_t(d) * ld);    // [d x chunk] transpose of W's chunk rows
   TP* Ht = cv.take<TP>(size_t(d) * pld);   // [d x T] transpose of H
   // H with the dead tokens' rows zeroed, in the live-first order (recompute
@@ -1639,14 +1635,14 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   // magnitude bounds of the scaled operands: [0] max |dlogp|, [1] max |H|,
   // [2 + c] max |W| over chunk c
   unsigned* bounds = kScaled ? cv.take<unsigned>(size_t(2 + nchunks)) : nullptr;
-  // recompute only: the live-first token order (position -> token) and the
-  // live counts of its blocks, followed by the number of live tokens
+  // the live-first token order (position -> token) and the live counts of
+  // its blocks, followed by the number of live tokens
   const int nlb = int(cdiv(Tn, kLiveBlock));
-  int* perm = cacheE ? nullptr : cv.take<int>(Tn);
-  int* live_blk = cacheE ? nullptr : cv.take<int>(size_t(nlb) + 1);
-  const int* nlive = cacheE ? nullptr : live_blk + nlb;
+  int* perm = cv.take<int>(Tn);
+  int* live_blk = cv.take<int>(size_t(nlb) + 1);
+  const int* nlive = live_blk + nlb;
   // the gradient contractions also skip the dead tokens' MFMAs
-  const bool skip = nlive != nullptr && (flags & MC_BWD_SKIP_DEAD_TOKENS) != 0;
+  const bool skip = (flags & MC_BWD_SKIP_DEAD_TOKENS) != 0;
   int ncu = 0, dev = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -1655,7 +1651,7 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
   const int nTd = int(cdiv(d, kBN));
 
   const double es = sizeof(T);
-  if (!cacheE) {
+  {
     ProfScope ps_(s, "logprob_bwd_live_order", 0.0, 24.0 * Tn);
     hipLaunchKernelGGL(k_live_count, dim3(nlb), dim3(256), 0, s, y, dlogp, Tn, V, live_blk);
     hipLaunchKernelGGL(k_live_perm, dim3(nlb), dim3(256), 0, s, y, dlogp, Tn, V, live_blk, nlb,
@@ -1703,16 +1699,15 @@ hipError_t bwd_impl(const T* H, const T* W, const int64_t* y, const float* lse,
     const size_t wc_bytes = size_t(Vs - v0) * d * sizeof(T);
     const size_t p_bytes = size_t(pld) * ld * sizeof(TP);
     if (cacheE) {
-      // algorithmic bytes: the writes and per-token values (the reads of
-      // the live tokens' cached values depend on dlogp and are not counted)
-      ProfScope ps_(s, "logprob_bwd_cache_probs", 0.0, es * double(Tn) * ldc + 4.0 * Tn * 5);
+      // algorithmic bytes: per-token values (the live tokens' reads and
+      // writes depend on dlogp and are not counted)
+      ProfScope ps_(s, "logprob_bwd_cache_probs", 0.0, 4.0 * Tn * 6);
       const int64_t panels = ldc / (128 / int64_t(sizeof(T)));
       const int64_t groups = cdiv(panels, kCachePanels), blocks = cdiv(Tn, 32);
-      if (groups * blocks > int64_t(0x7fffffff)) return hipErrorInvalidValue;
-      // the live-token count comes with the bucketing (run when dW is wanted)
-      hipLaunchKernelGGL(k_cache_to_probs<TP>, dim3(unsigned(groups * blocks)), dim3(256), 0, s,
-                         P, cacheM, lse, dlogp, y, Tn, V, pld, panels, uint32_t(groups),
-                         dW ? counts + Vs : nullptr, bounds);
+      if (groups * blocks > int64_t(0x7fffffff) || ldc > ld) return hipErrorInvalidValue;
+      hipLaunchKernelGGL(k_cache_gather<TP>, dim3(unsigned(groups * blocks)), dim3(256), 0, s,
+                         cacheE, cacheM, lse, dlogp, y, perm, nlive, Tn, V, pld, panels,
+                         uint32_t(groups), bounds, P);
     } else {
       // tile rows: chunk columns (up to the padded width ldc), tile columns: tokens
       Operand A{Wc, d, width, d}, B{Hm, d, Tn, d};   // B: H's rows in the live-first order
@@ -1839,7 +1834,8 @@ size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   const size_t es = dt == MC_BF16 ? 2 : 4;
   const size_t ld = align_up(size_t(V), 64);
   const size_t pld = size_t(cdiv(T, 64)) * 64;
-  size_t n = align_up(size_t(d) * ld * es, kWsAlign);
+  size_t n = align_up(pld * ld * es, kWsAlign);   // the operand, gathered from the cache
+  n += align_up(size_t(d) * ld * es, kWsAlign);
   n += align_up(size_t(d) * pld * es, kWsAlign);
   n += align_up(size_t(T) * size_t(d) * es, kWsAlign);   // H with dead rows zeroed
   n += align_up(size_t(V + 1) * 4, kWsAlign) + align_up(size_t(V) * 4, kWsAlign);
@@ -1851,6 +1847,8 @@ size_t bwd_cache_workspace(int64_t T, int64_t d, int64_t V, mc_dtype_t dt) {
   n += align_up(tail_slot_floats(d, V) * 4, kWsAlign);
   n += onehot_seg_bytes(T, d);
   if (dt == MC_BF16) n += align_up(size_t(3) * 4, kWsAlign);   // bounds (one chunk)
+  n += align_up(size_t(T) * 4, kWsAlign);                         // order
+  n += align_up(size_t(cdiv(T, kLiveBlock) + 1) * 4, kWsAlign);   // its counts
   return n;
 }
 

@@ -202,7 +202,9 @@ def test_cached_argument_checks(lib):
     need_b = lib.mc_logprob_bwd_cached_workspace_size(T, d, V, BF16)
     # the cache holds the padded [T x V] exp operand and the block maxima
     assert need_c >= 64 * 128 * 2 + 16 * 4 and lib.mc_logprob_cache_size(T, 60, V, BF16) == 0
-    assert 0 < need_b < lib.mc_logprob_bwd_workspace_size(T, d, V, BF16)
+    # the cached backward's workspace holds the gathered operand like the
+    # recompute backward's (one chunk here)
+    assert 0 < need_b <= lib.mc_logprob_bwd_workspace_size(T, d, V, BF16)
     fwd = lambda cache, cb, ws=FAKE_WS, wb=need_f: lib.mc_logprob_fwd_cached(
         FAKE, FAKE, FAKE, T, d, V, BF16, FAKE, FAKE, None, cache, cb, ws, wb, None)
     assert fwd(None, need_c) == WS
@@ -215,7 +217,7 @@ def test_cached_argument_checks(lib):
     assert bwd(None, need_c) == WS
     assert bwd(FAKE_WS, 0) == WS
     assert bwd(FAKE_WS, need_c, flags=8) == INVALID
-    assert bwd(FAKE_WS, need_c, flags=4) == INVALID   # skipping is the recompute pair's only
+    assert bwd(FAKE_WS, need_c, flags=12) == INVALID   # unknown bit beside a known one
     assert bwd(FAKE_WS, need_c, dh=FAKE + 4) == INVALID
 
 

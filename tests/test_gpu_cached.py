@@ -1,8 +1,10 @@
 """GPU parity of the softmax-cache path (mc_logprob_fwd_cached /
 mc_logprob_bwd_cached): the forward keeps exp(z - block max) and the block
-maxima, the backward normalises them in place instead of recomputing the
-logits.  Compared with the fp64 oracle element by element at small and mid
-sizes, on sampled rows at full size, and with the recompute path."""
+maxima, the backward gathers the live tokens' rows of them into its operand
+instead of recomputing the logits, leaving the cache as it was.  Compared
+with the fp64 oracle element by element at small and mid sizes, on sampled
+rows at full size, and with the recompute path; several backward calls on
+one cache; MC_BWD_SKIP_DEAD_TOKENS against the call without it."""
 import numpy as np
 import pytest
 
@@ -317,3 +319,40 @@ def test_zero_dlogp_rows_and_shared_targets(path, accumulate):
     assert rel_fro(dW, dW_o) <= GRAD_RTOL
     # a token with zero dlogp has a zero gradient row exactly
     assert (dH[dl == 0] == 0).all()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_cache_serves_several_backward_calls(dtype):
+    # the backward only reads the cache: two upstream gradients (a third of
+    # the tokens dead in the second) from one forward, each against the
+    # oracle, the first repeated bit for bit after the second; and each with
+    # MC_BWD_SKIP_DEAD_TOKENS (dW bit for bit, dH up to the order of sums)
+    mc = _mc()
+    d, V = 136, 1003
+    case = small_case(scaled_config(1, d=d, V=V, dtype=dtype, seed=91))
+    H, W, y = device_tensors(case)
+    T = H.shape[0]
+    rng = np.random.default_rng(92)
+    dls = [(rng.standard_normal(T) * 1e-2).astype(np.float32) for _ in range(2)]
+    dls[1][rng.random(T) < 0.33] = 0.0
+    cache = mc.softmax_cache(H, W)
+    _, lse = mc.logprob_fwd_cached(H, W, y, cache)
+    before = cache.clone()
+    outs = [mc.logprob_bwd_cached(H, W, y, lse, torch.from_numpy(dl).cuda(), cache)
+            for dl in dls]
+    again = mc.logprob_bwd_cached(H, W, y, lse, torch.from_numpy(dls[0]).cuda(), cache)
+    skips = [mc.logprob_bwd_cached(H, W, y, lse, torch.from_numpy(dl).cuda(), cache,
+                                   skip_dead_tokens=True) for dl in dls]
+    torch.cuda.synchronize()
+    assert torch.equal(cache, before)
+    assert torch.equal(outs[0][0], again[0]) and torch.equal(outs[0][1], again[1])
+    _, lse_o = oracle.logprob_fwd(case["H"], case["W"], case["y"])
+    for dl, (dH, dW), (dHs, dWs) in zip(dls, outs, skips):
+        dH_o, dW_o = oracle.logprob_bwd(case["H"], case["W"], case["y"], lse_o,
+                                        dl.astype(np.float64))
+        assert rel_fro(dH.double().cpu().numpy(), dH_o) <= GRAD_RTOL
+        assert rel_fro(dW.double().cpu().numpy(), dW_o) <= GRAD_RTOL
+        assert torch.equal(dW, dWs)
+        assert rel_fro(dHs.double().cpu().numpy(), dH.double().cpu().numpy()) <= 1e-6
+        dead = torch.from_numpy(dl == 0.0).cuda()
+        assert not dH[dead].any() and not dHs[dead].any()
