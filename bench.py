@@ -60,33 +60,33 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "3f6074ab4812437ca04d52d2f1120b49ace3cf65d2121b6caa1776279fa27d0b",
+        "3b2d83f3cd7b19a77e14a95c76dc73257901199e4036edb0f6abdef729fc8cf7",
     "read_bytes_per_launch": {
-        "logprob_fwd_gemm": 35619319808,
-        "logprob_fwd_merge": 78110848,
+        "logprob_fwd_gemm": 36766418496,
+        "logprob_fwd_merge": 78110784,
         "logprob_bwd_live_order": 436224,
-        "logprob_bwd_live_rows": 37180160,
-        "logprob_bwd_bounds": 80576,
-        "logprob_bwd_bucket": 5801920,
-        "logprob_bwd_probs": 11017802944,
-        "logprob_bwd_transpose": 689529056,
-        "logprob_bwd_dhidden": 26520335168,
-        "logprob_bwd_dweight": 10480632704,
-        "logprob_bwd_onehot_dw": 107672640,
+        "logprob_bwd_live_rows": 37180800,
+        "logprob_bwd_bounds": 76352,
+        "logprob_bwd_bucket": 5807616,
+        "logprob_bwd_probs": 11008324544,
+        "logprob_bwd_transpose": 689528768,
+        "logprob_bwd_dhidden": 25476738304,
+        "logprob_bwd_dweight": 8967786432,
+        "logprob_bwd_onehot_dw": 107667520,
         "rl_loss": 340480,
     },
     "write_bytes_per_launch": {
-        "logprob_fwd_gemm": 78367648,
+        "logprob_fwd_gemm": 78367616,
         "logprob_fwd_merge": 131072,
         "logprob_bwd_live_order": 66912,
         "logprob_bwd_live_rows": 134217728,
         "logprob_bwd_bounds": 32,
-        "logprob_bwd_bucket": 2647488,
-        "logprob_bwd_probs": 1322486528,
+        "logprob_bwd_bucket": 2647200,
+        "logprob_bwd_probs": 1322504064,
         "logprob_bwd_transpose": 689438720,
         "logprob_bwd_dhidden": 268435456,
         "logprob_bwd_dweight": 2556428288,
-        "logprob_bwd_onehot_dw": 69889184,
+        "logprob_bwd_onehot_dw": 69888224,
         "rl_loss": 80896,
     },
 }
@@ -403,7 +403,7 @@ def summarize(path, only=None):
 
     def role(name):
         for key in ("k_fwd_logits_lse", "k_bwd_probs", "k_bwd_dhidden", "k_bwd_dweight",
-                    "k_cache_to_probs", "k_transpose", "k_onehot_seg", "k_onehot_join", "k_lse_merge",
+                    "k_cache_gather", "k_transpose", "k_onehot_seg", "k_onehot_join", "k_lse_merge",
                     "k_shard_partial", "k_dh_tail_reduce", "k_tail_reduce", "k_surrogate", "k_seq_stats",
                     "k_bucket_rank", "k_bucket_fill", "k_hist", "k_scan", "k_fill_i32", "k_bound_abs",
                     "k_live_rows", "k_live_count", "k_live_perm",
