@@ -60,33 +60,33 @@ FLUSH_BYTES = 1 << 30         # scratch write between flushed reps (> L2 + 256 M
 # with this digest (else null).
 TRAFFIC = {
     "sources_sha256":
-        "3b2d83f3cd7b19a77e14a95c76dc73257901199e4036edb0f6abdef729fc8cf7",
+        "820083f7ed703dc9d45c95f71e34b4faf478f0fbbaa2986bf6e5b92012caadf3",
     "read_bytes_per_launch": {
-        "logprob_fwd_gemm": 36766418496,
-        "logprob_fwd_merge": 78110784,
+        "logprob_fwd_gemm": 37786938368,
+        "logprob_fwd_merge": 78110848,
         "logprob_bwd_live_order": 436224,
-        "logprob_bwd_live_rows": 37180800,
-        "logprob_bwd_bounds": 76352,
-        "logprob_bwd_bucket": 5807616,
-        "logprob_bwd_probs": 11008324544,
-        "logprob_bwd_transpose": 689528768,
-        "logprob_bwd_dhidden": 25476738304,
-        "logprob_bwd_dweight": 8967786432,
-        "logprob_bwd_onehot_dw": 107667520,
+        "logprob_bwd_live_rows": 37179776,
+        "logprob_bwd_bounds": 76928,
+        "logprob_bwd_bucket": 5807040,
+        "logprob_bwd_probs": 11528877824,
+        "logprob_bwd_transpose": 689524640,
+        "logprob_bwd_dhidden": 23638051072,
+        "logprob_bwd_dweight": 9204613184,
+        "logprob_bwd_onehot_dw": 107669504,
         "rl_loss": 340480,
     },
     "write_bytes_per_launch": {
-        "logprob_fwd_gemm": 78367616,
+        "logprob_fwd_gemm": 78367680,
         "logprob_fwd_merge": 131072,
         "logprob_bwd_live_order": 66912,
         "logprob_bwd_live_rows": 134217728,
         "logprob_bwd_bounds": 32,
-        "logprob_bwd_bucket": 2647200,
-        "logprob_bwd_probs": 1322504064,
+        "logprob_bwd_bucket": 2647584,
+        "logprob_bwd_probs": 1322502784,
         "logprob_bwd_transpose": 689438720,
         "logprob_bwd_dhidden": 268435456,
         "logprob_bwd_dweight": 2556428288,
-        "logprob_bwd_onehot_dw": 69888224,
+        "logprob_bwd_onehot_dw": 69888768,
         "rl_loss": 80896,
     },
 }
