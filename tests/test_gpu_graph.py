@@ -2,9 +2,9 @@
 
 Every entry point enqueues kernels only (no memsets, no allocations, no host
 synchronisation), so the whole step — forward, RL loss, backward, through
-either pair (recompute, with or without MC_BWD_SKIP_DEAD_TOKENS, whose
-tile plans come from the live count on the device, or the softmax cache
-held outside the graph) — can
+either pair (recompute, or the softmax cache held outside the graph), with
+or without MC_BWD_SKIP_DEAD_TOKENS, whose tile plans come from the live
+count on the device — can
 be captured once and replayed.  The test replays the captured step
 several times with eager work and synchronisations in between, checks every
 replay bit for bit against the eager step on the same inputs, then changes
@@ -48,7 +48,7 @@ def _step(mc, H, W, y, lr, st, params, cache=None, skip=False):
     if cache is None:
         dH, dW = mc.logprob_bwd(H, W, y, lse, out["dlogp"], skip_dead_tokens=skip)
     else:
-        dH, dW = mc.logprob_bwd_cached(H, W, y, lse, out["dlogp"], cache)
+        dH, dW = mc.logprob_bwd_cached(H, W, y, lse, out["dlogp"], cache, skip_dead_tokens=skip)
     return dict(logp=logp, lse=lse, loss=out["loss"], dlogp=out["dlogp"],
                 seq_mask=out["seq_mask"], seq_len=out["seq_len"], n_valid=out["n_valid"],
                 error_flag=out["error_flag"], dH=dH, dW=dW)
@@ -63,7 +63,7 @@ def _same(a, b):
         assert np.array_equal(a[k], b[k], equal_nan=True), k
 
 
-@pytest.mark.parametrize("pair", ["recompute", "cached", "skip"])
+@pytest.mark.parametrize("pair", ["recompute", "cached", "skip", "cached-skip"])
 def test_step_graph_replays(pair):
     import paper_2606_04847_amd as mc
     case = _case()
@@ -73,21 +73,21 @@ def test_step_graph_replays(pair):
     st = structure_tensors(case["s"])
     lr = torch.from_numpy(o["lr"]).cuda()
     params = to_params(p)
-    cache = mc.softmax_cache(H, W) if pair == "cached" else None
+    cache = mc.softmax_cache(H, W) if pair.startswith("cached") else None
 
-    eager = _host(_step(mc, H, W, y, lr, st, params, cache, pair == "skip"))
+    eager = _host(_step(mc, H, W, y, lr, st, params, cache, pair.endswith("skip")))
     assert_step_parity(eager, o)   # the eager step itself matches the oracle
 
     # warm up on a side stream, then capture
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        _step(mc, H, W, y, lr, st, params, cache, pair == "skip")
+        _step(mc, H, W, y, lr, st, params, cache, pair.endswith("skip"))
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
-        static = _step(mc, H, W, y, lr, st, params, cache, pair == "skip")
+        static = _step(mc, H, W, y, lr, st, params, cache, pair.endswith("skip"))
     torch.cuda.synchronize()
 
     for rep in range(3):
@@ -101,7 +101,7 @@ def test_step_graph_replays(pair):
 
     # the graph reads its inputs at replay time
     H.mul_(0.5)
-    eager2 = _host(_step(mc, H, W, y, lr, st, params, cache, pair == "skip"))
+    eager2 = _host(_step(mc, H, W, y, lr, st, params, cache, pair.endswith("skip")))
     assert not np.array_equal(eager2["dW"], eager["dW"])
     graph.replay()
     torch.cuda.synchronize()
