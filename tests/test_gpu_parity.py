@@ -125,6 +125,13 @@ def test_edge_shapes_fwd_bwd(dtype, T, d, V):
     assert rel_fro(dW.cpu().numpy(), dW_o) <= GRAD_RTOL
     if T > 4:
         assert np.all(dH[1].cpu().numpy() == 0.0) and np.all(dH[3].cpu().numpy() == 0.0)
+    # the same shapes with MC_BWD_SKIP_DEAD_TOKENS (the ignored targets dead)
+    dHs, dWs = mc.logprob_bwd(Hd, Wd, yd, lse, dl, skip_dead_tokens=True)
+    torch.cuda.synchronize()
+    assert torch.equal(dWs, dW)
+    assert rel_fro(dHs.double().cpu().numpy(), dH.double().cpu().numpy()) <= 1e-6
+    if T > 4:
+        assert not dHs[1].any() and not dHs[3].any()
 
 
 def test_zero_weight_closed_form():
